@@ -1,0 +1,110 @@
+"""Seeded synthetic inputs shared by the tests, the benchmark and the smoke run.
+
+This module only draws random numbers and lays them out; it holds none of the
+attention arithmetic.  Every draw comes from numpy's counter-based Philox
+generator keyed by (seed, purpose, index...), so a tensor can be regenerated
+piecewise and identically on any host.
+
+The workloads stand in for the paper's long-context runs (LongBench, passkey,
+and the latency tables) whose data and model weights are not used here: the
+shapes follow the models the paper evaluates (Qwen2.5-7B: 28 query heads, 4 KV
+heads, d_head 128; a Llama-3.1-8B-like shape: 32 query heads, 8 KV heads,
+d_head 128), values are N(0, 1) (optionally scaled), and "needles" are planted
+keys that a retrieval head can find far from the query.
+"""
+import hashlib
+
+import numpy as np
+
+_PURPOSES = {}
+
+
+def _purpose_id(name):
+    if name not in _PURPOSES:
+        _PURPOSES[name] = int.from_bytes(hashlib.sha256(name.encode()).digest()[:4], "little")
+    return _PURPOSES[name]
+
+
+def rng(seed, purpose, *index):
+    """Philox generator for (seed, purpose, index...)."""
+    key = [int(seed) & 0xFFFFFFFF, _purpose_id(purpose)] + [int(i) & 0xFFFFFFFF for i in index]
+    while len(key) < 4:
+        key.append(0)
+    if len(key) > 4:
+        h = hashlib.sha256(np.asarray(key, dtype=np.uint64).tobytes()).digest()
+        key = list(np.frombuffer(h[:16], dtype=np.uint32))
+    k = np.asarray(key[:4], dtype=np.uint32).view(np.uint64)
+    return np.random.Generator(np.random.Philox(key=k))
+
+
+def gaussian(shape, seed, purpose, *index, scale=1.0, dtype=np.float32):
+    """N(0, scale^2) samples, float32."""
+    x = rng(seed, purpose, *index).standard_normal(size=shape, dtype=np.float32)
+    if scale != 1.0:
+        x *= np.float32(scale)
+    return x.astype(dtype, copy=False)
+
+
+def choose_streaming(n_kv_heads, n_streaming, seed, purpose="streaming", *index):
+    """0/1 mask of length n_kv_heads with n_streaming ones, seeded choice."""
+    sel = rng(seed, purpose, *index).choice(n_kv_heads, size=n_streaming, replace=False)
+    m = np.zeros(n_kv_heads, dtype=np.uint8)
+    m[sel] = 1
+    return m
+
+
+def n_streaming_for(n_kv_heads, sparsity_pct):
+    """Streaming KV heads for a target sparsity: G - ceil((1 - s) G), in exact
+    integer arithmetic on a percentage."""
+    retrieval = -(-(100 - sparsity_pct) * n_kv_heads // 100)
+    return n_kv_heads - retrieval
+
+
+def page_permutation(n_pages, seed, purpose="pages"):
+    """A seeded shuffle of physical page ids (so logical order != physical)."""
+    return rng(seed, purpose).permutation(n_pages).astype(np.int32)
+
+
+def lengths_uniform(n, lo, hi, seed, purpose="lengths"):
+    """n integer lengths drawn uniformly from [lo, hi]."""
+    return rng(seed, purpose).integers(lo, hi + 1, size=n).astype(np.int64)
+
+
+def plant_needles(k, lens, n_needles, n_sink, window_max, seed, scale=4.0):
+    """Overwrite n_needles rows per (sequence, KV head) of k [B, L, Hkv, D]
+    in place with scale * |k_row| * u, u a seeded unit direction, at positions
+    drawn from [n_sink, len - window_max) so the needles are outside every
+    streaming head's window and only retrieval heads can see them.
+    Returns the positions [B, Hkv, n_needles]."""
+    b_n, _, hkv, d = k.shape
+    pos = np.zeros((b_n, hkv, n_needles), dtype=np.int64)
+    for b in range(b_n):
+        hi = int(lens[b]) - window_max
+        if hi <= n_sink:
+            continue
+        for g in range(hkv):
+            r = rng(seed, "needle", b, g)
+            u = r.standard_normal(d).astype(np.float64)
+            u /= np.linalg.norm(u)
+            p = np.sort(r.choice(np.arange(n_sink, hi), size=n_needles, replace=False))
+            pos[b, g] = p
+            for q in p:
+                nrm = float(np.linalg.norm(k[b, q, g].astype(np.float64)))
+                k[b, q, g] = (scale * nrm * u).astype(k.dtype)
+    return pos
+
+
+# Workloads.  Sizes follow the models the paper evaluates; see the module doc.
+CONFIGS = {
+    "tiny": dict(batch=1, hq=4, hkv=2, d=64, dtype="f32", seq=256, streaming=[0, 1],
+                 n_sink=4, window=32, decode_steps=16, seed=0),
+    "qwen25_prefill_32k": dict(batch=1, hq=28, hkv=4, d=128, dtype="bf16", seq=32768,
+                               streaming=[0, 1, 0, 1], n_sink=64, window=1024, k_scale=0.5, seed=1),
+    "llama_decode_b8_128k": dict(batch=8, hq=32, hkv=8, d=128, dtype="bf16", context=131072,
+                                 n_streaming=4, n_sink=64, window=1024, page=16, steps=64, seed=2),
+    "qwen25_stack_256k": dict(layers=28, batch=1, hq=28, hkv=4, d=128, dtype="bf16", seq=262144,
+                              n_streaming=2, n_sink=64, window=2048, decode_steps=128, seed=3),
+    "varlen_sweep": dict(n_seq=16, len_lo=4096, len_hi=65536, hq=32, hkv=8, d=128, dtype="bf16",
+                         sparsity_pct=[25, 50, 75], windows=[512, 4096], n_sink=64, needles=8,
+                         decode_steps=32, seed=4),
+}
