@@ -1,0 +1,193 @@
+/*
+ * aoh.h -- C interface of libaoh: head-mixed attention for Autonomy-of-Heads
+ * (AoH) on AMD Instinct MI355X (gfx950).
+ *
+ * The method (paper: "Autonomy-of-Heads: Data-Free Sparse Attention from Frozen
+ * Query-Key Geometry") labels every KV group of a layer as a retrieval group or
+ * a streaming group (Sec. 4, group-level classification; Appendix "GQA
+ * Extension").  At inference, retrieval heads attend to the whole causal
+ * prefix and keep an O(T) KV cache; streaming heads keep only s_sink sink
+ * tokens and s_recent recent tokens (Sec. 5, decode stage and chunked-prefill
+ * stage).  The two outputs are concatenated along the head axis in the
+ * original head order (Sec. 5, Eq. 8).  This library computes that attention
+ * -- the softmax(Q K^T / sqrt(d)) V of each head under its mask -- for a batch
+ * of prefills and for single-token decode steps, and maintains the two caches.
+ *
+ * Conventions common to every call
+ *   - Q, K and V arrive after any positional encoding; no scale other than
+ *     1/sqrt(D) is applied.
+ *   - GQA: query head h reads KV head g = h / (Hq / Hkv) (contiguous groups).
+ *   - head_is_streaming is a HOST array of Hkv bytes (0 = retrieval,
+ *     1 = streaming); the label is per KV group and every query head of the
+ *     group inherits it.
+ *   - Streaming mask: key j is visible to the query at position i when
+ *     j <= i and (j < n_sink or i - j < window).  The window includes the
+ *     current token, so a streaming query sees at most n_sink + window keys.
+ *     In prefill this per-token sink + band mask is used for every row (it is
+ *     the chunk-size-independent form of the paper's chunked eviction and
+ *     equals what decode sees).  Retrieval mask: j <= i.
+ *   - Supported: dtype bf16 (fp32 accumulation and softmax) or fp32
+ *     (fp32 throughout); D in {64, 128}; Hq a multiple of Hkv with
+ *     Hq / Hkv <= 16; Hkv <= 64.  n_sink >= 0, window >= 1.
+ *   - Every device pointer is owned by the caller.  The library allocates no
+ *     device memory, performs no host<->device copy and no synchronisation in
+ *     these calls, and keeps no pointer after returning.  All work is enqueued
+ *     on `stream` (a hipStream_t; NULL = the default stream), in order.
+ *   - Errors: arguments are validated before anything is enqueued; on any
+ *     non-OK status nothing was launched and aoh_last_error() returns a
+ *     message (thread-local, valid until the next call on the same thread).
+ *     A failed launch returns AOH_ERR_HIP.  Faults inside a kernel surface at
+ *     the caller's next synchronisation.  No C++ exception crosses this
+ *     interface.
+ *   - Calls are thread-safe; calls that write the same cache or workspace
+ *     concurrently race, as any two kernels writing one buffer would.
+ */
+#ifndef AOH_H_
+#define AOH_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  AOH_OK = 0,
+  AOH_ERR_INVALID_ARG = 1, /* null pointer, inconsistent shapes, bad strides */
+  AOH_ERR_UNSUPPORTED = 2, /* valid request outside the supported set above */
+  AOH_ERR_HIP = 3,         /* a HIP runtime call or kernel launch failed */
+  AOH_ERR_WORKSPACE = 4    /* decode workspace missing or too small */
+} aoh_status;
+
+typedef enum { AOH_BF16 = 0, AOH_F32 = 1 } aoh_dtype;
+
+/* Tokens per page of the paged cache and per block of the ring cache. */
+#define AOH_PAGE_TOKENS 16
+
+/*
+ * A strided dense tensor in device memory.  Strides are in elements; the last
+ * dimension must have stride 1.  Unused trailing shape/stride entries are
+ * ignored.
+ */
+typedef struct {
+  void* data;
+  int32_t dtype; /* aoh_dtype */
+  int32_t ndim;
+  int64_t shape[4];
+  int64_t stride[4];
+} aoh_tensor;
+
+/*
+ * Paged cache of the retrieval KV heads (the paper's O(T) cache, Sec. 5).
+ * Only retrieval KV heads are stored, indexed by rank r = position of the head
+ * among the retrieval KV heads in ascending KV-head id, so resident KV shrinks
+ * with the streaming fraction.  Token p of sequence b lives in physical page
+ * block_table[b * max_pages_per_seq + p / 16], row p % 16.  Layouts
+ * (contiguous, dtype = the call's dtype):
+ *   k: [num_pages][n_heads][16][D]   token-major inside a page
+ *   v: [num_pages][n_heads][D][16]   dimension-major inside a page
+ * block_table is a DEVICE int32 array [B][max_pages_per_seq]; the caller
+ * allocates pages and fills it for every page a call touches.
+ */
+typedef struct {
+  void* k;
+  void* v;
+  const int32_t* block_table;
+  int64_t num_pages;
+  int32_t max_pages_per_seq;
+  int32_t n_heads;
+} aoh_paged_cache;
+
+/*
+ * Ring cache of the streaming KV heads: the paper's fixed sink + recent cache
+ * (Sec. 5; 128 + 256 tokens in its experiments).  capacity must equal
+ * n_sink + window; storage is padded to Cpad = capacity rounded up to a
+ * multiple of 16 slots.  Token p goes to slot p if p < n_sink, else to
+ * n_sink + (p - n_sink) % window; slot c lives in block c / 16, row c % 16.
+ * Layouts (contiguous, rank s among the streaming KV heads):
+ *   k: [B][n_heads][Cpad/16][16][D]
+ *   v: [B][n_heads][Cpad/16][D][16]
+ * After any sequence of appends each slot holds the token of greatest
+ * position that maps to it.
+ */
+typedef struct {
+  void* k;
+  void* v;
+  int32_t n_heads;
+  int32_t capacity;
+} aoh_ring_cache;
+
+/*
+ * Head-mixed causal prefill (Sec. 5 chunked-prefill stage; Appendix H2Share
+ * "Inference Phase", prefill).  For every batch b, query head h and position i
+ * of the prompt:
+ *   out[b,i,h,:] = sum_{j visible} softmax_j(q[b,i,h,:] . k[b,j,g,:] / sqrt(D)) v[b,j,g,:]
+ * with g = h / (Hq/Hkv) and the mask of g's type.
+ *   q:   [B][T][Hq][D]   k, v: [B][T][Hkv][D]   out: [B][T][Hq][D]
+ * q, k, v share one dtype; out has the same dtype, or fp32 for bf16 inputs.
+ * T may be any value >= 1 (a ragged last tile is handled); B >= 1.
+ * Streaming heads only visit the sink tiles and the diagonal band of tiles;
+ * tiles outside the mask are never loaded.
+ */
+aoh_status aoh_prefill(const aoh_tensor* q, const aoh_tensor* k, const aoh_tensor* v,
+                       const uint8_t* head_is_streaming, int32_t n_sink, int32_t window,
+                       aoh_tensor* out, void* stream);
+
+/*
+ * Append n_new tokens per sequence to the caches (Sec. 5: retrieval heads
+ * retain every token; streaming heads evict all but the sink and recent
+ * tokens).  Token t of k_new/v_new has position start_pos[b] + t.
+ *   k_new, v_new: [B][n_new][Hkv][D]; start_pos: DEVICE int32 [B] (the
+ *   sequence length before the append).
+ * Retrieval KV heads are written to kv_full, streaming KV heads to kv_ring;
+ * either cache may be NULL when no head of its type exists.  Copies are
+ * bit-exact.  The paged cache must have pages mapped for every position
+ * written.  Only the last window tokens of a bulk append (and any sink
+ * positions) are written to the ring, so the result does not depend on
+ * write order.
+ */
+aoh_status aoh_kv_append(const aoh_tensor* k_new, const aoh_tensor* v_new,
+                         const uint8_t* head_is_streaming, const int32_t* start_pos,
+                         const aoh_paged_cache* kv_full, const aoh_ring_cache* kv_ring,
+                         int32_t n_sink, int32_t window, void* stream);
+
+/*
+ * Device workspace (bytes) that aoh_decode needs for its split-K partial
+ * results, for a batch of `batch` sequences, Hq query heads of width d_head,
+ * a paged cache of max_pages_per_seq pages per sequence and a ring of
+ * ring_capacity slots.  Returns 0 for invalid arguments.
+ */
+size_t aoh_decode_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t d_head,
+                                  int32_t max_pages_per_seq, int32_t ring_capacity);
+
+/*
+ * One single-token decode step (Sec. 5 decode stage, Eq. 8): for each
+ * sequence b and query head h, with the query at position lens[b] - 1,
+ *   out[b,h,:] = Attn(q[b,h,:], cache of KV group g)
+ * where a retrieval group's cache holds tokens 0..lens[b]-1 and a streaming
+ * group's ring holds its sink and recent tokens.  The step's own K/V must have
+ * been appended already (lens counts it).
+ *   q: [B][Hq][D]; out: [B][Hq][D] (dtype of q, or fp32 for bf16 q);
+ *   lens: DEVICE int32 [B], 1 <= lens[b] <= 16 * max_pages_per_seq.
+ * The grid is sized from the cache capacity, never from lens, so the host
+ * reads nothing back and the call can be captured in a HIP graph.
+ * workspace: DEVICE buffer of at least aoh_decode_workspace_bytes(...) bytes,
+ * owned by the caller; its contents are scratch.
+ */
+aoh_status aoh_decode(const aoh_tensor* q, const aoh_paged_cache* kv_full,
+                      const aoh_ring_cache* kv_ring, const uint8_t* head_is_streaming,
+                      const int32_t* lens, int32_t n_sink, int32_t window, aoh_tensor* out,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* Message for the last non-OK status returned on this thread ("" if none). */
+const char* aoh_last_error(void);
+
+/* Interface version: 100 * major + minor. */
+int32_t aoh_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AOH_H_ */

@@ -1,0 +1,228 @@
+"""Thin ctypes binding of libaoh (include/aoh.h).
+
+Every function here only marshals arguments: torch tensors become aoh_tensor
+descriptors (pointer, dtype, shape, strides) and the call goes to the C entry
+point of the same name, on the current HIP stream.  All arithmetic runs in the
+library's HIP kernels.  If libaoh.so is missing or cannot be loaded, every call
+raises: there is no fallback path.
+
+Cache helpers allocate the two cache layouts with torch (the library itself
+never allocates device memory).
+"""
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libaoh.so")
+
+AOH_OK, AOH_ERR_INVALID_ARG, AOH_ERR_UNSUPPORTED, AOH_ERR_HIP, AOH_ERR_WORKSPACE = range(5)
+AOH_BF16, AOH_F32 = 0, 1
+PAGE_TOKENS = 16
+
+_DTYPES = {torch.bfloat16: AOH_BF16, torch.float32: AOH_F32}
+
+
+class AohError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(f"aoh status {status}: {message}")
+        self.status = status
+
+
+class AohTensor(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("dtype", ctypes.c_int32), ("ndim", ctypes.c_int32),
+                ("shape", ctypes.c_int64 * 4), ("stride", ctypes.c_int64 * 4)]
+
+
+class AohPagedCache(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("block_table", ctypes.c_void_p),
+                ("num_pages", ctypes.c_int64), ("max_pages_per_seq", ctypes.c_int32),
+                ("n_heads", ctypes.c_int32)]
+
+
+class AohRingCache(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("n_heads", ctypes.c_int32),
+                ("capacity", ctypes.c_int32)]
+
+
+_lib = None
+
+EXPORTS = ("aoh_prefill", "aoh_kv_append", "aoh_decode_workspace_bytes", "aoh_decode",
+           "aoh_last_error", "aoh_version")
+
+
+def lib():
+    """Load libaoh.so once; raise if it is not built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2608_06849_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.POINTER
+        L.aoh_prefill.argtypes = [P(AohTensor), P(AohTensor), P(AohTensor), ctypes.c_void_p,
+                                  ctypes.c_int32, ctypes.c_int32, P(AohTensor), ctypes.c_void_p]
+        L.aoh_prefill.restype = ctypes.c_int
+        L.aoh_kv_append.argtypes = [P(AohTensor), P(AohTensor), ctypes.c_void_p, ctypes.c_void_p,
+                                    P(AohPagedCache), P(AohRingCache), ctypes.c_int32, ctypes.c_int32,
+                                    ctypes.c_void_p]
+        L.aoh_kv_append.restype = ctypes.c_int
+        L.aoh_decode_workspace_bytes.argtypes = [ctypes.c_int32] * 5
+        L.aoh_decode_workspace_bytes.restype = ctypes.c_size_t
+        L.aoh_decode.argtypes = [P(AohTensor), P(AohPagedCache), P(AohRingCache), ctypes.c_void_p,
+                                 ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, P(AohTensor),
+                                 ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+        L.aoh_decode.restype = ctypes.c_int
+        L.aoh_last_error.argtypes = []
+        L.aoh_last_error.restype = ctypes.c_char_p
+        L.aoh_version.argtypes = []
+        L.aoh_version.restype = ctypes.c_int32
+        _lib = L
+    return _lib
+
+
+def _check(status):
+    if status != AOH_OK:
+        raise AohError(status, lib().aoh_last_error().decode())
+
+
+def tensor_desc(t):
+    """aoh_tensor descriptor of a torch tensor (no copy)."""
+    if t.dtype not in _DTYPES:
+        raise TypeError(f"unsupported dtype {t.dtype}")
+    if t.dim() > 4:
+        raise ValueError("at most 4 dimensions")
+    d = AohTensor()
+    d.data = t.data_ptr()
+    d.dtype = _DTYPES[t.dtype]
+    d.ndim = t.dim()
+    for i in range(t.dim()):
+        d.shape[i] = t.shape[i]
+        d.stride[i] = t.stride(i)
+    return d
+
+
+class _Mask:
+    """Host byte array of head labels, kept alive for the duration of a call."""
+
+    def __init__(self, head_is_streaming):
+        m = bytes(int(x) for x in head_is_streaming)
+        self.buf = ctypes.create_string_buffer(m, max(len(m), 1))
+
+    @property
+    def ptr(self):
+        return ctypes.cast(self.buf, ctypes.c_void_p)
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+# ----------------------------------------------------------------------------- caches
+
+class PagedCache:
+    """Retrieval-head cache: 16-token pages, K token-major and V dimension-major
+    inside a page, and a per-sequence block table (device int32)."""
+
+    def __init__(self, k, v, block_table):
+        self.k, self.v, self.block_table = k, v, block_table
+
+    @classmethod
+    def allocate(cls, num_pages, n_heads, d, dtype, block_table, device="cuda"):
+        k = torch.empty((num_pages, n_heads, PAGE_TOKENS, d), dtype=dtype, device=device)
+        v = torch.empty((num_pages, n_heads, d, PAGE_TOKENS), dtype=dtype, device=device)
+        return cls(k, v, block_table.to(device=device, dtype=torch.int32).contiguous())
+
+    def desc(self):
+        c = AohPagedCache()
+        c.k, c.v = self.k.data_ptr(), self.v.data_ptr()
+        c.block_table = self.block_table.data_ptr()
+        c.num_pages = self.k.shape[0]
+        c.max_pages_per_seq = self.block_table.shape[1]
+        c.n_heads = self.k.shape[1]
+        return c
+
+
+class RingCache:
+    """Streaming-head cache: n_sink + window slots per (sequence, head), padded
+    to whole 16-slot blocks; K token-major and V dimension-major per block."""
+
+    def __init__(self, k, v, capacity):
+        self.k, self.v, self.capacity = k, v, capacity
+
+    @classmethod
+    def allocate(cls, batch, n_heads, n_sink, window, d, dtype, device="cuda"):
+        cap = n_sink + window
+        nblk = (cap + PAGE_TOKENS - 1) // PAGE_TOKENS
+        k = torch.empty((batch, n_heads, nblk, PAGE_TOKENS, d), dtype=dtype, device=device)
+        v = torch.empty((batch, n_heads, nblk, d, PAGE_TOKENS), dtype=dtype, device=device)
+        return cls(k, v, cap)
+
+    def desc(self):
+        c = AohRingCache()
+        c.k, c.v = self.k.data_ptr(), self.v.data_ptr()
+        c.n_heads = self.k.shape[1]
+        c.capacity = self.capacity
+        return c
+
+
+# ----------------------------------------------------------------------------- entry points
+
+def aoh_prefill(q, k, v, head_is_streaming, n_sink, window, out=None, stream=None):
+    """out[B,T,Hq,D] = head-mixed causal attention (see aoh.h)."""
+    if out is None:
+        out = torch.empty_like(q)
+    qd, kd, vd, od = tensor_desc(q), tensor_desc(k), tensor_desc(v), tensor_desc(out)
+    m = _Mask(head_is_streaming)
+    _check(lib().aoh_prefill(ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), m.ptr,
+                             n_sink, window, ctypes.byref(od), _stream(stream)))
+    return out
+
+
+def aoh_kv_append(k_new, v_new, head_is_streaming, start_pos, kv_full, kv_ring, n_sink, window,
+                  stream=None):
+    """Append k_new/v_new [B,n_new,Hkv,D] at positions start_pos[b] + t."""
+    kd, vd = tensor_desc(k_new), tensor_desc(v_new)
+    fd = kv_full.desc() if kv_full is not None else None
+    rd = kv_ring.desc() if kv_ring is not None else None
+    m = _Mask(head_is_streaming)
+    _check(lib().aoh_kv_append(ctypes.byref(kd), ctypes.byref(vd), m.ptr,
+                               _ptr(start_pos), ctypes.byref(fd) if fd else None,
+                               ctypes.byref(rd) if rd else None, n_sink, window, _stream(stream)))
+
+
+def aoh_decode_workspace_bytes(batch, n_q_heads, d_head, max_pages_per_seq, ring_capacity):
+    return int(lib().aoh_decode_workspace_bytes(batch, n_q_heads, d_head, max_pages_per_seq,
+                                                ring_capacity))
+
+
+def aoh_decode(q, kv_full, kv_ring, head_is_streaming, lens, n_sink, window, out=None,
+               workspace=None, stream=None):
+    """One decode step: out[B,Hq,D] for queries at positions lens[b]-1."""
+    if out is None:
+        out = torch.empty_like(q)
+    qd, od = tensor_desc(q), tensor_desc(out)
+    fd = kv_full.desc() if kv_full is not None else None
+    rd = kv_ring.desc() if kv_ring is not None else None
+    ws_ptr, ws_bytes = (workspace.data_ptr(), workspace.numel() * workspace.element_size()) \
+        if workspace is not None else (0, 0)
+    m = _Mask(head_is_streaming)
+    _check(lib().aoh_decode(ctypes.byref(qd), ctypes.byref(fd) if fd else None,
+                            ctypes.byref(rd) if rd else None, m.ptr,
+                            _ptr(lens), n_sink, window, ctypes.byref(od), ctypes.c_void_p(ws_ptr),
+                            ws_bytes, _stream(stream)))
+    return out
+
+
+def aoh_last_error():
+    return lib().aoh_last_error().decode()
+
+
+def aoh_version():
+    return int(lib().aoh_version())

@@ -1,0 +1,396 @@
+// Host side of libaoh: argument validation, the head-scheduling pass and the
+// launch plan for every entry point of aoh.h.
+//
+// Head-scheduling pass.  The paper reorders the Q/K/V projection weights
+// offline so that retrieval and streaming heads form contiguous slices and no
+// gather is needed (Sec. 5 "Reordering"; Appendix "GQA Extension", weight
+// reordering at KV-group and query-head granularity).  Here the caller's head
+// order is kept: the pass splits the KV heads by label into two lists that
+// travel by value in the kernel arguments, and each kernel maps its work item
+// to (KV head, query head) through its list.  Outputs land in the caller's
+// head order, so the concatenation of Eq. 8 needs no copy.  Each head type
+// gets its own launch, sized for its own work: causal query blocks of the
+// retrieval launch are issued longest first; the decode cache is cut into
+// splits so each launch has enough independent waves to fill the GPU.
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <algorithm>
+#include <cmath>
+
+#include "aoh.h"
+#include "aoh_internal.h"
+
+using namespace aoh;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+aoh_status fail(aoh_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+aoh_status ok() {
+  g_err[0] = '\0';
+  return AOH_OK;
+}
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+int elt_size(int dtype) { return dtype == AOH_BF16 ? 2 : 4; }
+
+// Checks a tensor descriptor: rank, dtype, positive sizes, unit last stride,
+// positive strides, alignment of the base pointer and strides for 16-byte
+// vector access.
+aoh_status check_tensor(const aoh_tensor* t, const char* name, int ndim, int dtype_a, int dtype_b) {
+  if (!t) return fail(AOH_ERR_INVALID_ARG, "%s: null descriptor", name);
+  if (!t->data) return fail(AOH_ERR_INVALID_ARG, "%s: null data pointer", name);
+  if (t->ndim != ndim) return fail(AOH_ERR_INVALID_ARG, "%s: expected %d dimensions, got %d", name, ndim, t->ndim);
+  if (t->dtype != dtype_a && t->dtype != dtype_b)
+    return fail(AOH_ERR_UNSUPPORTED, "%s: unsupported dtype %d", name, t->dtype);
+  for (int i = 0; i < ndim; ++i) {
+    if (t->shape[i] < 1) return fail(AOH_ERR_INVALID_ARG, "%s: dimension %d has size %lld", name, i, (long long)t->shape[i]);
+    if (t->stride[i] < 1) return fail(AOH_ERR_INVALID_ARG, "%s: stride %d must be positive", name, i);
+  }
+  if (t->stride[ndim - 1] != 1) return fail(AOH_ERR_INVALID_ARG, "%s: last dimension must be contiguous", name);
+  const int64_t vec = 16 / elt_size(t->dtype);
+  if (reinterpret_cast<uintptr_t>(t->data) % 16)
+    return fail(AOH_ERR_INVALID_ARG, "%s: data pointer must be 16-byte aligned", name);
+  for (int i = 0; i < ndim - 1; ++i)
+    if (t->stride[i] % vec)
+      return fail(AOH_ERR_INVALID_ARG, "%s: stride %d must be a multiple of %lld elements", name, i, (long long)vec);
+  return AOH_OK;
+}
+
+// Head-scheduling pass: KV-head lists by label (ascending id) and each KV
+// head's rank inside its cache.
+struct HeadSchedule {
+  int n_ret = 0, n_str = 0;
+  uint8_t ret[kMaxKvHeads];
+  uint8_t str[kMaxKvHeads];
+  uint8_t rank[kMaxKvHeads];
+  uint64_t streaming_mask = 0;
+};
+
+aoh_status schedule_heads(const uint8_t* head_is_streaming, int hkv, HeadSchedule* hs) {
+  if (!head_is_streaming) return fail(AOH_ERR_INVALID_ARG, "head_is_streaming: null pointer");
+  if (hkv < 1 || hkv > kMaxKvHeads) return fail(AOH_ERR_UNSUPPORTED, "Hkv=%d outside [1, %d]", hkv, kMaxKvHeads);
+  for (int g = 0; g < hkv; ++g) {
+    const uint8_t s = head_is_streaming[g];
+    if (s > 1) return fail(AOH_ERR_INVALID_ARG, "head_is_streaming[%d]=%d is not 0/1", g, (int)s);
+    if (s) {
+      hs->rank[g] = (uint8_t)hs->n_str;
+      hs->str[hs->n_str++] = (uint8_t)g;
+      hs->streaming_mask |= (1ull << g);
+    } else {
+      hs->rank[g] = (uint8_t)hs->n_ret;
+      hs->ret[hs->n_ret++] = (uint8_t)g;
+    }
+  }
+  return AOH_OK;
+}
+
+aoh_status check_mask_params(int n_sink, int window) {
+  if (n_sink < 0) return fail(AOH_ERR_INVALID_ARG, "n_sink=%d must be >= 0", n_sink);
+  if (window < 1) return fail(AOH_ERR_INVALID_ARG, "window=%d must be >= 1", window);
+  if ((int64_t)n_sink + window > (1ll << 30)) return fail(AOH_ERR_UNSUPPORTED, "n_sink + window too large");
+  return AOH_OK;
+}
+
+// Decode split plan.  A paged split is split_blocks_full 16-token blocks
+// (even, so a wave always reads whole 32-token chunks); about 512 splits per
+// KV head over the batch keep several waves per CU in flight.  The ring is cut
+// the same way with about 64 splits per KV head over the batch.
+struct SplitPlan {
+  int split_blocks_full, n_splits_full;
+  int split_blocks_ring, n_splits_ring;
+  int ring_blocks;
+  int max_splits;
+};
+
+SplitPlan plan_splits(int batch, int max_pages, int ring_cap) {
+  SplitPlan p;
+  const int target_full = std::max(1, 512 / batch);
+  int sb = (int)std::max<int64_t>(2, ceil_div(max_pages, target_full));
+  sb += sb & 1;
+  p.split_blocks_full = sb;
+  p.n_splits_full = (int)ceil_div(max_pages, sb);
+  p.ring_blocks = (int)ceil_div(std::max(ring_cap, 1), kPageTokens);
+  const int target_ring = std::max(1, 64 / batch);
+  int sbr = (int)std::max<int64_t>(2, ceil_div(p.ring_blocks, target_ring));
+  sbr += sbr & 1;
+  p.split_blocks_ring = sbr;
+  p.n_splits_ring = (int)ceil_div(p.ring_blocks, sbr);
+  p.max_splits = std::max(p.n_splits_full, p.n_splits_ring);
+  return p;
+}
+
+size_t workspace_bytes(int batch, int hq, int d, const SplitPlan& p) {
+  const size_t slots = (size_t)batch * hq * p.max_splits;
+  const size_t acc = slots * d * sizeof(float);
+  return acc + slots * 2 * sizeof(float);
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t aoh_version(void) { return 100; }
+
+const char* aoh_last_error(void) { return g_err; }
+
+aoh_status aoh_prefill(const aoh_tensor* q, const aoh_tensor* k, const aoh_tensor* v,
+                       const uint8_t* head_is_streaming, int32_t n_sink, int32_t window,
+                       aoh_tensor* out, void* stream) {
+  aoh_status st;
+  if ((st = check_tensor(q, "q", 4, AOH_BF16, AOH_F32))) return st;
+  const int dt = q->dtype;
+  if ((st = check_tensor(k, "k", 4, dt, dt))) return st;
+  if ((st = check_tensor(v, "v", 4, dt, dt))) return st;
+  if ((st = check_tensor(out, "out", 4, dt, AOH_F32))) return st;
+  const int64_t B = q->shape[0], T = q->shape[1], Hq = q->shape[2], D = q->shape[3];
+  const int64_t Hkv = k->shape[2];
+  for (const aoh_tensor* t : {k, v})
+    if (t->shape[0] != B || t->shape[1] != T || t->shape[2] != Hkv || t->shape[3] != D)
+      return fail(AOH_ERR_INVALID_ARG, "k/v must be [B=%lld, T=%lld, Hkv, D=%lld] with equal shapes",
+                  (long long)B, (long long)T, (long long)D);
+  if (out->shape[0] != B || out->shape[1] != T || out->shape[2] != Hq || out->shape[3] != D)
+    return fail(AOH_ERR_INVALID_ARG, "out must have the shape of q");
+  if (D != 64 && D != 128) return fail(AOH_ERR_UNSUPPORTED, "D=%lld; supported: 64, 128", (long long)D);
+  if (Hq % Hkv) return fail(AOH_ERR_UNSUPPORTED, "Hq=%lld is not a multiple of Hkv=%lld", (long long)Hq, (long long)Hkv);
+  if (T > (1ll << 30)) return fail(AOH_ERR_UNSUPPORTED, "T=%lld too large", (long long)T);
+  if ((st = check_mask_params(n_sink, window))) return st;
+  HeadSchedule hs;
+  if ((st = schedule_heads(head_is_streaming, (int)Hkv, &hs))) return st;
+  const int gs = (int)(Hq / Hkv);
+  const int rows = dt == AOH_BF16 ? kPrefillRows : kPrefillRowsF32;
+  const int64_t n_qblocks = ceil_div(T, rows);
+  if (n_qblocks * Hq * B >= (1ll << 31)) return fail(AOH_ERR_UNSUPPORTED, "grid too large");
+
+  PrefillArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.q = q->data; a.k = k->data; a.v = v->data; a.out = out->data;
+  a.q_sb = q->stride[0]; a.q_st = q->stride[1]; a.q_sh = q->stride[2];
+  a.k_sb = k->stride[0]; a.k_st = k->stride[1]; a.k_sh = k->stride[2];
+  a.v_sb = v->stride[0]; a.v_st = v->stride[1]; a.v_sh = v->stride[2];
+  a.o_sb = out->stride[0]; a.o_st = out->stride[1]; a.o_sh = out->stride[2];
+  a.B = (int)B; a.T = (int)T; a.gs = gs;
+  a.n_sink = n_sink; a.window = window;
+  a.n_qblocks = (int)n_qblocks;
+  a.scale = (float)(1.0 / std::sqrt((double)D));
+  a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)D));
+  const int out_f32 = out->dtype == AOH_F32 && dt == AOH_BF16;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  // Retrieval launch first: its causal work dominates (O(T^2) vs O(T(n_sink+window))).
+  if (hs.n_ret) {
+    a.n_kv = hs.n_ret;
+    std::memcpy(a.kv_heads, hs.ret, hs.n_ret);
+    hipError_t e = launch_prefill(a, dt, out_f32, (int)D, false, s);
+    if (e != hipSuccess) return fail(AOH_ERR_HIP, "prefill retrieval launch: %s", hipGetErrorString(e));
+  }
+  if (hs.n_str) {
+    a.n_kv = hs.n_str;
+    std::memcpy(a.kv_heads, hs.str, hs.n_str);
+    hipError_t e = launch_prefill(a, dt, out_f32, (int)D, true, s);
+    if (e != hipSuccess) return fail(AOH_ERR_HIP, "prefill streaming launch: %s", hipGetErrorString(e));
+  }
+  return ok();
+}
+
+static aoh_status check_paged(const aoh_paged_cache* c, int n_ret, int64_t B) {
+  if (!n_ret) return AOH_OK;
+  if (!c) return fail(AOH_ERR_INVALID_ARG, "kv_full is null but %d retrieval heads exist", n_ret);
+  if (!c->k || !c->v || !c->block_table) return fail(AOH_ERR_INVALID_ARG, "kv_full: null pointer");
+  if (c->n_heads != n_ret)
+    return fail(AOH_ERR_INVALID_ARG, "kv_full.n_heads=%d but the mask has %d retrieval heads", c->n_heads, n_ret);
+  if (c->num_pages < 1 || c->max_pages_per_seq < 1) return fail(AOH_ERR_INVALID_ARG, "kv_full: empty cache");
+  if (c->num_pages > (1ll << 31) - 1) return fail(AOH_ERR_UNSUPPORTED, "kv_full: too many pages");
+  if ((int64_t)c->max_pages_per_seq * kPageTokens > (1ll << 30)) return fail(AOH_ERR_UNSUPPORTED, "kv_full: too many pages per sequence");
+  if (reinterpret_cast<uintptr_t>(c->k) % 16 || reinterpret_cast<uintptr_t>(c->v) % 16)
+    return fail(AOH_ERR_INVALID_ARG, "kv_full: cache pointers must be 16-byte aligned");
+  (void)B;
+  return AOH_OK;
+}
+
+static aoh_status check_ring(const aoh_ring_cache* c, int n_str, int n_sink, int window) {
+  if (!n_str) return AOH_OK;
+  if (!c) return fail(AOH_ERR_INVALID_ARG, "kv_ring is null but %d streaming heads exist", n_str);
+  if (!c->k || !c->v) return fail(AOH_ERR_INVALID_ARG, "kv_ring: null pointer");
+  if (c->n_heads != n_str)
+    return fail(AOH_ERR_INVALID_ARG, "kv_ring.n_heads=%d but the mask has %d streaming heads", c->n_heads, n_str);
+  if (c->capacity != n_sink + window)
+    return fail(AOH_ERR_INVALID_ARG, "kv_ring.capacity=%d must equal n_sink + window = %d", c->capacity, n_sink + window);
+  if (reinterpret_cast<uintptr_t>(c->k) % 16 || reinterpret_cast<uintptr_t>(c->v) % 16)
+    return fail(AOH_ERR_INVALID_ARG, "kv_ring: cache pointers must be 16-byte aligned");
+  return AOH_OK;
+}
+
+aoh_status aoh_kv_append(const aoh_tensor* k_new, const aoh_tensor* v_new,
+                         const uint8_t* head_is_streaming, const int32_t* start_pos,
+                         const aoh_paged_cache* kv_full, const aoh_ring_cache* kv_ring,
+                         int32_t n_sink, int32_t window, void* stream) {
+  aoh_status st;
+  if ((st = check_tensor(k_new, "k_new", 4, AOH_BF16, AOH_F32))) return st;
+  const int dt = k_new->dtype;
+  if ((st = check_tensor(v_new, "v_new", 4, dt, dt))) return st;
+  for (int i = 0; i < 4; ++i)
+    if (v_new->shape[i] != k_new->shape[i]) return fail(AOH_ERR_INVALID_ARG, "k_new and v_new shapes differ");
+  const int64_t B = k_new->shape[0], n_new = k_new->shape[1], Hkv = k_new->shape[2], D = k_new->shape[3];
+  if (D != 64 && D != 128) return fail(AOH_ERR_UNSUPPORTED, "D=%lld; supported: 64, 128", (long long)D);
+  if (n_new > (1ll << 30)) return fail(AOH_ERR_UNSUPPORTED, "n_new too large");
+  if (B > 65535) return fail(AOH_ERR_UNSUPPORTED, "batch too large");
+  if (!start_pos) return fail(AOH_ERR_INVALID_ARG, "start_pos: null pointer");
+  if ((st = check_mask_params(n_sink, window))) return st;
+  HeadSchedule hs;
+  if ((st = schedule_heads(head_is_streaming, (int)Hkv, &hs))) return st;
+  if ((st = check_paged(kv_full, hs.n_ret, B))) return st;
+  if ((st = check_ring(kv_ring, hs.n_str, n_sink, window))) return st;
+
+  AppendArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.k_new = k_new->data; a.v_new = v_new->data;
+  a.k_sb = k_new->stride[0]; a.k_st = k_new->stride[1]; a.k_sh = k_new->stride[2];
+  a.v_sb = v_new->stride[0]; a.v_st = v_new->stride[1]; a.v_sh = v_new->stride[2];
+  a.start_pos = start_pos;
+  a.B = (int)B; a.n_new = (int)n_new; a.Hkv = (int)Hkv;
+  if (hs.n_ret) {
+    a.pk = kv_full->k; a.pv = kv_full->v; a.block_table = kv_full->block_table;
+    a.max_pages = kv_full->max_pages_per_seq; a.num_pages = (int)kv_full->num_pages; a.n_ret = hs.n_ret;
+  }
+  if (hs.n_str) {
+    a.rk = kv_ring->k; a.rv = kv_ring->v; a.n_str = hs.n_str;
+    a.ring_blocks = (int)ceil_div(kv_ring->capacity, kPageTokens);
+  }
+  a.n_sink = n_sink; a.window = window;
+  a.n_chunks = (int)ceil_div(n_new, kPageTokens) + 1;
+  a.streaming_mask = hs.streaming_mask;
+  std::memcpy(a.rank, hs.rank, sizeof(a.rank));
+  hipError_t e = launch_append(a, dt, (int)D, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(AOH_ERR_HIP, "append launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+size_t aoh_decode_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t d_head,
+                                  int32_t max_pages_per_seq, int32_t ring_capacity) {
+  if (batch < 1 || n_q_heads < 1 || (d_head != 64 && d_head != 128) || max_pages_per_seq < 1 ||
+      ring_capacity < 0)
+    return 0;
+  return workspace_bytes(batch, n_q_heads, d_head, plan_splits(batch, max_pages_per_seq, ring_capacity));
+}
+
+aoh_status aoh_decode(const aoh_tensor* q, const aoh_paged_cache* kv_full,
+                      const aoh_ring_cache* kv_ring, const uint8_t* head_is_streaming,
+                      const int32_t* lens, int32_t n_sink, int32_t window, aoh_tensor* out,
+                      void* workspace, size_t workspace_bytes_given, void* stream) {
+  aoh_status st;
+  if ((st = check_tensor(q, "q", 3, AOH_BF16, AOH_F32))) return st;
+  const int dt = q->dtype;
+  if ((st = check_tensor(out, "out", 3, dt, AOH_F32))) return st;
+  const int64_t B = q->shape[0], Hq = q->shape[1], D = q->shape[2];
+  if (out->shape[0] != B || out->shape[1] != Hq || out->shape[2] != D)
+    return fail(AOH_ERR_INVALID_ARG, "out must have the shape of q");
+  if (D != 64 && D != 128) return fail(AOH_ERR_UNSUPPORTED, "D=%lld; supported: 64, 128", (long long)D);
+  if (!lens) return fail(AOH_ERR_INVALID_ARG, "lens: null pointer");
+  if ((st = check_mask_params(n_sink, window))) return st;
+  // The label array has one entry per KV head; its length is Hkv.  The
+  // caches tell how many heads of each type exist, so Hkv = n_ret + n_str.
+  const int n_ret_c = kv_full ? kv_full->n_heads : 0;
+  const int n_str_c = kv_ring ? kv_ring->n_heads : 0;
+  const int64_t Hkv = (int64_t)n_ret_c + n_str_c;
+  if (Hkv < 1) return fail(AOH_ERR_INVALID_ARG, "no cache given");
+  if (Hq % Hkv) return fail(AOH_ERR_UNSUPPORTED, "Hq=%lld is not a multiple of Hkv=%lld", (long long)Hq, (long long)Hkv);
+  HeadSchedule hs;
+  if ((st = schedule_heads(head_is_streaming, (int)Hkv, &hs))) return st;
+  if ((st = check_paged(kv_full, hs.n_ret, B))) return st;
+  if ((st = check_ring(kv_ring, hs.n_str, n_sink, window))) return st;
+  const int gs = (int)(Hq / Hkv);
+  if (dt == AOH_BF16 && gs > 16) return fail(AOH_ERR_UNSUPPORTED, "Hq/Hkv=%d > 16", gs);
+  const int max_pages = hs.n_ret ? kv_full->max_pages_per_seq : 1;
+  const int ring_cap = n_sink + window;
+  const SplitPlan sp = plan_splits((int)B, max_pages, ring_cap);
+
+  DecodeArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.q = q->data; a.q_sb = q->stride[0]; a.q_sh = q->stride[1];
+  a.lens = lens;
+  a.B = (int)B; a.Hq = (int)Hq; a.gs = gs;
+  a.ring_cap = ring_cap;
+  a.scale = (float)(1.0 / std::sqrt((double)D));
+  a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)D));
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+
+  if (dt == AOH_F32) {
+    // fp32: direct per-head kernel, no workspace.
+    if (hs.n_ret) {
+      DecodeArgs r = a;
+      r.kc = kv_full->k; r.vc = kv_full->v; r.block_table = kv_full->block_table;
+      r.max_pages = kv_full->max_pages_per_seq; r.num_pages = (int)kv_full->num_pages;
+      r.n_cache_heads = hs.n_ret; r.n_kv = hs.n_ret;
+      std::memcpy(r.kv_heads, hs.ret, hs.n_ret);
+      hipError_t e = launch_decode_f32(r, (int)D, false, out->data, out->stride[0], out->stride[1], s);
+      if (e != hipSuccess) return fail(AOH_ERR_HIP, "decode launch: %s", hipGetErrorString(e));
+    }
+    if (hs.n_str) {
+      DecodeArgs r = a;
+      r.kc = kv_ring->k; r.vc = kv_ring->v; r.n_cache_heads = hs.n_str; r.n_kv = hs.n_str;
+      r.ring_blocks = sp.ring_blocks;
+      std::memcpy(r.kv_heads, hs.str, hs.n_str);
+      hipError_t e = launch_decode_f32(r, (int)D, true, out->data, out->stride[0], out->stride[1], s);
+      if (e != hipSuccess) return fail(AOH_ERR_HIP, "decode launch: %s", hipGetErrorString(e));
+    }
+    return ok();
+  }
+
+  const size_t need = workspace_bytes((int)B, (int)Hq, (int)D, sp);
+  if (!workspace) return fail(AOH_ERR_WORKSPACE, "workspace is null; %zu bytes needed", need);
+  if (workspace_bytes_given < need)
+    return fail(AOH_ERR_WORKSPACE, "workspace has %zu bytes; %zu needed", workspace_bytes_given, need);
+  if (reinterpret_cast<uintptr_t>(workspace) % 16) return fail(AOH_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
+  float* part_acc = reinterpret_cast<float*>(workspace);
+  float* part_ml = part_acc + (size_t)B * Hq * sp.max_splits * D;
+  a.part_acc = part_acc; a.part_ml = part_ml; a.max_splits = sp.max_splits;
+
+  if (hs.n_ret) {
+    DecodeArgs r = a;
+    r.kc = kv_full->k; r.vc = kv_full->v; r.block_table = kv_full->block_table;
+    r.max_pages = kv_full->max_pages_per_seq; r.num_pages = (int)kv_full->num_pages;
+    r.n_cache_heads = hs.n_ret; r.n_kv = hs.n_ret;
+    r.split_blocks = sp.split_blocks_full; r.n_splits = sp.n_splits_full;
+    std::memcpy(r.kv_heads, hs.ret, hs.n_ret);
+    if ((int64_t)r.n_splits * r.n_kv * B >= (1ll << 31)) return fail(AOH_ERR_UNSUPPORTED, "grid too large");
+    hipError_t e = launch_decode_split(r, dt, (int)D, false, s);
+    if (e != hipSuccess) return fail(AOH_ERR_HIP, "decode split launch: %s", hipGetErrorString(e));
+  }
+  if (hs.n_str) {
+    DecodeArgs r = a;
+    r.kc = kv_ring->k; r.vc = kv_ring->v; r.n_cache_heads = hs.n_str; r.n_kv = hs.n_str;
+    r.ring_blocks = sp.ring_blocks;
+    r.split_blocks = sp.split_blocks_ring; r.n_splits = sp.n_splits_ring;
+    std::memcpy(r.kv_heads, hs.str, hs.n_str);
+    hipError_t e = launch_decode_split(r, dt, (int)D, true, s);
+    if (e != hipSuccess) return fail(AOH_ERR_HIP, "decode split launch: %s", hipGetErrorString(e));
+  }
+  MergeArgs m;
+  std::memset(&m, 0, sizeof(m));
+  m.part_acc = part_acc; m.part_ml = part_ml; m.lens = lens;
+  m.out = out->data; m.o_sb = out->stride[0]; m.o_sh = out->stride[1];
+  m.B = (int)B; m.Hq = (int)Hq; m.gs = gs; m.max_splits = sp.max_splits;
+  m.split_tokens_full = sp.split_blocks_full * kPageTokens;
+  m.split_tokens_ring = sp.split_blocks_ring * kPageTokens;
+  m.n_splits_full = sp.n_splits_full;
+  m.n_splits_ring = sp.n_splits_ring;
+  m.max_len = max_pages * kPageTokens;
+  m.ring_cap = ring_cap;
+  m.streaming_mask = hs.streaming_mask;
+  const int out_f32 = out->dtype == AOH_F32;
+  hipError_t e = launch_decode_merge(m, dt, out_f32, (int)D, s);
+  if (e != hipSuccess) return fail(AOH_ERR_HIP, "decode merge launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,114 @@
+// Kernel argument blocks and launchers shared by the host layer (abi.cpp) and
+// the kernel translation units.  Arguments travel by value in kernargs: the
+// head lists produced by the scheduling pass are small fixed arrays, so no
+// device memory is needed to describe a launch.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace aoh {
+
+constexpr int kMaxKvHeads = 64;
+constexpr int kPageTokens = 16;  // tokens per cache page / ring block
+
+// One prefill launch covers every query head of the KV heads in kv_heads[]
+// (all of one type).  Work item = (batch, query head, 128-row query block).
+struct PrefillArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  void* out;
+  int64_t q_sb, q_st, q_sh;
+  int64_t k_sb, k_st, k_sh;
+  int64_t v_sb, v_st, v_sh;
+  int64_t o_sb, o_st, o_sh;
+  int32_t B, T, gs;      // gs = query heads per KV head
+  int32_t n_kv;          // KV heads in this launch
+  int32_t n_sink, window;
+  int32_t n_qblocks;     // ceil(T / rows per block)
+  float scale_log2;      // log2(e) / sqrt(D)
+  float scale;           // 1 / sqrt(D)
+  uint8_t kv_heads[kMaxKvHeads];
+};
+
+// One decode split launch covers the KV heads of one cache type.
+// Work item = (batch, KV head of the list, split of split_blocks 16-token blocks).
+struct DecodeArgs {
+  const void* q;
+  int64_t q_sb, q_sh;
+  const void* kc;               // cache K base
+  const void* vc;               // cache V base
+  const int32_t* block_table;   // paged cache only (nullptr for the ring)
+  const int32_t* lens;
+  float* part_acc;              // [B][Hq][max_splits][D]
+  float* part_ml;               // [B][Hq][max_splits][2]  (m in log2 units, l)
+  int32_t max_pages;            // paged: pages per sequence row of block_table
+  int32_t num_pages;            // paged: physical pages (entries outside are never read)
+  int32_t n_cache_heads;        // heads stored in the cache (ranks)
+  int32_t ring_blocks;          // ring: Cpad / 16 (0 for the paged cache)
+  int32_t ring_cap;             // ring: n_sink + window
+  int32_t B, Hq, gs, n_kv;
+  int32_t split_blocks;         // 16-token blocks per split
+  int32_t n_splits;             // splits per (batch, KV head)
+  int32_t max_splits;
+  float scale_log2;
+  float scale;
+  uint8_t kv_heads[kMaxKvHeads];  // KV head ids; rank in the cache = index here
+};
+
+struct MergeArgs {
+  const float* part_acc;
+  const float* part_ml;
+  const int32_t* lens;
+  void* out;
+  int64_t o_sb, o_sh;
+  int32_t B, Hq, gs;
+  int32_t max_splits;
+  int32_t split_tokens_full;    // tokens per split, paged cache
+  int32_t split_tokens_ring;    // tokens per split, ring
+  int32_t n_splits_full;        // splits written per (b, head), paged cache
+  int32_t n_splits_ring;        // splits written per (b, head), ring
+  int32_t max_len;              // 16 * pages per sequence: lens are clamped to it
+  int32_t ring_cap;
+  uint64_t streaming_mask;      // bit g set = KV head g streaming
+};
+
+struct AppendArgs {
+  const void* k_new;
+  const void* v_new;
+  int64_t k_sb, k_st, k_sh;
+  int64_t v_sb, v_st, v_sh;
+  const int32_t* start_pos;
+  int32_t B, n_new, Hkv;
+  // paged cache
+  void* pk;
+  void* pv;
+  const int32_t* block_table;
+  int32_t max_pages;
+  int32_t num_pages;
+  int32_t n_ret;
+  // ring cache
+  void* rk;
+  void* rv;
+  int32_t n_str;
+  int32_t ring_blocks;
+  int32_t n_sink, window;
+  int32_t n_chunks;             // 16-position chunks launched per (b, head)
+  uint64_t streaming_mask;
+  uint8_t rank[kMaxKvHeads];    // rank of each KV head inside its cache
+};
+
+// Launchers (return the launch status; no synchronisation).
+hipError_t launch_prefill(const PrefillArgs& a, int dtype, int out_f32, int d, bool streaming,
+                          hipStream_t s);
+hipError_t launch_decode_split(const DecodeArgs& a, int dtype, int d, bool ring, hipStream_t s);
+hipError_t launch_decode_merge(const MergeArgs& a, int dtype, int out_f32, int d, hipStream_t s);
+hipError_t launch_decode_f32(const DecodeArgs& a, int d, bool ring, void* out, int64_t o_sb, int64_t o_sh,
+                             hipStream_t s);
+hipError_t launch_append(const AppendArgs& a, int dtype, int d, hipStream_t s);
+
+// Query rows per prefill workgroup (bf16 path) and per fp32 workgroup.
+constexpr int kPrefillRows = 128;
+constexpr int kPrefillRowsF32 = 64;
+
+}  // namespace aoh

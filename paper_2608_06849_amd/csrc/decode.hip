@@ -1,0 +1,341 @@
+// Single-token decode over the two caches (paper Sec. 5, decode stage, Eq. 8).
+//
+// Split-K ("flash-decoding") structure:
+//   pass 1 (decode_split): one wave per (sequence, KV head, split of the
+//     cache).  The wave reads the split's K/V once for the whole GQA group and
+//     keeps fp32 partial results (running max m, sum l, unnormalised acc[D])
+//     for every query head of the group.
+//   pass 2 (decode_merge): per (sequence, query head), log-sum-exp merge of
+//     the partials of the splits that hold tokens, normalise, store in the
+//     caller's head order.
+//
+// bf16 pass 1 works on chunks of 32 tokens = two 16-token cache blocks with
+// v_mfma_f32_16x16x32_bf16:
+//   S^T[16 tokens x 16 heads] = K[16 x 32 dims] . Q^T  (x2 token blocks, D/32 k-steps)
+//   O^T[16 dims x 16 heads]  += V^T[16 dims x 32 tokens] . P^T   (D/16 dim blocks)
+// Query heads of the group sit in the 16 MFMA columns (group size <= 16), so
+// softmax statistics are per lane column.  Lane group G = lane / 16 holds,
+// for both token blocks, chunk tokens 8G..8G+7, which makes the P^T operand
+// lane-local and lets the V^T operand be one 16-byte load from the
+// dimension-major V page ([D][16] per page).  K rows are read with 16-byte
+// loads covering 64 contiguous bytes per token row per instruction.
+#include "aoh_device.h"
+#include "aoh_internal.h"
+
+namespace aoh {
+
+template <int D, bool RING>
+__global__ __launch_bounds__(kWave) void decode_split_bf16_kernel(DecodeArgs a) {
+  constexpr int kKSteps = D / 32;   // 32-dim k-steps for Q K^T
+  constexpr int kDimBlocks = D / 16;
+  const int wg = blockIdx.x;
+  const int split = wg % a.n_splits;
+  const int rest = wg / a.n_splits;
+  const int kvl = rest % a.n_kv;
+  const int b = rest / a.n_kv;
+  const int g = a.kv_heads[kvl];
+  const int rank = kvl;
+  const int lane = threadIdx.x;
+  const int col = lane & 15;   // query head within the group (MFMA column)
+  const int G = lane >> 4;     // lane group
+
+  const int len = a.lens[b];
+  // Lengths beyond the cache capacity are clamped so no read leaves the cache.
+  const int n_valid = RING ? min(len, a.ring_cap) : min(len, a.max_pages * kPage);
+  const int n_blocks_valid = (n_valid + kPage - 1) / kPage;
+  const int blk0 = split * a.split_blocks;
+  const int blk_end = min(blk0 + a.split_blocks, n_blocks_valid);
+  if (blk0 >= blk_end) return;
+  const int tok_end = min(n_valid, blk_end * kPage);
+
+  // Q^T operand: column = query head g*gs + col (zero beyond the group).
+  const bool head_ok = col < a.gs;
+  const int hq = g * a.gs + col;
+  bf16x8 qreg[kKSteps];
+  {
+    const uint16_t* qp = reinterpret_cast<const uint16_t*>(a.q) + (int64_t)b * a.q_sb + (int64_t)hq * a.q_sh;
+#pragma unroll
+    for (int s = 0; s < kKSteps; ++s) {
+      u32x4 x = {0u, 0u, 0u, 0u};
+      if (head_ok) x = ld16(qp + 32 * s + 8 * G);
+      qreg[s] = __builtin_bit_cast(bf16x8, x);
+    }
+  }
+
+  const uint16_t* kc = reinterpret_cast<const uint16_t*>(a.kc);
+  const uint16_t* vc = reinterpret_cast<const uint16_t*>(a.vc);
+  auto block_base = [&](int blk, int64_t& kb, int64_t& vb) {
+    int64_t unit;
+    if (RING) {
+      unit = ((int64_t)b * a.n_cache_heads + rank) * a.ring_blocks + blk;
+    } else {
+      int page = a.block_table[(int64_t)b * a.max_pages + blk];
+      page = (page < 0 || page >= a.num_pages) ? 0 : page;  // invalid entry: read page 0, never outside
+      unit = (int64_t)page * a.n_cache_heads + rank;
+    }
+    kb = unit * (kPage * D);
+    vb = unit * (kPage * D);
+  };
+
+  // K row of MFMA row m = lane & 15 for token block X: chunk token
+  // 8*(m/4) + 4X + (m%4), i.e. page (m/4)/2, row 8*((m/4)%2) + 4X + (m%4).
+  const int m = lane & 15;
+  const int k_half = (m >> 2) >> 1;           // 0: first page of the chunk, 1: second
+  const int k_row0 = 8 * ((m >> 2) & 1) + (m & 3);
+  // V^T operand: dim = 16*nb + (lane & 15), tokens 8G..8G+7 of the chunk.
+  const int v_half = G >> 1;
+  const int v_off = 8 * (G & 1);
+
+  u32x4 kreg[2][kKSteps];
+  u32x4 vreg[kDimBlocks];
+  auto load_chunk = [&](int c) {
+    int64_t kbA, vbA, kbB, vbB;
+    block_base(c, kbA, vbA);
+    if (c + 1 < blk_end) {
+      block_base(c + 1, kbB, vbB);
+    } else {
+      kbB = kbA;
+      vbB = vbA;
+    }
+    const int64_t kb = k_half ? kbB : kbA;
+    const int64_t vb = v_half ? vbB : vbA;
+#pragma unroll
+    for (int X = 0; X < 2; ++X)
+#pragma unroll
+      for (int s = 0; s < kKSteps; ++s)
+        kreg[X][s] = ld16(kc + kb + (int64_t)(k_row0 + 4 * X) * D + 32 * s + 8 * G);
+#pragma unroll
+    for (int nb = 0; nb < kDimBlocks; ++nb)
+      vreg[nb] = ld16(vc + vb + (int64_t)(16 * nb + (lane & 15)) * kPage + v_off);
+  };
+
+  f32x4 acc[kDimBlocks];
+#pragma unroll
+  for (int nb = 0; nb < kDimBlocks; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY;
+  float l_run = 0.f;
+
+  load_chunk(blk0);
+  for (int c = blk0; c < blk_end; c += 2) {
+    u32x4 kcur[2][kKSteps];
+    u32x4 vcur[kDimBlocks];
+#pragma unroll
+    for (int X = 0; X < 2; ++X)
+#pragma unroll
+      for (int s = 0; s < kKSteps; ++s) kcur[X][s] = kreg[X][s];
+#pragma unroll
+    for (int nb = 0; nb < kDimBlocks; ++nb) vcur[nb] = vreg[nb];
+    if (c + 2 < blk_end) load_chunk(c + 2);
+
+    // S^T for the two 16-token blocks.
+    f32x4 sc[2];
+#pragma unroll
+    for (int X = 0; X < 2; ++X) {
+      sc[X] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < kKSteps; ++s) sc[X] = mfma16(__builtin_bit_cast(bf16x8, kcur[X][s]), qreg[s], sc[X]);
+    }
+    // This lane's 8 scores: chunk tokens 8G + j, j = 4X + i.
+    const int tok0 = c * kPage + 8 * G;
+    const bool partial = (c * kPage + 2 * kPage) > tok_end;
+    float x[8];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int X = 0; X < 2; ++X)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float v = sc[X][i] * a.scale_log2;
+        if (partial && tok0 + 4 * X + i >= tok_end) v = -INFINITY;
+        x[4 * X + i] = v;
+        mx = fmaxf(mx, v);
+      }
+    mx = wave_xor_max(mx, 16);
+    mx = wave_xor_max(mx, 32);
+    const float m_new = fmaxf(m_run, mx);  // finite: every chunk holds a valid token
+    const float alpha = fast_exp2(m_run - m_new);
+    m_run = m_new;
+    bf16x8 pop;
+    float psum = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float p = fast_exp2(x[j] - m_new);
+      psum += p;
+      pop[j] = f32_to_bf16(p);
+    }
+    l_run = l_run * alpha + psum;
+    if (partial) {
+      // Slots past the valid range may hold stale or uninitialised data: zero
+      // their V so 0 * garbage cannot poison the product.
+#pragma unroll
+      for (int nb = 0; nb < kDimBlocks; ++nb) {
+        bf16x8 vv = __builtin_bit_cast(bf16x8, vcur[nb]);
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (tok0 + j >= tok_end) vv[j] = (bf16)0.f;
+        vcur[nb] = __builtin_bit_cast(u32x4, vv);
+      }
+    }
+#pragma unroll
+    for (int nb = 0; nb < kDimBlocks; ++nb) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[nb][i] *= alpha;
+      acc[nb] = mfma16(__builtin_bit_cast(bf16x8, vcur[nb]), pop, acc[nb]);
+    }
+  }
+
+  // Partial results of this split: m (log2 units), l, acc[D] for each head.
+  float l_tot = wave_xor_sum(l_run, 16);
+  l_tot = wave_xor_sum(l_tot, 32);
+  if (head_ok) {
+    const int64_t slot = ((int64_t)b * a.Hq + hq) * a.max_splits + split;
+    float* pa = a.part_acc + slot * D;
+#pragma unroll
+    for (int nb = 0; nb < kDimBlocks; ++nb)
+      *reinterpret_cast<f32x4*>(pa + 16 * nb + 4 * G) = acc[nb];
+    if (G == 0) {
+      a.part_ml[slot * 2 + 0] = m_run;
+      a.part_ml[slot * 2 + 1] = l_tot;
+    }
+  }
+}
+
+// fp32 decode: one workgroup of 64 threads per (sequence, query head) of the
+// listed KV heads; threads stride over the valid tokens, then combine through
+// LDS.  Writes the final output directly (no split partials).
+template <int D, bool RING>
+__global__ __launch_bounds__(kWave) void decode_f32_kernel(DecodeArgs a, void* out, int64_t o_sb, int64_t o_sh) {
+#pragma clang fp contract(off)
+  __shared__ float sh_acc[kWave][D + 1];
+  __shared__ float sh_m[kWave], sh_l[kWave];
+  const int wg = blockIdx.x;
+  const int n_qh = a.n_kv * a.gs;
+  const int qhl = wg % n_qh;
+  const int b = wg / n_qh;
+  const int kvl = qhl / a.gs;
+  const int g = a.kv_heads[kvl];
+  const int hq = g * a.gs + qhl % a.gs;
+  const int t = threadIdx.x;
+  const int len = a.lens[b];
+  const int n_valid = RING ? min(len, a.ring_cap) : min(len, a.max_pages * kPage);
+  const float* qp = reinterpret_cast<const float*>(a.q) + (int64_t)b * a.q_sb + (int64_t)hq * a.q_sh;
+  const float* kc = reinterpret_cast<const float*>(a.kc);
+  const float* vc = reinterpret_cast<const float*>(a.vc);
+  float q[D], o[D];
+#pragma unroll
+  for (int d = 0; d < D; ++d) {
+    q[d] = qp[d];
+    o[d] = 0.f;
+  }
+  float mrun = -INFINITY, lrun = 0.f;
+  for (int tok = t; tok < n_valid; tok += kWave) {
+    const int blk = tok / kPage, row = tok % kPage;
+    int64_t unit;
+    if (RING) {
+      unit = ((int64_t)b * a.n_cache_heads + kvl) * a.ring_blocks + blk;
+    } else {
+      int page = a.block_table[(int64_t)b * a.max_pages + blk];
+      page = (page < 0 || page >= a.num_pages) ? 0 : page;
+      unit = (int64_t)page * a.n_cache_heads + kvl;
+    }
+    const float* kr = kc + unit * (kPage * D) + (int64_t)row * D;
+    const float* vr = vc + unit * (kPage * D) + row;
+    float s = 0.f;
+#pragma unroll
+    for (int d = 0; d < D; ++d) s = fmaf(q[d], kr[d], s);
+    s *= a.scale;
+    const float mn = fmaxf(mrun, s);
+    const float al = expf(mrun - mn);
+    const float p = expf(s - mn);
+    lrun = lrun * al + p;
+#pragma unroll
+    for (int d = 0; d < D; ++d) o[d] = o[d] * al + p * vr[(int64_t)d * kPage];
+    mrun = mn;
+  }
+  sh_m[t] = mrun;
+  sh_l[t] = lrun;
+#pragma unroll
+  for (int d = 0; d < D; ++d) sh_acc[t][d] = o[d];
+  __syncthreads();
+  float mx = -INFINITY;
+  for (int i = 0; i < kWave; ++i) mx = fmaxf(mx, sh_m[i]);
+  float L = 0.f;
+  for (int i = 0; i < kWave; ++i)
+    if (sh_m[i] != -INFINITY) L += expf(sh_m[i] - mx) * sh_l[i];
+  float* op = reinterpret_cast<float*>(out) + (int64_t)b * o_sb + (int64_t)hq * o_sh;
+  for (int d = t; d < D; d += kWave) {
+    float acc = 0.f;
+    for (int i = 0; i < kWave; ++i)
+      if (sh_m[i] != -INFINITY) acc += expf(sh_m[i] - mx) * sh_acc[i][d];
+    op[d] = acc / L;
+  }
+}
+
+template <int D, bool OUT_F32>
+__global__ __launch_bounds__(D) void decode_merge_kernel(MergeArgs a) {
+  const int wg = blockIdx.x;
+  const int hq = wg % a.Hq;
+  const int b = wg / a.Hq;
+  const int d = threadIdx.x;
+  const int g = hq / a.gs;
+  const bool streaming = (a.streaming_mask >> g) & 1ull;
+  const int len = a.lens[b];
+  const int n_valid = streaming ? min(len, a.ring_cap) : min(len, a.max_len);
+  const int split_tok = streaming ? a.split_tokens_ring : a.split_tokens_full;
+  const int ns = min((n_valid + split_tok - 1) / split_tok, streaming ? a.n_splits_ring : a.n_splits_full);
+  const int64_t base = ((int64_t)b * a.Hq + hq) * a.max_splits;
+  float mx = -INFINITY;
+  for (int s = 0; s < ns; ++s) mx = fmaxf(mx, a.part_ml[(base + s) * 2]);
+  float L = 0.f, acc = 0.f;
+  for (int s = 0; s < ns; ++s) {
+    const float w = fast_exp2(a.part_ml[(base + s) * 2] - mx);
+    L += w * a.part_ml[(base + s) * 2 + 1];
+    acc += w * a.part_acc[(base + s) * D + d];
+  }
+  const float o = acc / L;
+  if (OUT_F32) {
+    reinterpret_cast<float*>(a.out)[(int64_t)b * a.o_sb + (int64_t)hq * a.o_sh + d] = o;
+  } else {
+    reinterpret_cast<uint16_t*>(a.out)[(int64_t)b * a.o_sb + (int64_t)hq * a.o_sh + d] = f32_to_bf16_bits(o);
+  }
+}
+
+template <int D, bool RING>
+static hipError_t launch_split_bf16(const DecodeArgs& a, hipStream_t s) {
+  const int grid = a.n_splits * a.n_kv * a.B;
+  hipLaunchKernelGGL((decode_split_bf16_kernel<D, RING>), dim3(grid), dim3(kWave), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_split(const DecodeArgs& a, int dtype, int d, bool ring, hipStream_t s) {
+  (void)dtype;
+  if (d == 64) return ring ? launch_split_bf16<64, true>(a, s) : launch_split_bf16<64, false>(a, s);
+  return ring ? launch_split_bf16<128, true>(a, s) : launch_split_bf16<128, false>(a, s);
+}
+
+template <int D, bool RING>
+static hipError_t launch_f32(const DecodeArgs& a, void* out, int64_t o_sb, int64_t o_sh, hipStream_t s) {
+  const int grid = a.n_kv * a.gs * a.B;
+  hipLaunchKernelGGL((decode_f32_kernel<D, RING>), dim3(grid), dim3(kWave), 0, s, a, out, o_sb, o_sh);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_f32(const DecodeArgs& a, int d, bool ring, void* out, int64_t o_sb, int64_t o_sh,
+                             hipStream_t s) {
+  if (d == 64) return ring ? launch_f32<64, true>(a, out, o_sb, o_sh, s) : launch_f32<64, false>(a, out, o_sb, o_sh, s);
+  return ring ? launch_f32<128, true>(a, out, o_sb, o_sh, s) : launch_f32<128, false>(a, out, o_sb, o_sh, s);
+}
+
+hipError_t launch_decode_merge(const MergeArgs& a, int dtype, int out_f32, int d, hipStream_t s) {
+  (void)dtype;
+  const int grid = a.B * a.Hq;
+  if (d == 64) {
+    if (out_f32) hipLaunchKernelGGL((decode_merge_kernel<64, true>), dim3(grid), dim3(64), 0, s, a);
+    else hipLaunchKernelGGL((decode_merge_kernel<64, false>), dim3(grid), dim3(64), 0, s, a);
+  } else {
+    if (out_f32) hipLaunchKernelGGL((decode_merge_kernel<128, true>), dim3(grid), dim3(128), 0, s, a);
+    else hipLaunchKernelGGL((decode_merge_kernel<128, false>), dim3(grid), dim3(128), 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace aoh

@@ -1,0 +1,157 @@
+"""Host-side checks of the C interface: the library loads, exports every symbol
+the header declares, and rejects invalid arguments before launching anything.
+No GPU is needed: every call here fails validation, which runs on the host."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_06849_amd import aoh as A
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = 0x10000  # 16-byte aligned stand-in for a device pointer; never dereferenced
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "aoh.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(aoh_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = _declared()
+    assert set(names) == set(A.EXPORTS)
+    L = A.lib()
+    for n in names:
+        assert getattr(L, n) is not None
+
+
+def test_version():
+    assert A.aoh_version() == 100
+
+
+def _t(shape, dtype=A.AOH_BF16, data=FAKE, stride=None):
+    d = A.AohTensor()
+    d.data = data
+    d.dtype = dtype
+    d.ndim = len(shape)
+    if stride is None:
+        stride, acc = [], 1
+        for s in reversed(shape):
+            stride.insert(0, acc)
+            acc *= s
+    for i, (s, st) in enumerate(zip(shape, stride)):
+        d.shape[i] = s
+        d.stride[i] = st
+    return d
+
+
+def _prefill(q, k, v, out, mask=b"\x00\x01", n_sink=4, window=32):
+    buf = ctypes.create_string_buffer(mask, len(mask))
+    st = A.lib().aoh_prefill(ctypes.byref(q), ctypes.byref(k), ctypes.byref(v),
+                             ctypes.cast(buf, ctypes.c_void_p), n_sink, window, ctypes.byref(out), None)
+    return st, A.aoh_last_error()
+
+
+def _good():
+    return _t((1, 256, 4, 64)), _t((1, 256, 2, 64)), _t((1, 256, 2, 64)), _t((1, 256, 4, 64))
+
+
+@pytest.mark.parametrize("case,status,msg", [
+    ("null_q_data", A.AOH_ERR_INVALID_ARG, "null data"),
+    ("bad_rank", A.AOH_ERR_INVALID_ARG, "dimensions"),
+    ("bad_dtype", A.AOH_ERR_UNSUPPORTED, "dtype"),
+    ("d96", A.AOH_ERR_UNSUPPORTED, "supported: 64, 128"),
+    ("gqa", A.AOH_ERR_UNSUPPORTED, "multiple"),
+    ("window0", A.AOH_ERR_INVALID_ARG, "window"),
+    ("sink_neg", A.AOH_ERR_INVALID_ARG, "n_sink"),
+    ("mask2", A.AOH_ERR_INVALID_ARG, "not 0/1"),
+    ("misaligned", A.AOH_ERR_INVALID_ARG, "aligned"),
+    ("noncontig", A.AOH_ERR_INVALID_ARG, "contiguous"),
+    ("out_shape", A.AOH_ERR_INVALID_ARG, "shape of q"),
+    ("kv_mismatch", A.AOH_ERR_INVALID_ARG, "k/v"),
+    ("mixed_dtype", A.AOH_ERR_UNSUPPORTED, "dtype"),
+])
+def test_prefill_validation(case, status, msg):
+    q, k, v, out = _good()
+    kw = {}
+    if case == "null_q_data":
+        q.data = None
+    elif case == "bad_rank":
+        q.ndim = 3
+    elif case == "bad_dtype":
+        q.dtype = 7
+    elif case == "d96":
+        q, k, v, out = _t((1, 8, 4, 96)), _t((1, 8, 2, 96)), _t((1, 8, 2, 96)), _t((1, 8, 4, 96))
+    elif case == "gqa":
+        q, out = _t((1, 256, 3, 64)), _t((1, 256, 3, 64))
+    elif case == "window0":
+        kw["window"] = 0
+    elif case == "sink_neg":
+        kw["n_sink"] = -1
+    elif case == "mask2":
+        kw["mask"] = b"\x00\x02"
+    elif case == "misaligned":
+        q.data = FAKE + 2
+    elif case == "noncontig":
+        q = _t((1, 256, 4, 64), stride=(256 * 4 * 128, 4 * 128, 128, 2))
+    elif case == "out_shape":
+        out = _t((1, 256, 2, 64))
+    elif case == "kv_mismatch":
+        k = _t((1, 128, 2, 64))
+    elif case == "mixed_dtype":
+        k = _t((1, 256, 2, 64), dtype=A.AOH_F32)
+    st, err = _prefill(q, k, v, out, **kw)
+    assert st == status, err
+    assert msg in err
+
+
+def test_decode_workspace_size_and_checks():
+    L = A.lib()
+    n = A.aoh_decode_workspace_bytes(8, 32, 128, 8196, 1088)
+    assert n > 0 and n % 4 == 0
+    # grows with batch and heads, zero on invalid input
+    assert A.aoh_decode_workspace_bytes(8, 32, 128, 8196, 1088) >= A.aoh_decode_workspace_bytes(4, 32, 128, 8196, 1088)
+    assert A.aoh_decode_workspace_bytes(0, 32, 128, 16, 64) == 0
+    assert A.aoh_decode_workspace_bytes(1, 32, 96, 16, 64) == 0
+    # a decode call with a too-small workspace fails before launching
+    q, out = _t((2, 8, 128)), _t((2, 8, 128))
+    full = A.AohPagedCache(k=FAKE, v=FAKE, block_table=FAKE, num_pages=8, max_pages_per_seq=4, n_heads=1)
+    ring = A.AohRingCache(k=FAKE, v=FAKE, n_heads=1, capacity=4 + 32)
+    mask = ctypes.create_string_buffer(b"\x00\x01", 2)
+    need = A.aoh_decode_workspace_bytes(2, 8, 128, 4, 36)
+    st = L.aoh_decode(ctypes.byref(q), ctypes.byref(full), ctypes.byref(ring), ctypes.cast(mask, ctypes.c_void_p),
+                      ctypes.c_void_p(FAKE), 4, 32, ctypes.byref(out), ctypes.c_void_p(FAKE), need - 4, None)
+    assert st == A.AOH_ERR_WORKSPACE, A.aoh_last_error()
+    # ring capacity must equal n_sink + window
+    st = L.aoh_decode(ctypes.byref(q), ctypes.byref(full), ctypes.byref(ring), ctypes.cast(mask, ctypes.c_void_p),
+                      ctypes.c_void_p(FAKE), 4, 33, ctypes.byref(out), ctypes.c_void_p(FAKE), need, None)
+    assert st == A.AOH_ERR_INVALID_ARG and "capacity" in A.aoh_last_error()
+    # head counts of the caches must match the labels
+    full.n_heads = 2
+    st = L.aoh_decode(ctypes.byref(q), ctypes.byref(full), ctypes.byref(ring), ctypes.cast(mask, ctypes.c_void_p),
+                      ctypes.c_void_p(FAKE), 4, 32, ctypes.byref(out), ctypes.c_void_p(FAKE), need, None)
+    assert st != A.AOH_OK
+    # group size above 16 is not supported by the bf16 decode kernel
+    q2, out2 = _t((2, 34, 128)), _t((2, 34, 128))
+    full.n_heads = 1
+    st = L.aoh_decode(ctypes.byref(q2), ctypes.byref(full), ctypes.byref(ring), ctypes.cast(mask, ctypes.c_void_p),
+                      ctypes.c_void_p(FAKE), 4, 32, ctypes.byref(out2), ctypes.c_void_p(FAKE), 1 << 30, None)
+    assert st == A.AOH_ERR_UNSUPPORTED and "16" in A.aoh_last_error()
+
+
+def test_append_validation():
+    L = A.lib()
+    k, v = _t((2, 5, 2, 128)), _t((2, 5, 2, 128))
+    mask = ctypes.create_string_buffer(b"\x00\x01", 2)
+    ring = A.AohRingCache(k=FAKE, v=FAKE, n_heads=1, capacity=36)
+    # retrieval head present but no paged cache
+    st = L.aoh_kv_append(ctypes.byref(k), ctypes.byref(v), ctypes.cast(mask, ctypes.c_void_p),
+                         ctypes.c_void_p(FAKE), None, ctypes.byref(ring), 4, 32, None)
+    assert st == A.AOH_ERR_INVALID_ARG and "kv_full" in A.aoh_last_error()
+    # null start positions
+    full = A.AohPagedCache(k=FAKE, v=FAKE, block_table=FAKE, num_pages=8, max_pages_per_seq=4, n_heads=1)
+    st = L.aoh_kv_append(ctypes.byref(k), ctypes.byref(v), ctypes.cast(mask, ctypes.c_void_p),
+                         None, ctypes.byref(full), ctypes.byref(ring), 4, 32, None)
+    assert st == A.AOH_ERR_INVALID_ARG and "start_pos" in A.aoh_last_error()

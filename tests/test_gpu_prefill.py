@@ -1,0 +1,109 @@
+"""Prefill parity on the GPU: libaoh (through the C interface) against the
+float64 oracle, on seeded inputs, at sizes that span several tiles and a
+ragged tail, plus exact special cases."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import attention as OA
+from paper_2608_06849_amd import aoh_prefill
+from tests.helpers import assert_parity, bits, f64, to_dtype
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _inputs(B, T, Hq, Hkv, D, dtype, seed, k_scale=1.0):
+    q = to_dtype(synth.gaussian((B, T, Hq, D), seed, "q"), dtype).to(DEV)
+    k = to_dtype(synth.gaussian((B, T, Hkv, D), seed, "k", scale=k_scale), dtype).to(DEV)
+    v = to_dtype(synth.gaussian((B, T, Hkv, D), seed, "v"), dtype).to(DEV)
+    return q, k, v
+
+
+def test_tiny_fp32_workload():
+    # batch 1, 4 query heads over 2 KV heads, d 64, fp32, 256 tokens; KV head 1
+    # streaming with 4 sink tokens and a 32-token window
+    cfg = synth.CONFIGS["tiny"]
+    q, k, v = _inputs(1, 256, 4, 2, 64, torch.float32, cfg["seed"])
+    mask = cfg["streaming"]
+    out = aoh_prefill(q, k, v, mask, cfg["n_sink"], cfg["window"])
+    torch.cuda.synchronize()
+    want = OA.prefill(f64(q), f64(k), f64(v), mask, cfg["n_sink"], cfg["window"])
+    assert_parity(out, want, torch.float32, "tiny fp32 prefill")
+
+
+CASES = [
+    # B, T, Hq, Hkv, D, mask, n_sink, window
+    (2, 300, 8, 2, 128, [1, 0], 4, 100),      # ragged tail, GQA 4
+    (1, 513, 14, 2, 128, [0, 1], 64, 128),    # GQA 7 (Qwen-like), tile-skipping band
+    (1, 700, 4, 4, 64, [1, 0, 1, 1], 0, 1),   # d 64, window of one token, no sink
+    (1, 1, 4, 2, 128, [1, 0], 4, 32),         # single token
+    (3, 129, 8, 8, 128, [1] * 8, 130, 5),     # sink covers the sequence -> dense
+    (1, 1000, 4, 2, 128, [1, 1], 70, 200),    # sink spans two tiles, band far away
+    (1, 640, 2, 1, 64, [1], 0, 64),           # window exactly one tile
+    (1, 257, 4, 1, 128, [0], 4, 32),          # all retrieval
+]
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+@pytest.mark.parametrize("B,T,Hq,Hkv,D,mask,n_sink,window", CASES)
+def test_prefill_matches_oracle(B, T, Hq, Hkv, D, mask, n_sink, window, dtype):
+    q, k, v = _inputs(B, T, Hq, Hkv, D, dtype, seed=T * 7 + Hq)
+    out = aoh_prefill(q, k, v, mask, n_sink, window)
+    torch.cuda.synchronize()
+    want = OA.prefill(f64(q), f64(k), f64(v), mask, n_sink, window)
+    assert_parity(out, want, dtype, f"prefill {B,T,Hq,Hkv,D,mask,n_sink,window}")
+
+
+def test_prefill_fp32_output_and_strided_inputs():
+    # q, k, v as column slices of one fused [B, T, Hq + 2 Hkv, D] buffer
+    B, T, Hq, Hkv, D = 2, 333, 8, 2, 128
+    qkv = to_dtype(synth.gaussian((B, T, Hq + 2 * Hkv, D), 5, "qkv"), torch.bfloat16).to(DEV)
+    q, k, v = qkv[:, :, :Hq], qkv[:, :, Hq:Hq + Hkv], qkv[:, :, Hq + Hkv:]
+    assert not q.is_contiguous()
+    out = torch.empty((B, T, Hq, D), dtype=torch.float32, device=DEV)
+    aoh_prefill(q, k, v, [0, 1], 16, 64, out=out)
+    torch.cuda.synchronize()
+    want = OA.prefill(f64(q), f64(k), f64(v), [0, 1], 16, 64)
+    mx, _ = assert_parity(out, want, torch.bfloat16, "strided prefill, fp32 out")
+    assert mx < 5e-3  # no bf16 rounding of the output
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_window_one_returns_own_value_exactly(dtype):
+    B, T, Hq, Hkv, D = 1, 300, 4, 2, 128
+    q, k, v = _inputs(B, T, Hq, Hkv, D, dtype, seed=11)
+    out = aoh_prefill(q, k, v, [1, 1], 0, 1)
+    torch.cuda.synchronize()
+    for h in range(Hq):
+        got, want = out[:, :, h], v[:, :, h // 2]
+        if not np.array_equal(bits(got), bits(want)):
+            d = np.abs(f64(got) - f64(want))
+            bad = np.argwhere(d > 0)
+            raise AssertionError(f"head {h}: {len(bad)} elements differ, max {d.max():.3e}, first {bad[:5].tolist()}")
+
+
+def test_zero_keys_average_visible_values():
+    # K = 0: every visible key has weight exactly 1/count; V[j] = j mod 64 is
+    # exact in bf16, so with an fp32 output the only error is fp32 summation
+    B, T, Hq, Hkv, D = 1, 1000, 4, 2, 128
+    q = to_dtype(synth.gaussian((B, T, Hq, D), 3, "q"), torch.bfloat16).to(DEV)
+    k = torch.zeros((B, T, Hkv, D), dtype=torch.bfloat16, device=DEV)
+    vv = np.broadcast_to((np.arange(T) % 64).astype(np.float32)[None, :, None, None], (B, T, Hkv, D))
+    v = to_dtype(vv, torch.bfloat16).to(DEV)
+    out = torch.empty((B, T, Hq, D), dtype=torch.float32, device=DEV)
+    for n_sink, window in [(4, 32), (0, 100), (70, 64), (3, 1)]:
+        aoh_prefill(q, k, v, [0, 1], n_sink, window, out=out)
+        torch.cuda.synchronize()
+        want = OA.prefill(f64(q), f64(k), f64(v), [0, 1], n_sink, window)
+        err = np.abs(f64(out) - want).max()
+        assert err < 1e-4, (n_sink, window, err)
+
+
+def test_deterministic():
+    q, k, v = _inputs(1, 777, 8, 2, 128, torch.bfloat16, seed=9)
+    a = aoh_prefill(q, k, v, [0, 1], 4, 50)
+    b = aoh_prefill(q, k, v, [0, 1], 4, 50)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits(a), bits(b))
