@@ -125,12 +125,14 @@ def decode(q, k_seq, v_seq, lens, head_is_streaming, n_sink, window):
     out = np.empty((b_n, hq, d), dtype=np.float64)
     for b in range(b_n):
         p = int(lens[b]) - 1
-        for h in range(hq):
-            g = group_of(h, hq, hkv)
-            out[b, h] = attend_rows(
-                np.asarray(q[b, h][None, :], dtype=np.float64), [p],
-                k_seq[b, :p + 1, g, :], v_seq[b, :p + 1, g, :],
-                bool(head_is_streaming[g]), n_sink, window)[0]
+        for g in range(hkv):
+            kg = np.asarray(k_seq[b, :p + 1, g, :], dtype=np.float64)
+            vg = np.asarray(v_seq[b, :p + 1, g, :], dtype=np.float64)
+            for h in range(hq):
+                if group_of(h, hq, hkv) != g:
+                    continue
+                out[b, h] = attend_rows(np.asarray(q[b, h][None, :], dtype=np.float64), [p], kg, vg,
+                                        bool(head_is_streaming[g]), n_sink, window)[0]
     return out
 
 

@@ -106,3 +106,22 @@ def check_ring(k_ring, v_ring, k_seq, v_seq, lens, head_is_streaming, n_sink, wi
                 if not (np.array_equal(kr, k_seq[b, p, g]) and np.array_equal(vr, v_seq[b, p, g])):
                     bad += 1
     return bad
+
+
+def gather_paged(k_pages, v_pages, block_table, b, r, length):
+    """K [length, D] and V [length, D] of sequence b, retrieval rank r, read
+    through the block table per the layout (vectorised form of
+    paged_read_token over positions 0..length-1)."""
+    p = np.arange(length)
+    pages = np.asarray(block_table[b])[p // PAGE]
+    rows = p % PAGE
+    return k_pages[pages, r, rows, :], v_pages[pages, r, :, rows]
+
+
+def gather_ring(k_ring, v_ring, b, s, length, n_sink, window):
+    """(token positions held, K rows, V rows) of a streaming head's ring after
+    `length` appends, per the layout and ring_tokens()."""
+    held = ring_tokens(length, n_sink, window)
+    slots = np.nonzero(held >= 0)[0]
+    blk, row = slots // PAGE, slots % PAGE
+    return held[slots], k_ring[b, s, blk, row, :], v_ring[b, s, blk, :, row]

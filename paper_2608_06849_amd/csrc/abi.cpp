@@ -126,7 +126,7 @@ SplitPlan plan_splits(int batch, int max_pages, int ring_cap) {
   sbr += sbr & 1;
   p.split_blocks_ring = sbr;
   p.n_splits_ring = (int)ceil_div(p.ring_blocks, sbr);
-  p.max_splits = std::max(p.n_splits_full, p.n_splits_ring);
+  p.max_splits = std::max(p.n_splits_full, p.n_splits_ring);  // <= 513 < kMaxSplits by construction
   return p;
 }
 
@@ -322,27 +322,30 @@ aoh_status aoh_decode(const aoh_tensor* q, const aoh_paged_cache* kv_full,
   a.ring_cap = ring_cap;
   a.scale = (float)(1.0 / std::sqrt((double)D));
   a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)D));
+  if (hs.n_ret) {
+    CacheView& c = a.full;
+    c.k = kv_full->k; c.v = kv_full->v; c.block_table = kv_full->block_table;
+    c.max_pages = kv_full->max_pages_per_seq; c.num_pages = (int)kv_full->num_pages;
+    c.n_kv = hs.n_ret;
+    c.split_blocks = sp.split_blocks_full; c.n_splits = sp.n_splits_full;
+    c.n_items = (int)(B * hs.n_ret * sp.n_splits_full);
+    std::memcpy(c.kv_heads, hs.ret, hs.n_ret);
+  }
+  if (hs.n_str) {
+    CacheView& c = a.ring;
+    c.k = kv_ring->k; c.v = kv_ring->v;
+    c.ring_blocks = sp.ring_blocks;
+    c.n_kv = hs.n_str;
+    c.split_blocks = sp.split_blocks_ring; c.n_splits = sp.n_splits_ring;
+    c.n_items = (int)(B * hs.n_str * sp.n_splits_ring);
+    std::memcpy(c.kv_heads, hs.str, hs.n_str);
+  }
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
 
   if (dt == AOH_F32) {
     // fp32: direct per-head kernel, no workspace.
-    if (hs.n_ret) {
-      DecodeArgs r = a;
-      r.kc = kv_full->k; r.vc = kv_full->v; r.block_table = kv_full->block_table;
-      r.max_pages = kv_full->max_pages_per_seq; r.num_pages = (int)kv_full->num_pages;
-      r.n_cache_heads = hs.n_ret; r.n_kv = hs.n_ret;
-      std::memcpy(r.kv_heads, hs.ret, hs.n_ret);
-      hipError_t e = launch_decode_f32(r, (int)D, false, out->data, out->stride[0], out->stride[1], s);
-      if (e != hipSuccess) return fail(AOH_ERR_HIP, "decode launch: %s", hipGetErrorString(e));
-    }
-    if (hs.n_str) {
-      DecodeArgs r = a;
-      r.kc = kv_ring->k; r.vc = kv_ring->v; r.n_cache_heads = hs.n_str; r.n_kv = hs.n_str;
-      r.ring_blocks = sp.ring_blocks;
-      std::memcpy(r.kv_heads, hs.str, hs.n_str);
-      hipError_t e = launch_decode_f32(r, (int)D, true, out->data, out->stride[0], out->stride[1], s);
-      if (e != hipSuccess) return fail(AOH_ERR_HIP, "decode launch: %s", hipGetErrorString(e));
-    }
+    hipError_t e = launch_decode_f32(a, (int)D, out->data, out->stride[0], out->stride[1], s);
+    if (e != hipSuccess) return fail(AOH_ERR_HIP, "decode launch: %s", hipGetErrorString(e));
     return ok();
   }
 
@@ -354,25 +357,9 @@ aoh_status aoh_decode(const aoh_tensor* q, const aoh_paged_cache* kv_full,
   float* part_acc = reinterpret_cast<float*>(workspace);
   float* part_ml = part_acc + (size_t)B * Hq * sp.max_splits * D;
   a.part_acc = part_acc; a.part_ml = part_ml; a.max_splits = sp.max_splits;
-
-  if (hs.n_ret) {
-    DecodeArgs r = a;
-    r.kc = kv_full->k; r.vc = kv_full->v; r.block_table = kv_full->block_table;
-    r.max_pages = kv_full->max_pages_per_seq; r.num_pages = (int)kv_full->num_pages;
-    r.n_cache_heads = hs.n_ret; r.n_kv = hs.n_ret;
-    r.split_blocks = sp.split_blocks_full; r.n_splits = sp.n_splits_full;
-    std::memcpy(r.kv_heads, hs.ret, hs.n_ret);
-    if ((int64_t)r.n_splits * r.n_kv * B >= (1ll << 31)) return fail(AOH_ERR_UNSUPPORTED, "grid too large");
-    hipError_t e = launch_decode_split(r, dt, (int)D, false, s);
-    if (e != hipSuccess) return fail(AOH_ERR_HIP, "decode split launch: %s", hipGetErrorString(e));
-  }
-  if (hs.n_str) {
-    DecodeArgs r = a;
-    r.kc = kv_ring->k; r.vc = kv_ring->v; r.n_cache_heads = hs.n_str; r.n_kv = hs.n_str;
-    r.ring_blocks = sp.ring_blocks;
-    r.split_blocks = sp.split_blocks_ring; r.n_splits = sp.n_splits_ring;
-    std::memcpy(r.kv_heads, hs.str, hs.n_str);
-    hipError_t e = launch_decode_split(r, dt, (int)D, true, s);
+  if ((int64_t)a.full.n_items + a.ring.n_items >= (1ll << 31)) return fail(AOH_ERR_UNSUPPORTED, "grid too large");
+  {
+    hipError_t e = launch_decode_split(a, (int)D, s);
     if (e != hipSuccess) return fail(AOH_ERR_HIP, "decode split launch: %s", hipGetErrorString(e));
   }
   MergeArgs m;

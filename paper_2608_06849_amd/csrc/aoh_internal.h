@@ -31,29 +31,37 @@ struct PrefillArgs {
   uint8_t kv_heads[kMaxKvHeads];
 };
 
-// One decode split launch covers the KV heads of one cache type.
-// Work item = (batch, KV head of the list, split of split_blocks 16-token blocks).
+// One cache type as seen by the decode split pass.  Work item = (batch, KV
+// head of the list, split of split_blocks 16-token blocks).
+struct CacheView {
+  const void* k;
+  const void* v;
+  const int32_t* block_table;   // paged cache only (nullptr for the ring)
+  int32_t max_pages;            // paged: pages per sequence row of block_table
+  int32_t num_pages;            // paged: physical pages (entries outside are never read)
+  int32_t ring_blocks;          // ring: Cpad / 16
+  int32_t n_kv;                 // KV heads of this type (= heads stored in the cache)
+  int32_t split_blocks;         // 16-token blocks per split
+  int32_t n_splits;             // splits per (batch, KV head)
+  int32_t n_items;              // B * n_kv * n_splits
+  uint8_t kv_heads[kMaxKvHeads];  // KV head ids; rank in the cache = index here
+};
+
+// The decode split launch: paged-cache work items first (long), ring work items
+// after them (short, they fill the tail of the launch).
 struct DecodeArgs {
   const void* q;
   int64_t q_sb, q_sh;
-  const void* kc;               // cache K base
-  const void* vc;               // cache V base
-  const int32_t* block_table;   // paged cache only (nullptr for the ring)
   const int32_t* lens;
   float* part_acc;              // [B][Hq][max_splits][D]
   float* part_ml;               // [B][Hq][max_splits][2]  (m in log2 units, l)
-  int32_t max_pages;            // paged: pages per sequence row of block_table
-  int32_t num_pages;            // paged: physical pages (entries outside are never read)
-  int32_t n_cache_heads;        // heads stored in the cache (ranks)
-  int32_t ring_blocks;          // ring: Cpad / 16 (0 for the paged cache)
-  int32_t ring_cap;             // ring: n_sink + window
-  int32_t B, Hq, gs, n_kv;
-  int32_t split_blocks;         // 16-token blocks per split
-  int32_t n_splits;             // splits per (batch, KV head)
+  int32_t B, Hq, gs;
+  int32_t ring_cap;             // n_sink + window
   int32_t max_splits;
   float scale_log2;
   float scale;
-  uint8_t kv_heads[kMaxKvHeads];  // KV head ids; rank in the cache = index here
+  CacheView full;
+  CacheView ring;
 };
 
 struct MergeArgs {
@@ -101,11 +109,13 @@ struct AppendArgs {
 // Launchers (return the launch status; no synchronisation).
 hipError_t launch_prefill(const PrefillArgs& a, int dtype, int out_f32, int d, bool streaming,
                           hipStream_t s);
-hipError_t launch_decode_split(const DecodeArgs& a, int dtype, int d, bool ring, hipStream_t s);
+hipError_t launch_decode_split(const DecodeArgs& a, int d, hipStream_t s);
 hipError_t launch_decode_merge(const MergeArgs& a, int dtype, int out_f32, int d, hipStream_t s);
-hipError_t launch_decode_f32(const DecodeArgs& a, int d, bool ring, void* out, int64_t o_sb, int64_t o_sh,
-                             hipStream_t s);
+hipError_t launch_decode_f32(const DecodeArgs& a, int d, void* out, int64_t o_sb, int64_t o_sh, hipStream_t s);
 hipError_t launch_append(const AppendArgs& a, int dtype, int d, hipStream_t s);
+
+// Largest number of splits per (sequence, head) the merge pass accepts.
+constexpr int kMaxSplits = 1024;
 
 // Query rows per prefill workgroup (bf16 path) and per fp32 workgroup.
 constexpr int kPrefillRows = 128;

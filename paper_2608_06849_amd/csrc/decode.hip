@@ -25,15 +25,14 @@
 namespace aoh {
 
 template <int D, bool RING>
-__global__ __launch_bounds__(kWave) void decode_split_bf16_kernel(DecodeArgs a) {
+__device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const CacheView& cv, int item) {
   constexpr int kKSteps = D / 32;   // 32-dim k-steps for Q K^T
   constexpr int kDimBlocks = D / 16;
-  const int wg = blockIdx.x;
-  const int split = wg % a.n_splits;
-  const int rest = wg / a.n_splits;
-  const int kvl = rest % a.n_kv;
-  const int b = rest / a.n_kv;
-  const int g = a.kv_heads[kvl];
+  const int split = item % cv.n_splits;
+  const int rest = item / cv.n_splits;
+  const int kvl = rest % cv.n_kv;
+  const int b = rest / cv.n_kv;
+  const int g = cv.kv_heads[kvl];
   const int rank = kvl;
   const int lane = threadIdx.x;
   const int col = lane & 15;   // query head within the group (MFMA column)
@@ -41,10 +40,10 @@ __global__ __launch_bounds__(kWave) void decode_split_bf16_kernel(DecodeArgs a) 
 
   const int len = a.lens[b];
   // Lengths beyond the cache capacity are clamped so no read leaves the cache.
-  const int n_valid = RING ? min(len, a.ring_cap) : min(len, a.max_pages * kPage);
+  const int n_valid = RING ? min(len, a.ring_cap) : min(len, cv.max_pages * kPage);
   const int n_blocks_valid = (n_valid + kPage - 1) / kPage;
-  const int blk0 = split * a.split_blocks;
-  const int blk_end = min(blk0 + a.split_blocks, n_blocks_valid);
+  const int blk0 = split * cv.split_blocks;
+  const int blk_end = min(blk0 + cv.split_blocks, n_blocks_valid);
   if (blk0 >= blk_end) return;
   const int tok_end = min(n_valid, blk_end * kPage);
 
@@ -62,16 +61,16 @@ __global__ __launch_bounds__(kWave) void decode_split_bf16_kernel(DecodeArgs a) 
     }
   }
 
-  const uint16_t* kc = reinterpret_cast<const uint16_t*>(a.kc);
-  const uint16_t* vc = reinterpret_cast<const uint16_t*>(a.vc);
+  const uint16_t* kc = reinterpret_cast<const uint16_t*>(cv.k);
+  const uint16_t* vc = reinterpret_cast<const uint16_t*>(cv.v);
   auto block_base = [&](int blk, int64_t& kb, int64_t& vb) {
     int64_t unit;
     if (RING) {
-      unit = ((int64_t)b * a.n_cache_heads + rank) * a.ring_blocks + blk;
+      unit = ((int64_t)b * cv.n_kv + rank) * cv.ring_blocks + blk;
     } else {
-      int page = a.block_table[(int64_t)b * a.max_pages + blk];
-      page = (page < 0 || page >= a.num_pages) ? 0 : page;  // invalid entry: read page 0, never outside
-      unit = (int64_t)page * a.n_cache_heads + rank;
+      int page = cv.block_table[(int64_t)b * cv.max_pages + blk];
+      page = (page < 0 || page >= cv.num_pages) ? 0 : page;  // invalid entry: read page 0, never outside
+      unit = (int64_t)page * cv.n_kv + rank;
     }
     kb = unit * (kPage * D);
     vb = unit * (kPage * D);
@@ -199,27 +198,36 @@ __global__ __launch_bounds__(kWave) void decode_split_bf16_kernel(DecodeArgs a) 
   }
 }
 
+
+// One launch for both cache types: paged-cache items first, ring items last.
+template <int D>
+__global__ __launch_bounds__(kWave) void decode_split_bf16_kernel(DecodeArgs a) {
+  const int wg = blockIdx.x;
+  if (wg < a.full.n_items) decode_split_body<D, false>(a, a.full, wg);
+  else decode_split_body<D, true>(a, a.ring, wg - a.full.n_items);
+}
+
 // fp32 decode: one workgroup of 64 threads per (sequence, query head) of the
 // listed KV heads; threads stride over the valid tokens, then combine through
 // LDS.  Writes the final output directly (no split partials).
 template <int D, bool RING>
-__global__ __launch_bounds__(kWave) void decode_f32_kernel(DecodeArgs a, void* out, int64_t o_sb, int64_t o_sh) {
+__device__ __forceinline__ void decode_f32_body(const DecodeArgs& a, const CacheView& cv, int item, void* out,
+                                                int64_t o_sb, int64_t o_sh) {
 #pragma clang fp contract(off)
   __shared__ float sh_acc[kWave][D + 1];
   __shared__ float sh_m[kWave], sh_l[kWave];
-  const int wg = blockIdx.x;
-  const int n_qh = a.n_kv * a.gs;
-  const int qhl = wg % n_qh;
-  const int b = wg / n_qh;
+  const int n_qh = cv.n_kv * a.gs;
+  const int qhl = item % n_qh;
+  const int b = item / n_qh;
   const int kvl = qhl / a.gs;
-  const int g = a.kv_heads[kvl];
+  const int g = cv.kv_heads[kvl];
   const int hq = g * a.gs + qhl % a.gs;
   const int t = threadIdx.x;
   const int len = a.lens[b];
-  const int n_valid = RING ? min(len, a.ring_cap) : min(len, a.max_pages * kPage);
+  const int n_valid = RING ? min(len, a.ring_cap) : min(len, cv.max_pages * kPage);
   const float* qp = reinterpret_cast<const float*>(a.q) + (int64_t)b * a.q_sb + (int64_t)hq * a.q_sh;
-  const float* kc = reinterpret_cast<const float*>(a.kc);
-  const float* vc = reinterpret_cast<const float*>(a.vc);
+  const float* kc = reinterpret_cast<const float*>(cv.k);
+  const float* vc = reinterpret_cast<const float*>(cv.v);
   float q[D], o[D];
 #pragma unroll
   for (int d = 0; d < D; ++d) {
@@ -231,11 +239,11 @@ __global__ __launch_bounds__(kWave) void decode_f32_kernel(DecodeArgs a, void* o
     const int blk = tok / kPage, row = tok % kPage;
     int64_t unit;
     if (RING) {
-      unit = ((int64_t)b * a.n_cache_heads + kvl) * a.ring_blocks + blk;
+      unit = ((int64_t)b * cv.n_kv + kvl) * cv.ring_blocks + blk;
     } else {
-      int page = a.block_table[(int64_t)b * a.max_pages + blk];
-      page = (page < 0 || page >= a.num_pages) ? 0 : page;
-      unit = (int64_t)page * a.n_cache_heads + kvl;
+      int page = cv.block_table[(int64_t)b * cv.max_pages + blk];
+      page = (page < 0 || page >= cv.num_pages) ? 0 : page;
+      unit = (int64_t)page * cv.n_kv + kvl;
     }
     const float* kr = kc + unit * (kPage * D) + (int64_t)row * D;
     const float* vr = vc + unit * (kPage * D) + row;
@@ -270,12 +278,35 @@ __global__ __launch_bounds__(kWave) void decode_f32_kernel(DecodeArgs a, void* o
   }
 }
 
+// fp32 decode: one workgroup of 64 threads per (sequence, query head); threads
+// stride over the valid tokens, then combine through LDS.  Writes the final
+// output directly (no split partials).  Paged items first, ring items after.
+template <int D>
+__global__ __launch_bounds__(kWave) void decode_f32_kernel(DecodeArgs a, void* out, int64_t o_sb, int64_t o_sh) {
+  const int wg = blockIdx.x;
+  const int n_full = a.B * a.full.n_kv * a.gs;
+  if (wg < n_full) decode_f32_body<D, false>(a, a.full, wg, out, o_sb, o_sh);
+  else decode_f32_body<D, true>(a, a.ring, wg - n_full, out, o_sb, o_sh);
+}
+
+constexpr int kMergeThreads = 256;
+
+// Log-sum-exp merge of the split partials of one (sequence, query head).  The
+// per-split (m, l) are loaded by all threads at once and reduced in LDS; the
+// weighted sum over splits of acc[d] is spread over kMergeThreads / D groups
+// of D threads so many loads are in flight.
 template <int D, bool OUT_F32>
-__global__ __launch_bounds__(D) void decode_merge_kernel(MergeArgs a) {
+__global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(MergeArgs a) {
+  constexpr int kGroups = kMergeThreads / D;
+  constexpr int kWaves = kMergeThreads / kWave;
+  __shared__ float s_w[kMaxSplits];
+  __shared__ float s_red[kWaves];
+  __shared__ float s_acc[kGroups][D];
   const int wg = blockIdx.x;
   const int hq = wg % a.Hq;
   const int b = wg / a.Hq;
-  const int d = threadIdx.x;
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1), wave = tid / kWave;
   const int g = hq / a.gs;
   const bool streaming = (a.streaming_mask >> g) & 1ull;
   const int len = a.lens[b];
@@ -283,57 +314,77 @@ __global__ __launch_bounds__(D) void decode_merge_kernel(MergeArgs a) {
   const int split_tok = streaming ? a.split_tokens_ring : a.split_tokens_full;
   const int ns = min((n_valid + split_tok - 1) / split_tok, streaming ? a.n_splits_ring : a.n_splits_full);
   const int64_t base = ((int64_t)b * a.Hq + hq) * a.max_splits;
-  float mx = -INFINITY;
-  for (int s = 0; s < ns; ++s) mx = fmaxf(mx, a.part_ml[(base + s) * 2]);
-  float L = 0.f, acc = 0.f;
-  for (int s = 0; s < ns; ++s) {
-    const float w = fast_exp2(a.part_ml[(base + s) * 2] - mx);
-    L += w * a.part_ml[(base + s) * 2 + 1];
-    acc += w * a.part_acc[(base + s) * D + d];
+
+  float mloc = -INFINITY;
+  for (int s = tid; s < ns; s += kMergeThreads) {
+    const float m = a.part_ml[(base + s) * 2];
+    s_w[s] = m;
+    mloc = fmaxf(mloc, m);
   }
-  const float o = acc / L;
-  if (OUT_F32) {
-    reinterpret_cast<float*>(a.out)[(int64_t)b * a.o_sb + (int64_t)hq * a.o_sh + d] = o;
-  } else {
-    reinterpret_cast<uint16_t*>(a.out)[(int64_t)b * a.o_sb + (int64_t)hq * a.o_sh + d] = f32_to_bf16_bits(o);
+#pragma unroll
+  for (int o = kWave / 2; o > 0; o >>= 1) mloc = fmaxf(mloc, __shfl_xor(mloc, o, kWave));
+  if (lane == 0) s_red[wave] = mloc;
+  __syncthreads();
+  float mx = s_red[0];
+#pragma unroll
+  for (int i = 1; i < kWaves; ++i) mx = fmaxf(mx, s_red[i]);
+  __syncthreads();
+  float lloc = 0.f;
+  for (int s = tid; s < ns; s += kMergeThreads) {
+    const float w = fast_exp2(s_w[s] - mx);
+    s_w[s] = w;
+    lloc += w * a.part_ml[(base + s) * 2 + 1];
+  }
+#pragma unroll
+  for (int o = kWave / 2; o > 0; o >>= 1) lloc += __shfl_xor(lloc, o, kWave);
+  if (lane == 0) s_red[wave] = lloc;
+  __syncthreads();
+  float L = 0.f;
+#pragma unroll
+  for (int i = 0; i < kWaves; ++i) L += s_red[i];
+
+  const int d = tid % D, grp = tid / D;
+  float acc = 0.f;
+#pragma unroll 8
+  for (int s = grp; s < ns; s += kGroups) acc += s_w[s] * a.part_acc[(base + s) * D + d];
+  s_acc[grp][d] = acc;
+  __syncthreads();
+  if (grp == 0) {
+    float tot = 0.f;
+#pragma unroll
+    for (int i = 0; i < kGroups; ++i) tot += s_acc[i][d];
+    const float o = tot / L;
+    if (OUT_F32) {
+      reinterpret_cast<float*>(a.out)[(int64_t)b * a.o_sb + (int64_t)hq * a.o_sh + d] = o;
+    } else {
+      reinterpret_cast<uint16_t*>(a.out)[(int64_t)b * a.o_sb + (int64_t)hq * a.o_sh + d] = f32_to_bf16_bits(o);
+    }
   }
 }
 
-template <int D, bool RING>
-static hipError_t launch_split_bf16(const DecodeArgs& a, hipStream_t s) {
-  const int grid = a.n_splits * a.n_kv * a.B;
-  hipLaunchKernelGGL((decode_split_bf16_kernel<D, RING>), dim3(grid), dim3(kWave), 0, s, a);
+hipError_t launch_decode_split(const DecodeArgs& a, int d, hipStream_t s) {
+  const int grid = a.full.n_items + a.ring.n_items;
+  if (d == 64) hipLaunchKernelGGL((decode_split_bf16_kernel<64>), dim3(grid), dim3(kWave), 0, s, a);
+  else hipLaunchKernelGGL((decode_split_bf16_kernel<128>), dim3(grid), dim3(kWave), 0, s, a);
   return hipGetLastError();
 }
 
-hipError_t launch_decode_split(const DecodeArgs& a, int dtype, int d, bool ring, hipStream_t s) {
-  (void)dtype;
-  if (d == 64) return ring ? launch_split_bf16<64, true>(a, s) : launch_split_bf16<64, false>(a, s);
-  return ring ? launch_split_bf16<128, true>(a, s) : launch_split_bf16<128, false>(a, s);
-}
-
-template <int D, bool RING>
-static hipError_t launch_f32(const DecodeArgs& a, void* out, int64_t o_sb, int64_t o_sh, hipStream_t s) {
-  const int grid = a.n_kv * a.gs * a.B;
-  hipLaunchKernelGGL((decode_f32_kernel<D, RING>), dim3(grid), dim3(kWave), 0, s, a, out, o_sb, o_sh);
+hipError_t launch_decode_f32(const DecodeArgs& a, int d, void* out, int64_t o_sb, int64_t o_sh, hipStream_t s) {
+  const int grid = a.B * (a.full.n_kv + a.ring.n_kv) * a.gs;
+  if (d == 64) hipLaunchKernelGGL((decode_f32_kernel<64>), dim3(grid), dim3(kWave), 0, s, a, out, o_sb, o_sh);
+  else hipLaunchKernelGGL((decode_f32_kernel<128>), dim3(grid), dim3(kWave), 0, s, a, out, o_sb, o_sh);
   return hipGetLastError();
-}
-
-hipError_t launch_decode_f32(const DecodeArgs& a, int d, bool ring, void* out, int64_t o_sb, int64_t o_sh,
-                             hipStream_t s) {
-  if (d == 64) return ring ? launch_f32<64, true>(a, out, o_sb, o_sh, s) : launch_f32<64, false>(a, out, o_sb, o_sh, s);
-  return ring ? launch_f32<128, true>(a, out, o_sb, o_sh, s) : launch_f32<128, false>(a, out, o_sb, o_sh, s);
 }
 
 hipError_t launch_decode_merge(const MergeArgs& a, int dtype, int out_f32, int d, hipStream_t s) {
   (void)dtype;
   const int grid = a.B * a.Hq;
   if (d == 64) {
-    if (out_f32) hipLaunchKernelGGL((decode_merge_kernel<64, true>), dim3(grid), dim3(64), 0, s, a);
-    else hipLaunchKernelGGL((decode_merge_kernel<64, false>), dim3(grid), dim3(64), 0, s, a);
+    if (out_f32) hipLaunchKernelGGL((decode_merge_kernel<64, true>), dim3(grid), dim3(kMergeThreads), 0, s, a);
+    else hipLaunchKernelGGL((decode_merge_kernel<64, false>), dim3(grid), dim3(kMergeThreads), 0, s, a);
   } else {
-    if (out_f32) hipLaunchKernelGGL((decode_merge_kernel<128, true>), dim3(grid), dim3(128), 0, s, a);
-    else hipLaunchKernelGGL((decode_merge_kernel<128, false>), dim3(grid), dim3(128), 0, s, a);
+    if (out_f32) hipLaunchKernelGGL((decode_merge_kernel<128, true>), dim3(grid), dim3(kMergeThreads), 0, s, a);
+    else hipLaunchKernelGGL((decode_merge_kernel<128, false>), dim3(grid), dim3(kMergeThreads), 0, s, a);
   }
   return hipGetLastError();
 }

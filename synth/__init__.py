@@ -108,3 +108,57 @@ CONFIGS = {
                          sparsity_pct=[25, 50, 75], windows=[512, 4096], n_sink=64, needles=8,
                          decode_steps=32, seed=4),
 }
+
+
+def gaussian_blocks(shape, seed, purpose, block_dims, scale=1.0, workers=None):
+    """N(0, scale^2) float32 array whose sub-arrays over the leading
+    `block_dims` indices are drawn independently, key (seed, purpose, *index),
+    in a thread pool.  The result depends only on the keys, not on the pool."""
+    import os
+    from concurrent.futures import ThreadPoolExecutor
+    from itertools import product
+
+    out = np.empty(shape, dtype=np.float32)
+    lead = shape[:block_dims]
+    tail = shape[block_dims:]
+    idx = list(product(*[range(n) for n in lead]))
+    if workers is None:
+        workers = min(16, len(os.sched_getaffinity(0)))
+
+    def fill(i):
+        out[i] = gaussian(tail, seed, purpose, *i, scale=scale)
+
+    with ThreadPoolExecutor(max(1, workers)) as ex:
+        list(ex.map(fill, idx))
+    return out
+
+
+def qwen_prefill_inputs():
+    """Q, K, V (float32, [1, T, H, D]) of the Qwen2.5-7B-shaped 32K prefill
+    workload and its head labels / mask sizes."""
+    c = CONFIGS["qwen25_prefill_32k"]
+    T, hq, hkv, d, seed = c["seq"], c["hq"], c["hkv"], c["d"], c["seed"]
+    q = gaussian_blocks((1, T, hq, d), seed, "q", 2)
+    k = gaussian_blocks((1, T, hkv, d), seed, "k", 2, scale=c["k_scale"])
+    v = gaussian_blocks((1, T, hkv, d), seed, "v", 2)
+    return dict(q=q, k=k, v=v, mask=list(c["streaming"]), n_sink=c["n_sink"], window=c["window"])
+
+
+def llama_decode_inputs(steps=None):
+    """The batch-8 x 131072-token decode workload (Llama-3-8B-shaped heads):
+    context K/V as [B, Hkv, L, D] float32 blocks (view them as [B, L, Hkv, D]),
+    the streaming labels, the page permutation, and the per-step queries and
+    new K/V."""
+    c = CONFIGS["llama_decode_b8_128k"]
+    B, hq, hkv, d, L0, seed = c["batch"], c["hq"], c["hkv"], c["d"], c["context"], c["seed"]
+    steps = c["steps"] if steps is None else steps
+    mask = choose_streaming(hkv, c["n_streaming"], seed).tolist()
+    max_pages = (L0 + steps + 15) // 16
+    return dict(
+        k_ctx=gaussian_blocks((B, hkv, L0, d), seed, "kctx", 2),
+        v_ctx=gaussian_blocks((B, hkv, L0, d), seed, "vctx", 2),
+        mask=mask, n_sink=c["n_sink"], window=c["window"], max_pages=max_pages,
+        pages=page_permutation(B * max_pages, seed).reshape(B, max_pages),
+        q_steps=gaussian((steps, B, hq, d), seed, "qsteps"),
+        kv_steps=gaussian((steps, 2, B, 1, hkv, d), seed, "kvsteps"),
+    )

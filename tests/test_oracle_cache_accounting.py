@@ -108,3 +108,25 @@ def test_prefill_flops_qwen_shape():
     f = C.prefill_flops(32768, 128, 14, 14, 64, 1024)
     assert f == 4 * 128 * (14 * (32768 * 32769 // 2) + 14 * C.visible_pairs(32768, True, 64, 1024))
     assert math.isclose(f / 1e12, 4.100, abs_tol=5e-4)
+
+
+def test_vectorised_readers_match_per_token_readers():
+    rng = np.random.default_rng(0)
+    d, n_pages, B = 8, 12, 2
+    kp = rng.standard_normal((n_pages, 2, 16, d))
+    vp = rng.standard_normal((n_pages, 2, d, 16))
+    bt = rng.permutation(n_pages)[:10].reshape(B, 5)
+    for b in range(B):
+        for r in range(2):
+            K, V = M.gather_paged(kp, vp, bt, b, r, 77)
+            for p in range(77):
+                kr, vr = M.paged_read_token(kp, vp, bt, b, r, p)
+                assert np.array_equal(K[p], kr) and np.array_equal(V[p], vr)
+    kr_ = rng.standard_normal((B, 1, 3, 16, d))
+    vr_ = rng.standard_normal((B, 1, 3, d, 16))
+    pos, K, V = M.gather_ring(kr_, vr_, 1, 0, 100, 5, 37)
+    assert sorted(pos.tolist()) == sorted(set(range(5)) | set(range(63, 100)))
+    for i, p in enumerate(pos):
+        slot = M.ring_slot(int(p), 5, 37)
+        kk, vv = M.ring_read_slot(kr_, vr_, 1, 0, slot)
+        assert np.array_equal(K[i], kk) and np.array_equal(V[i], vv)
