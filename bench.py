@@ -226,7 +226,7 @@ def main():
             "frac_of_bf16_peak": round(flops_step / (prefill_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         },
         "roofline": {
-            "kernel": "prefill_bf16_kernel<128,retrieval> (14 q heads x 256 query blocks)",
+            "kernel": f"prefill_bf16_kernel<128,retrieval> ({gs * n_ret} q heads x {T} rows)",
             "bound": "mfma", "achieved": round(ret_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
             "frac": round(ret_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
             "algorithmic_per_launch": f"{flops_ret:.4e} FLOP", "avg_launch_ms": round(ret_ms, 4),

@@ -21,23 +21,37 @@
 //
 // fp32 kernel: a plain per-row kernel (one thread per query row) kept exact
 // for fp32 inputs; it has no performance role.
+#include <type_traits>
+
 #include "aoh_device.h"
 #include "aoh_internal.h"
 
 namespace aoh {
 
 constexpr int kBN = 64;          // keys per tile
-constexpr int kWaves = 4;        // waves per workgroup
+constexpr int kWaves = kPrefillWaves;  // waves per workgroup
 constexpr int kRowsPerWave = 32;
 
+#ifndef AOH_PREFILL_V_PAD
+#define AOH_PREFILL_V_PAD 32
+#endif
 template <int D>
 struct PrefillLds {
-  static constexpr int kStride = D + 8;  // bf16 elements per LDS row (16 B pad)
-  uint16_t k[kBN][kStride];
-  uint16_t v[kBN][kStride];
+  // Row paddings (bf16 elements): K rows are read 16 bytes per lane down 32
+  // rows; V rows are read by the transpose read as 4 rows x 32 bytes per
+  // 16 lanes.  Each padding spreads its access pattern over distinct banks.
+  static constexpr int kStrideK = D + 8;
+  static constexpr int kStrideV = D + AOH_PREFILL_V_PAD;
+  uint16_t k[kBN][kStrideK];
+  uint16_t v[kBN][kStrideV];
 };
 
-// Tile visit plan of one 128-row query block [i0, i0 + 128).
+// Lazy rescaling threshold (log2 units): the running max used for the
+// exponentials is only raised when a row's true max exceeds it by more than
+// this, so P stays below 2^8 and the O rescale is skipped on most tiles.
+constexpr float kRescaleThreshold = 8.0f;
+
+// Tile visit plan of one query block [i0, i0 + kPrefillRows).
 struct TilePlan {
   int n_sink_tiles;  // leading sink tiles visited before the band
   int band_first;    // first band tile
@@ -113,7 +127,7 @@ __global__ __launch_bounds__(kWaves * kWave, 2) void prefill_bf16_kernel(Prefill
   for (int mb = 0; mb < kMBlocks; ++mb)
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc_o[mb][i] = 0.f;
-  float m_run = -INFINITY;  // running max (log2 domain) of this lane's row
+  float m_run = -INFINITY;  // reference max (log2 units) of this lane's row
   float l_run = 0.f;        // this lane's partial row sum (partner lane has the rest)
 
   const TilePlan plan = make_plan<STREAM>(i0, kPrefillRows, T, a.n_sink, a.window);
@@ -147,6 +161,85 @@ __global__ __launch_bounds__(kWaves * kWave, 2) void prefill_bf16_kernel(Prefill
     }
   };
 
+  const float c = a.scale_log2;
+  // One 64-key tile for this wave: S^T, online softmax, O^T += V^T P^T.
+  // MASKED selects the per-element mask; full tiles carry no mask code.
+  auto tile_step = [&](int kb, auto masked) {
+    constexpr bool MASKED = decltype(masked)::value;
+    f32x16 s_acc[2];
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) s_acc[blk][i] = 0.f;
+#pragma unroll
+      for (int s = 0; s < kKSteps; ++s) {
+        const bf16x8 kop = *reinterpret_cast<const bf16x8*>(&lds.k[32 * blk + l32][8 * h2 + 16 * s]);
+        s_acc[blk] = mfma32(kop, qreg[s], s_acc[blk]);
+      }
+    }
+    // Mask (raw scores), row max of the raw scores.
+    float mx = -INFINITY;
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        float x = s_acc[blk][i];
+        if (MASKED) {
+          const int key = kb + 32 * blk + 8 * (i >> 2) + 4 * h2 + (i & 3);
+          bool vis = key <= my_row;
+          if (STREAM) vis = vis && (key < a.n_sink || my_row - key < a.window);
+          x = vis ? x : -INFINITY;
+          s_acc[blk][i] = x;
+        }
+        mx = fmaxf(mx, x);
+      }
+    mx = wave_xor_max(mx, 32) * c;  // log2 units (c > 0 keeps the order)
+    // Raise the reference max only when some row needs it (wave-uniform).
+    if (__any(mx > m_run + kRescaleThreshold)) {
+      const float m_new = fmaxf(m_run, mx);
+      // 0 when only m_run is -inf; 1 when the row has seen no visible key yet.
+      const float alpha = (m_new == -INFINITY) ? 1.f : fast_exp2(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int mb = 0; mb < kMBlocks; ++mb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc_o[mb][i] *= alpha;
+    }
+    const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
+    float psum = 0.f;
+    bf16x8 pop[4];  // P^T operands for the 4 key steps of 16 keys
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float p = fast_exp2(fmaf(s_acc[blk][i], c, -m_use));
+        psum += p;
+        pop[blk * 2 + (i >> 3)][i & 7] = f32_to_bf16(p);
+      }
+    l_run += psum;
+
+    // O^T += V^T . P^T.  Key step t covers keys 16t..16t+15; the k index
+    // 8*h2 + j maps to key 16t + 4*h2 + j (j < 4) or 16t + 8 + 4*h2 + (j-4).
+    const int q16 = lane >> 4;        // 16-lane block
+    const int i16 = lane & 15;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int vrow = 16 * t + 4 * h2 + (i16 >> 2);
+#pragma unroll
+      for (int mb = 0; mb < kMBlocks; ++mb) {
+        const int vcol = 32 * mb + 16 * (q16 & 1) + 4 * (i16 & 3);
+        const i16x4 lo = lds_read_tr16(&lds.v[vrow][vcol]);
+        const i16x4 hi = lds_read_tr16(&lds.v[vrow + 8][vcol]);
+        // Whole-vector concatenation: per-element bf16 insertion of the
+        // transposed halves is avoided on purpose (it was lowered to a
+        // broadcast of the first element by this toolchain).
+        const i16x8 cat = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        acc_o[mb] = mfma32(__builtin_bit_cast(bf16x8, cat), pop[t], acc_o[mb]);
+      }
+    }
+  };
+
   if (plan.n_visit > 0) load_tile(plan.tile(0) * kBN);
 
   for (int it = 0; it < plan.n_visit; ++it) {
@@ -162,74 +255,8 @@ __global__ __launch_bounds__(kWaves * kWave, 2) void prefill_bf16_kernel(Prefill
       const bool need_mask = (kb + kBN - 1 > r0) ||
                              (STREAM && !(kb + kBN - 1 < a.n_sink ||
                                           (r0 + kRowsPerWave - 1) - kb < a.window));
-      // S^T = K_tile . Q^T, two 32-key blocks.
-      f32x16 s_acc[2];
-#pragma unroll
-      for (int blk = 0; blk < 2; ++blk) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) s_acc[blk][i] = 0.f;
-#pragma unroll
-        for (int s = 0; s < kKSteps; ++s) {
-          const bf16x8 kop = *reinterpret_cast<const bf16x8*>(&lds.k[32 * blk + l32][8 * h2 + 16 * s]);
-          s_acc[blk] = mfma32(kop, qreg[s], s_acc[blk]);
-        }
-      }
-      // Scale, mask, running max.
-      float mx = -INFINITY;
-#pragma unroll
-      for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          float x = s_acc[blk][i] * a.scale_log2;
-          if (need_mask) {
-            const int key = kb + 32 * blk + 8 * (i >> 2) + 4 * h2 + (i & 3);
-            bool vis = key <= my_row;
-            if (STREAM) vis = vis && (key < a.n_sink || my_row - key < a.window);
-            x = vis ? x : -INFINITY;
-          }
-          s_acc[blk][i] = x;
-          mx = fmaxf(mx, x);
-        }
-      mx = wave_xor_max(mx, 32);
-      const float m_new = fmaxf(m_run, mx);
-      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-      const float alpha = fast_exp2(m_run - m_use);
-      m_run = m_new;
-      float psum = 0.f;
-      bf16x8 pop[4];  // P^T operands for the 4 key steps of 16 keys
-#pragma unroll
-      for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const float p = fast_exp2(s_acc[blk][i] - m_use);
-          psum += p;
-          pop[blk * 2 + (i >> 3)][i & 7] = f32_to_bf16(p);
-        }
-      l_run = l_run * alpha + psum;
-#pragma unroll
-      for (int mb = 0; mb < kMBlocks; ++mb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) acc_o[mb][i] *= alpha;
-
-      // O^T += V^T . P^T.  Key step t covers keys 16t..16t+15; the k index
-      // 8*h2 + j maps to key 16t + 4*h2 + j (j < 4) or 16t + 8 + 4*h2 + (j-4).
-      const int q16 = lane >> 4;        // 16-lane block
-      const int i16 = lane & 15;
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int vrow = 16 * t + 4 * h2 + (i16 >> 2);
-#pragma unroll
-        for (int mb = 0; mb < kMBlocks; ++mb) {
-          const int vcol = 32 * mb + 16 * (q16 & 1) + 4 * (i16 & 3);
-          const i16x4 lo = lds_read_tr16(&lds.v[vrow][vcol]);
-          const i16x4 hi = lds_read_tr16(&lds.v[vrow + 8][vcol]);
-          // Whole-vector concatenation: per-element bf16 insertion of the
-          // transposed halves is avoided on purpose (it was lowered to a
-          // broadcast of the first element by this toolchain).
-          const i16x8 cat = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-          acc_o[mb] = mfma32(__builtin_bit_cast(bf16x8, cat), pop[t], acc_o[mb]);
-        }
-      }
+      if (need_mask) tile_step(kb, std::true_type{});
+      else tile_step(kb, std::false_type{});
     }
     __syncthreads();
   }
