@@ -70,20 +70,21 @@ def lengths_uniform(n, lo, hi, seed, purpose="lengths"):
     return rng(seed, purpose).integers(lo, hi + 1, size=n).astype(np.int64)
 
 
-def plant_needles(k, lens, n_needles, n_sink, window_max, seed, scale=4.0):
+def plant_needles(k, lens, n_needles, n_sink, window_max, seed, scale=4.0, seq_ids=None):
     """Overwrite n_needles rows per (sequence, KV head) of k [B, L, Hkv, D]
     in place with scale * |k_row| * u, u a seeded unit direction, at positions
     drawn from [n_sink, len - window_max) so the needles are outside every
     streaming head's window and only retrieval heads can see them.
     Returns the positions [B, Hkv, n_needles]."""
     b_n, _, hkv, d = k.shape
+    seq_ids = list(range(b_n)) if seq_ids is None else list(seq_ids)
     pos = np.zeros((b_n, hkv, n_needles), dtype=np.int64)
     for b in range(b_n):
         hi = int(lens[b]) - window_max
         if hi <= n_sink:
             continue
         for g in range(hkv):
-            r = rng(seed, "needle", b, g)
+            r = rng(seed, "needle", seq_ids[b], g)
             u = r.standard_normal(d).astype(np.float64)
             u /= np.linalg.norm(u)
             p = np.sort(r.choice(np.arange(n_sink, hi), size=n_needles, replace=False))
@@ -133,14 +134,21 @@ def gaussian_blocks(shape, seed, purpose, block_dims, scale=1.0, workers=None):
     return out
 
 
+def gaussian_bthd(B, T, H, D, seed, purpose, scale=1.0):
+    """N(0, scale^2) float32 [B, T, H, D] (contiguous), drawn as independent
+    [T, D] blocks per (batch, head) keyed (seed, purpose, b, h)."""
+    x = gaussian_blocks((B, H, T, D), seed, purpose, 2, scale=scale)
+    return np.ascontiguousarray(x.transpose(0, 2, 1, 3))
+
+
 def qwen_prefill_inputs():
     """Q, K, V (float32, [1, T, H, D]) of the Qwen2.5-7B-shaped 32K prefill
     workload and its head labels / mask sizes."""
     c = CONFIGS["qwen25_prefill_32k"]
     T, hq, hkv, d, seed = c["seq"], c["hq"], c["hkv"], c["d"], c["seed"]
-    q = gaussian_blocks((1, T, hq, d), seed, "q", 2)
-    k = gaussian_blocks((1, T, hkv, d), seed, "k", 2, scale=c["k_scale"])
-    v = gaussian_blocks((1, T, hkv, d), seed, "v", 2)
+    q = gaussian_bthd(1, T, hq, d, seed, "q")
+    k = gaussian_bthd(1, T, hkv, d, seed, "k", scale=c["k_scale"])
+    v = gaussian_bthd(1, T, hkv, d, seed, "v")
     return dict(q=q, k=k, v=v, mask=list(c["streaming"]), n_sink=c["n_sink"], window=c["window"])
 
 
@@ -162,3 +170,38 @@ def llama_decode_inputs(steps=None):
         q_steps=gaussian((steps, B, hq, d), seed, "qsteps"),
         kv_steps=gaussian((steps, 2, B, 1, hkv, d), seed, "kvsteps"),
     )
+
+
+def stack_layer_inputs(layer):
+    """Q, K, V (float32, [1, T, H, D]) and head labels of one layer of the
+    28-layer Qwen2.5-7B-shaped 262144-token stack; every layer is regenerated
+    from (seed, layer)."""
+    c = CONFIGS["qwen25_stack_256k"]
+    T, hq, hkv, d, seed = c["seq"], c["hq"], c["hkv"], c["d"], c["seed"]
+    return dict(
+        q=gaussian_bthd(1, T, hq, d, seed * 1000 + layer, "q"),
+        k=gaussian_bthd(1, T, hkv, d, seed * 1000 + layer, "k"),
+        v=gaussian_bthd(1, T, hkv, d, seed * 1000 + layer, "v"),
+        mask=choose_streaming(hkv, c["n_streaming"], seed, "streaming", layer).tolist(),
+    )
+
+
+def stack_decode_inputs(layer, steps):
+    """Per-step query and new K/V of one stack layer: q [steps, 1, Hq, D],
+    kv [steps, 2, 1, 1, Hkv, D]."""
+    c = CONFIGS["qwen25_stack_256k"]
+    seed = c["seed"] * 1000 + layer
+    return (gaussian((steps, 1, c["hq"], c["d"]), seed, "qdec"),
+            gaussian((steps, 2, 1, 1, c["hkv"], c["d"]), seed, "kvdec"))
+
+
+def sweep_sequence(b, length):
+    """Q, K, V (float32 [1, len, H, D]) of sequence b of the variable-length
+    sweep, with 8 needles planted in K (outside every window of the sweep)."""
+    c = CONFIGS["varlen_sweep"]
+    hq, hkv, d, seed = c["hq"], c["hkv"], c["d"], c["seed"]
+    q = gaussian_bthd(1, length, hq, d, seed * 1000 + b, "q")
+    k = gaussian_bthd(1, length, hkv, d, seed * 1000 + b, "k")
+    v = gaussian_bthd(1, length, hkv, d, seed * 1000 + b, "v")
+    needles = plant_needles(k, [length], c["needles"], c["n_sink"], max(c["windows"]), seed, seq_ids=[b])
+    return dict(q=q, k=k, v=v, needles=needles[0])
