@@ -113,9 +113,13 @@ struct SplitPlan {
   int max_splits;
 };
 
+#ifndef AOH_DECODE_SPLIT_TARGET
+#define AOH_DECODE_SPLIT_TARGET 512
+#endif
+
 SplitPlan plan_splits(int batch, int max_pages, int ring_cap) {
   SplitPlan p;
-  const int target_full = std::max(1, 512 / batch);
+  const int target_full = std::max(1, AOH_DECODE_SPLIT_TARGET / batch);
   int sb = (int)std::max<int64_t>(2, ceil_div(max_pages, target_full));
   sb += sb & 1;
   p.split_blocks_full = sb;

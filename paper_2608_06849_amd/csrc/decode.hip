@@ -102,10 +102,10 @@ __device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const Cac
     for (int X = 0; X < 2; ++X)
 #pragma unroll
       for (int s = 0; s < kKSteps; ++s)
-        kreg[X][s] = ld16(kc + kb + (int64_t)(k_row0 + 4 * X) * D + 32 * s + 8 * G);
+        kreg[X][s] = ld16_stream(kc + kb + (int64_t)(k_row0 + 4 * X) * D + 32 * s + 8 * G);
 #pragma unroll
     for (int nb = 0; nb < kDimBlocks; ++nb)
-      vreg[nb] = ld16(vc + vb + (int64_t)(16 * nb + (lane & 15)) * kPage + v_off);
+      vreg[nb] = ld16_stream(vc + vb + (int64_t)(16 * nb + (lane & 15)) * kPage + v_off);
   };
 
   f32x4 acc[kDimBlocks];
