@@ -117,13 +117,13 @@ hipError_t launch_append(const AppendArgs& a, int dtype, int d, hipStream_t s);
 // Largest number of splits per (sequence, head) the merge pass accepts.
 constexpr int kMaxSplits = 1024;
 
-// Waves per bf16 prefill workgroup (32 query rows each) and query rows per
-// workgroup (bf16 path) and per fp32 workgroup.
-#ifndef AOH_PREFILL_WAVES
-#define AOH_PREFILL_WAVES 8
+// Query rows per bf16 prefill workgroup, and 32-row MFMA blocks per wave
+// (the workgroup has kPrefillRows / (32 * kPrefillRB) waves).
+#ifndef AOH_PREFILL_RB
+#define AOH_PREFILL_RB 1
 #endif
-constexpr int kPrefillWaves = AOH_PREFILL_WAVES;
-constexpr int kPrefillRows = 32 * kPrefillWaves;
+constexpr int kPrefillRB = AOH_PREFILL_RB;
+constexpr int kPrefillRows = 256;
 constexpr int kPrefillRowsF32 = 64;
 
 }  // namespace aoh

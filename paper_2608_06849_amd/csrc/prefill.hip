@@ -29,12 +29,19 @@
 namespace aoh {
 
 constexpr int kBN = 64;          // keys per tile
-constexpr int kWaves = kPrefillWaves;  // waves per workgroup
-constexpr int kRowsPerWave = 32;
+constexpr int kRB = kPrefillRB;                 // 32-row MFMA blocks per wave
+constexpr int kRowsPerWave = 32 * kRB;
+constexpr int kWaves = kPrefillRows / kRowsPerWave;  // waves per workgroup
 
 #ifndef AOH_PREFILL_V_PAD
 #define AOH_PREFILL_V_PAD 32
 #endif
+#ifndef AOH_PREFILL_STAGE_TILES
+#define AOH_PREFILL_STAGE_TILES 1
+#endif
+// 64-key tiles per LDS stage (one barrier per stage).
+constexpr int kStageTiles = AOH_PREFILL_STAGE_TILES;
+
 template <int D>
 struct PrefillLds {
   // Row paddings (bf16 elements): K rows are read 16 bytes per lane down 32
@@ -42,8 +49,8 @@ struct PrefillLds {
   // 16 lanes.  Each padding spreads its access pattern over distinct banks.
   static constexpr int kStrideK = D + 8;
   static constexpr int kStrideV = D + AOH_PREFILL_V_PAD;
-  uint16_t k[kBN][kStrideK];
-  uint16_t v[kBN][kStrideV];
+  uint16_t k[kBN * kStageTiles][kStrideK];
+  uint16_t v[kBN * kStageTiles][kStrideV];
 };
 
 // Lazy rescaling threshold (log2 units): the running max used for the
@@ -81,8 +88,8 @@ __device__ __forceinline__ TilePlan make_plan(int i0, int rows, int T, int n_sin
 }
 
 template <int D, bool STREAM, bool OUT_F32>
-__global__ __launch_bounds__(kWaves * kWave, 2) void prefill_bf16_kernel(PrefillArgs a) {
-  __shared__ __align__(16) PrefillLds<D> lds;
+__global__ __launch_bounds__(kWaves * kWave, kRB == 1 ? 2 : 1) void prefill_bf16_kernel(PrefillArgs a) {
+  __shared__ __align__(16) PrefillLds<D> lds[2];
   constexpr int kChunksPerRow = D / 8;                     // 16-byte chunks per key row
   constexpr int kChunksPerThread = kBN * kChunksPerRow / (kWaves * kWave);
   constexpr int kKSteps = D / 16;                          // MFMA k-steps over D
@@ -106,167 +113,265 @@ __global__ __launch_bounds__(kWaves * kWave, 2) void prefill_bf16_kernel(Prefill
   const int h2 = lane >> 5;
   const int T = a.T;
   const int i0 = qb * kPrefillRows;
-  const int r0 = i0 + wave * kRowsPerWave;
-  const int my_row = r0 + l32;
+  const int r0 = i0 + wave * kRowsPerWave;      // first row of this wave
+  int my_row[kRB];                              // row of this lane in each 32-row block
+#pragma unroll
+  for (int rb = 0; rb < kRB; ++rb) my_row[rb] = r0 + 32 * rb + l32;
 
   const uint16_t* qp = reinterpret_cast<const uint16_t*>(a.q) + (int64_t)b * a.q_sb + (int64_t)h * a.q_sh;
   const uint16_t* kp = reinterpret_cast<const uint16_t*>(a.k) + (int64_t)b * a.k_sb + (int64_t)g * a.k_sh;
   const uint16_t* vp = reinterpret_cast<const uint16_t*>(a.v) + (int64_t)b * a.v_sb + (int64_t)g * a.v_sh;
 
-  // Q^T operand: lane holds row my_row, dims 8*h2 + 16*s .. +8.
-  bf16x8 qreg[kKSteps];
+  // Q^T operands: lane holds row my_row[rb], dims 8*h2 + 16*s .. +8.
+  bf16x8 qreg[kRB][kKSteps];
 #pragma unroll
-  for (int s = 0; s < kKSteps; ++s) {
-    u32x4 x = {0u, 0u, 0u, 0u};
-    if (my_row < T) x = ld16(qp + (int64_t)my_row * a.q_st + 8 * h2 + 16 * s);
-    qreg[s] = __builtin_bit_cast(bf16x8, x);
-  }
+  for (int rb = 0; rb < kRB; ++rb)
+#pragma unroll
+    for (int s = 0; s < kKSteps; ++s) {
+      u32x4 x = {0u, 0u, 0u, 0u};
+      if (my_row[rb] < T) x = ld16(qp + (int64_t)my_row[rb] * a.q_st + 8 * h2 + 16 * s);
+      qreg[rb][s] = __builtin_bit_cast(bf16x8, x);
+    }
 
-  f32x16 acc_o[kMBlocks];
+  f32x16 acc_o[kRB][kMBlocks];
+  float m_run[kRB];  // reference max (log2 units) of this lane's row
+  float l_run[kRB];  // this lane's partial row sum (partner lane has the rest)
 #pragma unroll
-  for (int mb = 0; mb < kMBlocks; ++mb)
+  for (int rb = 0; rb < kRB; ++rb) {
+    m_run[rb] = -INFINITY;
+    l_run[rb] = 0.f;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) acc_o[mb][i] = 0.f;
-  float m_run = -INFINITY;  // reference max (log2 units) of this lane's row
-  float l_run = 0.f;        // this lane's partial row sum (partner lane has the rest)
+    for (int mb = 0; mb < kMBlocks; ++mb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc_o[rb][mb][i] = 0.f;
+  }
 
   const TilePlan plan = make_plan<STREAM>(i0, kPrefillRows, T, a.n_sink, a.window);
 
-  // Cooperative tile staging: registers -> LDS.
-  u32x4 kst[kChunksPerThread], vst[kChunksPerThread];
-  auto load_tile = [&](int kb) {
+  // Cooperative staging of one stage (kStageTiles tiles of 64 keys): global ->
+  // registers -> LDS (double buffered).  Per-thread row/column are fixed, so
+  // the global address of a tile is one scalar offset away.
+  u32x4 kst[kStageTiles][kChunksPerThread], vst[kStageTiles][kChunksPerThread];
+  int st_row[kChunksPerThread], st_col[kChunksPerThread];
 #pragma unroll
-    for (int r = 0; r < kChunksPerThread; ++r) {
-      const int c = tid + r * kWaves * kWave;
-      const int row = c / kChunksPerRow;
-      const int col = (c % kChunksPerRow) * 8;
-      const int key = kb + row;
-      if (key < T) {
-        kst[r] = ld16(kp + (int64_t)key * a.k_st + col);
-        vst[r] = ld16(vp + (int64_t)key * a.v_st + col);
-      } else {
-        kst[r] = u32x4{0u, 0u, 0u, 0u};
-        vst[r] = u32x4{0u, 0u, 0u, 0u};
+  for (int r = 0; r < kChunksPerThread; ++r) {
+    const int cidx = tid + r * kWaves * kWave;
+    st_row[r] = cidx / kChunksPerRow;
+    st_col[r] = (cidx % kChunksPerRow) * 8;
+  }
+  auto load_tile = [&](int u, int kb) {
+    if (kb + kBN <= T) {
+#pragma unroll
+      for (int r = 0; r < kChunksPerThread; ++r) {
+        kst[u][r] = ld16(kp + (int64_t)(kb + st_row[r]) * a.k_st + st_col[r]);
+        vst[u][r] = ld16(vp + (int64_t)(kb + st_row[r]) * a.v_st + st_col[r]);
+      }
+    } else {
+      // Ragged last tile: rows past T read row T-1 and are zeroed.
+#pragma unroll
+      for (int r = 0; r < kChunksPerThread; ++r) {
+        const int key = kb + st_row[r];
+        const int key_c = min(key, T - 1);
+        const u32x4 kx = ld16(kp + (int64_t)key_c * a.k_st + st_col[r]);
+        const u32x4 vx = ld16(vp + (int64_t)key_c * a.v_st + st_col[r]);
+        const bool in = key < T;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          kst[u][r][e] = in ? kx[e] : 0u;
+          vst[u][r][e] = in ? vx[e] : 0u;
+        }
       }
     }
   };
-  auto store_tile = [&]() {
+  auto load_stage = [&](int stage) {
 #pragma unroll
-    for (int r = 0; r < kChunksPerThread; ++r) {
-      const int c = tid + r * kWaves * kWave;
-      const int row = c / kChunksPerRow;
-      const int col = (c % kChunksPerRow) * 8;
-      *reinterpret_cast<u32x4*>(&lds.k[row][col]) = kst[r];
-      *reinterpret_cast<u32x4*>(&lds.v[row][col]) = vst[r];
+    for (int u = 0; u < kStageTiles; ++u) {
+      const int it = stage * kStageTiles + u;
+      if (it < plan.n_visit) load_tile(u, plan.tile(it) * kBN);
     }
+  };
+  auto store_stage = [&](PrefillLds<D>& buf) {
+#pragma unroll
+    for (int u = 0; u < kStageTiles; ++u)
+#pragma unroll
+      for (int r = 0; r < kChunksPerThread; ++r) {
+        *reinterpret_cast<u32x4*>(&buf.k[kBN * u + st_row[r]][st_col[r]]) = kst[u][r];
+        *reinterpret_cast<u32x4*>(&buf.v[kBN * u + st_row[r]][st_col[r]]) = vst[u][r];
+      }
   };
 
   const float c = a.scale_log2;
-  // One 64-key tile for this wave: S^T, online softmax, O^T += V^T P^T.
-  // MASKED selects the per-element mask; full tiles carry no mask code.
-  auto tile_step = [&](int kb, auto masked) {
+  // Softmax of one 32-key block of S^T for row block rb, in two halves so the
+  // caller can put independent MFMAs between them:
+  //   block_max:  mask, row max, lazy rescale decision (a wave-uniform branch)
+  //   block_exp:  exponentials into the two P^T operands of the block's key steps
+  auto block_max = [&](int rb, f32x16& sb, int key0, auto masked) {
     constexpr bool MASKED = decltype(masked)::value;
-    f32x16 s_acc[2];
-#pragma unroll
-    for (int blk = 0; blk < 2; ++blk) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) s_acc[blk][i] = 0.f;
-#pragma unroll
-      for (int s = 0; s < kKSteps; ++s) {
-        const bf16x8 kop = *reinterpret_cast<const bf16x8*>(&lds.k[32 * blk + l32][8 * h2 + 16 * s]);
-        s_acc[blk] = mfma32(kop, qreg[s], s_acc[blk]);
-      }
-    }
-    // Mask (raw scores), row max of the raw scores.
     float mx = -INFINITY;
 #pragma unroll
-    for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        float x = s_acc[blk][i];
-        if (MASKED) {
-          const int key = kb + 32 * blk + 8 * (i >> 2) + 4 * h2 + (i & 3);
-          bool vis = key <= my_row;
-          if (STREAM) vis = vis && (key < a.n_sink || my_row - key < a.window);
-          x = vis ? x : -INFINITY;
-          s_acc[blk][i] = x;
-        }
-        mx = fmaxf(mx, x);
+    for (int i = 0; i < 16; ++i) {
+      float x = sb[i];
+      if (MASKED) {
+        const int key = key0 + 8 * (i >> 2) + 4 * h2 + (i & 3);
+        bool vis = key <= my_row[rb];
+        if (STREAM) vis = vis && (key < a.n_sink || my_row[rb] - key < a.window);
+        x = vis ? x : -INFINITY;
+        sb[i] = x;
       }
+      mx = fmaxf(mx, x);
+    }
     mx = wave_xor_max(mx, 32) * c;  // log2 units (c > 0 keeps the order)
     // Raise the reference max only when some row needs it (wave-uniform).
-    if (__any(mx > m_run + kRescaleThreshold)) {
-      const float m_new = fmaxf(m_run, mx);
+    if (__any(mx > m_run[rb] + kRescaleThreshold)) {
+      const float m_new = fmaxf(m_run[rb], mx);
       // 0 when only m_run is -inf; 1 when the row has seen no visible key yet.
-      const float alpha = (m_new == -INFINITY) ? 1.f : fast_exp2(m_run - m_new);
-      m_run = m_new;
-      l_run *= alpha;
+      const float alpha = (m_new == -INFINITY) ? 1.f : fast_exp2(m_run[rb] - m_new);
+      m_run[rb] = m_new;
+      l_run[rb] *= alpha;
 #pragma unroll
       for (int mb = 0; mb < kMBlocks; ++mb)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) acc_o[mb][i] *= alpha;
+        for (int i = 0; i < 16; ++i) acc_o[rb][mb][i] *= alpha;
     }
-    const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
+  };
+  auto block_exp = [&](int rb, const f32x16& sb, bf16x8& p_lo, bf16x8& p_hi) {
+    const float m_use = (m_run[rb] == -INFINITY) ? 0.f : m_run[rb];
     float psum = 0.f;
-    bf16x8 pop[4];  // P^T operands for the 4 key steps of 16 keys
 #pragma unroll
-    for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float p = fast_exp2(fmaf(s_acc[blk][i], c, -m_use));
-        psum += p;
-        pop[blk * 2 + (i >> 3)][i & 7] = f32_to_bf16(p);
-      }
-    l_run += psum;
+    for (int i = 0; i < 16; ++i) {
+      const float p = fast_exp2(fmaf(sb[i], c, -m_use));
+      psum += p;
+      if (i < 8) p_lo[i] = f32_to_bf16(p);
+      else p_hi[i - 8] = f32_to_bf16(p);
+    }
+    l_run[rb] += psum;
+  };
 
-    // O^T += V^T . P^T.  Key step t covers keys 16t..16t+15; the k index
-    // 8*h2 + j maps to key 16t + 4*h2 + j (j < 4) or 16t + 8 + 4*h2 + (j-4).
-    const int q16 = lane >> 4;        // 16-lane block
-    const int i16 = lane & 15;
+  // S^T of one 32-key block for every row block: each K operand read from LDS
+  // feeds kRB MFMAs.
+  auto qk_block = [&](const PrefillLds<D>& buf, int u, int blk, f32x16 (&sb)[kRB]) {
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int vrow = 16 * t + 4 * h2 + (i16 >> 2);
+    for (int rb = 0; rb < kRB; ++rb)
 #pragma unroll
-      for (int mb = 0; mb < kMBlocks; ++mb) {
-        const int vcol = 32 * mb + 16 * (q16 & 1) + 4 * (i16 & 3);
-        const i16x4 lo = lds_read_tr16(&lds.v[vrow][vcol]);
-        const i16x4 hi = lds_read_tr16(&lds.v[vrow + 8][vcol]);
-        // Whole-vector concatenation: per-element bf16 insertion of the
-        // transposed halves is avoided on purpose (it was lowered to a
-        // broadcast of the first element by this toolchain).
-        const i16x8 cat = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-        acc_o[mb] = mfma32(__builtin_bit_cast(bf16x8, cat), pop[t], acc_o[mb]);
-      }
+      for (int i = 0; i < 16; ++i) sb[rb][i] = 0.f;
+#pragma unroll
+    for (int s = 0; s < kKSteps; ++s) {
+      const bf16x8 kop = *reinterpret_cast<const bf16x8*>(&buf.k[kBN * u + 32 * blk + l32][8 * h2 + 16 * s]);
+#pragma unroll
+      for (int rb = 0; rb < kRB; ++rb) sb[rb] = mfma32(kop, qreg[rb][s], sb[rb]);
+    }
+  };
+  // O^T += V^T . P^T for key step t (keys 16t..16t+15 of the tile): the k
+  // index 8*h2 + j maps to key 16t + 4*h2 + j (j < 4) or 16t + 8 + 4*h2 + (j-4).
+  // Each V^T operand (two transpose reads) feeds kRB MFMAs.
+  const int q16 = lane >> 4;        // 16-lane block
+  const int i16 = lane & 15;
+  auto pv_step = [&](const PrefillLds<D>& buf, int u, int t, const bf16x8 (&pop)[kRB]) {
+    const int vrow = kBN * u + 16 * t + 4 * h2 + (i16 >> 2);
+#pragma unroll
+    for (int mb = 0; mb < kMBlocks; ++mb) {
+      const int vcol = 32 * mb + 16 * (q16 & 1) + 4 * (i16 & 3);
+      const i16x4 lo = lds_read_tr16(&buf.v[vrow][vcol]);
+      const i16x4 hi = lds_read_tr16(&buf.v[vrow + 8][vcol]);
+      // Whole-vector concatenation: per-element bf16 insertion of the
+      // transposed halves is avoided on purpose (it was lowered to a
+      // broadcast of the first element by this toolchain).
+      const i16x8 cat = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      const bf16x8 vop = __builtin_bit_cast(bf16x8, cat);
+#pragma unroll
+      for (int rb = 0; rb < kRB; ++rb) acc_o[rb][mb] = mfma32(vop, pop[rb], acc_o[rb][mb]);
     }
   };
 
-  if (plan.n_visit > 0) load_tile(plan.tile(0) * kBN);
+  // One 64-key tile for this wave.  MASKED selects the per-element mask; full
+  // tiles carry no mask code.  Order: S^T of block 0, its max; then the S^T
+  // MFMAs of block 1 next to the exponentials of block 0 and the P.V MFMAs of
+  // block 0 next to the max of block 1 (same scheduling region, independent
+  // work for the matrix core and the vector ALU); then block 1.
+#ifndef AOH_PREFILL_SETPRIO
+#define AOH_PREFILL_SETPRIO 1
+#endif
+  // Wave issue priority (s_setprio, inside this wave only): raised while a wave
+  // issues its MFMA clusters so the matrix core is fed first and the other
+  // wave's vector work fills the gaps.
+  auto prio = [&](int p) {
+#if AOH_PREFILL_SETPRIO
+    if (p) __builtin_amdgcn_s_setprio(1);
+    else __builtin_amdgcn_s_setprio(0);
+#else
+    (void)p;
+#endif
+  };
+  auto tile_step = [&](const PrefillLds<D>& buf, int u, int kb, auto masked) {
+    f32x16 s0[kRB], s1[kRB];
+    bf16x8 p0[kRB], p1[kRB], p2[kRB], p3[kRB];  // P^T operands of the 4 key steps
+    prio(1);
+    qk_block(buf, u, 0, s0);
+    prio(0);
+#pragma unroll
+    for (int rb = 0; rb < kRB; ++rb) block_max(rb, s0[rb], kb, masked);
+    prio(1);
+    qk_block(buf, u, 1, s1);
+#pragma unroll
+    for (int rb = 0; rb < kRB; ++rb) block_exp(rb, s0[rb], p0[rb], p1[rb]);
+    pv_step(buf, u, 0, p0);
+    pv_step(buf, u, 1, p1);
+    prio(0);
+#pragma unroll
+    for (int rb = 0; rb < kRB; ++rb) block_max(rb, s1[rb], kb + 32, masked);
+#pragma unroll
+    for (int rb = 0; rb < kRB; ++rb) block_exp(rb, s1[rb], p2[rb], p3[rb]);
+    prio(1);
+    pv_step(buf, u, 2, p2);
+    pv_step(buf, u, 3, p3);
+    prio(0);
+  };
 
-  for (int it = 0; it < plan.n_visit; ++it) {
-    const int kb = plan.tile(it) * kBN;
-    store_tile();
-    __syncthreads();
-    if (it + 1 < plan.n_visit) load_tile(plan.tile(it + 1) * kBN);
-
-    // Is any element of this wave's 32 x 64 block visible?  Is every element?
-    const bool wave_dead = (kb > r0 + kRowsPerWave - 1) ||
-                           (STREAM && kb >= a.n_sink && (r0 - (kb + kBN - 1)) >= a.window);
-    if (!wave_dead) {
-      const bool need_mask = (kb + kBN - 1 > r0) ||
-                             (STREAM && !(kb + kBN - 1 < a.n_sink ||
-                                          (r0 + kRowsPerWave - 1) - kb < a.window));
-      if (need_mask) tile_step(kb, std::true_type{});
-      else tile_step(kb, std::false_type{});
+  // Double-buffered main loop: one barrier per stage of kStageTiles tiles.
+  // While stage `st` is computed from lds[st & 1], stage st+1 waits in
+  // registers and is written to the other buffer afterwards; stage st+2 is
+  // fetched from global memory.
+  const int n_stage = (plan.n_visit + kStageTiles - 1) / kStageTiles;
+  if (n_stage > 0) {
+    load_stage(0);
+    store_stage(lds[0]);
+    if (n_stage > 1) load_stage(1);
+  }
+  __syncthreads();
+  for (int st = 0; st < n_stage; ++st) {
+    const PrefillLds<D>& buf = lds[st & 1];
+#pragma unroll
+    for (int u = 0; u < kStageTiles; ++u) {
+      const int it = st * kStageTiles + u;
+      if (it < plan.n_visit) {
+        const int kb = plan.tile(it) * kBN;
+        // Is any element of this wave's rows x 64 keys visible?  Is every element?
+        const bool wave_dead = (kb > r0 + kRowsPerWave - 1) ||
+                               (STREAM && kb >= a.n_sink && (r0 - (kb + kBN - 1)) >= a.window);
+        if (!wave_dead) {
+          const bool need_mask = (kb + kBN - 1 > r0) ||
+                                 (STREAM && !(kb + kBN - 1 < a.n_sink ||
+                                              (r0 + kRowsPerWave - 1) - kb < a.window));
+          if (need_mask) tile_step(buf, u, kb, std::true_type{});
+          else tile_step(buf, u, kb, std::false_type{});
+        }
+      }
+    }
+    if (st + 1 < n_stage) {
+      store_stage(lds[(st + 1) & 1]);
+      if (st + 2 < n_stage) load_stage(st + 2);
     }
     __syncthreads();
   }
 
-  // Epilogue: combine the two half-row sums, normalise, store.
-  const float l_tot = wave_xor_sum(l_run, 32);
-  const float inv = 1.f / l_tot;
-  if (my_row < T) {
+  // Epilogue: normalise by the row sum, store.
+#pragma unroll
+  for (int rb = 0; rb < kRB; ++rb) {
+    const float l_tot = wave_xor_sum(l_run[rb], 32);
+    const float inv = 1.f / l_tot;
+    if (my_row[rb] >= T) continue;
     if (OUT_F32) {
-      float* op = reinterpret_cast<float*>(a.out) + (int64_t)b * a.o_sb + (int64_t)my_row * a.o_st +
+      float* op = reinterpret_cast<float*>(a.out) + (int64_t)b * a.o_sb + (int64_t)my_row[rb] * a.o_st +
                   (int64_t)h * a.o_sh;
 #pragma unroll
       for (int mb = 0; mb < kMBlocks; ++mb)
@@ -274,21 +379,21 @@ __global__ __launch_bounds__(kWaves * kWave, 2) void prefill_bf16_kernel(Prefill
         for (int q4 = 0; q4 < 4; ++q4) {
           f32x4 w;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) w[e] = acc_o[mb][4 * q4 + e] * inv;
+          for (int e = 0; e < 4; ++e) w[e] = acc_o[rb][mb][4 * q4 + e] * inv;
           *reinterpret_cast<f32x4*>(op + 32 * mb + 8 * q4 + 4 * h2) = w;
         }
     } else {
-      uint16_t* op = reinterpret_cast<uint16_t*>(a.out) + (int64_t)b * a.o_sb + (int64_t)my_row * a.o_st +
+      uint16_t* op = reinterpret_cast<uint16_t*>(a.out) + (int64_t)b * a.o_sb + (int64_t)my_row[rb] * a.o_st +
                      (int64_t)h * a.o_sh;
 #pragma unroll
       for (int mb = 0; mb < kMBlocks; ++mb)
 #pragma unroll
         for (int q4 = 0; q4 < 4; ++q4) {
           u32x2 w;
-          w[0] = (uint32_t)f32_to_bf16_bits(acc_o[mb][4 * q4 + 0] * inv) |
-                 ((uint32_t)f32_to_bf16_bits(acc_o[mb][4 * q4 + 1] * inv) << 16);
-          w[1] = (uint32_t)f32_to_bf16_bits(acc_o[mb][4 * q4 + 2] * inv) |
-                 ((uint32_t)f32_to_bf16_bits(acc_o[mb][4 * q4 + 3] * inv) << 16);
+          w[0] = (uint32_t)f32_to_bf16_bits(acc_o[rb][mb][4 * q4 + 0] * inv) |
+                 ((uint32_t)f32_to_bf16_bits(acc_o[rb][mb][4 * q4 + 1] * inv) << 16);
+          w[1] = (uint32_t)f32_to_bf16_bits(acc_o[rb][mb][4 * q4 + 2] * inv) |
+                 ((uint32_t)f32_to_bf16_bits(acc_o[rb][mb][4 * q4 + 3] * inv) << 16);
           *reinterpret_cast<u32x2*>(op + 32 * mb + 8 * q4 + 4 * h2) = w;
         }
     }
