@@ -67,7 +67,50 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-all-retrieval", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy 5 times (for scaling HBM counters)")
     return ap.parse_args()
+
+
+def copy_calibration():
+    """A plain copy of known size: 1 GiB read + 1 GiB written per dispatch."""
+    import torch
+    src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log("copy calibration: 5 x 1 GiB device-to-device copies done")
+
+
+# HBM traffic per launch measured with rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE
+# (KiB per dispatch), divided by the ratio those counters read for a plain
+# 1 GiB copy (bench.py --copy-calibration), and the hash of the kernel sources
+# they were taken on: a source change makes the figure stale and it is dropped.
+TRAFFIC = {
+    "source_hash": "6ff0fd057756bc7d",
+    "fetch_factor": 524301.2 / 1048576.0,   # FETCH_SIZE of a 1 GiB copy / 1 GiB
+    "write_factor": 1048576.0 / 1048576.0,  # WRITE_SIZE of a 1 GiB copy / 1 GiB
+    "prefill_retrieval": {"fetch_kib": 1033996.8, "write_kib": 114701.0},
+    "decode_split": {"fetch_kib": 1061481.4, "write_kib": 4829.6},
+}
+
+
+def kernel_source_hash():
+    import hashlib
+    root = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2608_06849_amd", "csrc")
+    h = hashlib.sha256()
+    for name in ("prefill.hip", "decode.hip", "aoh_device.h", "aoh_internal.h"):
+        with open(os.path.join(root, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_for(kernel):
+    if TRAFFIC is None or TRAFFIC.get("source_hash") != kernel_source_hash():
+        return None
+    t = TRAFFIC[kernel]
+    return round((t["fetch_kib"] / TRAFFIC["fetch_factor"] + t["write_kib"] / TRAFFIC["write_factor"]) * 1024)
 
 
 def main():
@@ -77,6 +120,10 @@ def main():
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}); "
               "the hot path is not sharded across GPUs", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_calibration:
+        copy_calibration()
+        return
 
     import torch
 
@@ -228,7 +275,7 @@ def main():
         "roofline": {
             "kernel": f"prefill_bf16_kernel<128,retrieval> ({gs * n_ret} q heads x {T} rows)",
             "bound": "mfma", "achieved": round(ret_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-            "frac": round(ret_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+            "frac": round(ret_tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic_for("prefill_retrieval"),
             "algorithmic_per_launch": f"{flops_ret:.4e} FLOP", "avg_launch_ms": round(ret_ms, 4),
         },
         "all_retrieval": None if all_ret is None else {
@@ -320,7 +367,8 @@ def decode_leg(args, torch, synth, PagedCache, RingCache, aoh_decode, aoh_decode
         "roofline": {
             "kernel": "decode_split_bf16_kernel<128,paged> + ring split + merge (one aoh_decode call)",
             "bound": "hbm", "achieved": round(b_last / (dec_ms * 1e-3) / 1e9, 1), "peak": PEAK_HBM_GBPS,
-            "unit": "GB/s", "frac": round(b_last / (dec_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4), "traffic": None,
+            "unit": "GB/s", "frac": round(b_last / (dec_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+            "traffic": traffic_for("decode_split"),
             "algorithmic_per_launch": f"{b_last:.4e} B", "avg_launch_ms": round(dec_ms, 4),
         },
     }
