@@ -67,6 +67,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-all-retrieval", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-stack-decode", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (for scaling HBM counters)")
     return ap.parse_args()
@@ -241,6 +242,11 @@ def main():
         dec = decode_leg(args, torch, synth, PagedCache, RingCache, aoh_decode, aoh_decode_workspace_bytes,
                          aoh_kv_append, decode_bytes)
 
+    stack = None
+    if not args.no_stack_decode:
+        stack = stack_decode_leg(args, torch, synth, PagedCache, RingCache, aoh_decode, aoh_decode_workspace_bytes,
+                                 aoh_kv_append, decode_bytes)
+
     # ------------------------------------------------------------------ CPU baseline (oracle)
     cpu = None
     if not args.no_cpu_baseline:
@@ -284,6 +290,7 @@ def main():
             "speedup_prefill": round(all_ret["prefill_ms"] / prefill_ms, 3),
         },
         "decode": dec,
+        "stack_decode": stack,
         "cpu_baseline": cpu,
         "paper_context": "paper (hardware unstated, end-to-end model latency, bf16, batch 1): prefill/decode "
                          "latency reduction up to 41.4%/66.0% and 50.0% KV saving at 256K, 50% sparsity",
@@ -380,6 +387,82 @@ def decode_leg(args, torch, synth, PagedCache, RingCache, aoh_decode, aoh_decode
         res["speedup_vs_all_retrieval"] = round(ms_all / ms, 3)
         res["resident_kv_gb_all_retrieval"] = round((full_all.k.numel() + full_all.v.numel()) * 2 / 1e9, 4)
         log(f"decode all-retrieval {ms_all:.4f} ms/step")
+    return res
+
+
+def stack_decode_leg(args, torch, synth, PagedCache, RingCache, aoh_decode, aoh_decode_workspace_bytes,
+                     aoh_kv_append, decode_bytes):
+    """Decode steps through all 28 layers of the Qwen2.5-7B-shaped stack at a
+    262144-token context (batch 1, 2 of 4 KV heads streaming per layer,
+    n_sink 64, window 2048), issued eagerly and as one captured HIP graph per
+    step.  Cache contents do not change the timing; they are filled from
+    torch's seeded device generator."""
+    c = synth.CONFIGS["qwen25_stack_256k"]
+    L, T, Hq, Hkv, D, n_sink, window = c["layers"], c["seq"], c["hq"], c["hkv"], c["d"], c["n_sink"], c["window"]
+    steps = 16
+    dev, bf = "cuda", torch.bfloat16
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(c["seed"])
+    max_pages = (T + 2 * steps + 16 + 15) // 16
+    bt = torch.arange(max_pages, dtype=torch.int32)[None]
+    layers = []
+    for l in range(L):
+        mask = synth.choose_streaming(Hkv, c["n_streaming"], c["seed"], "streaming", l).tolist()
+        full = PagedCache.allocate(max_pages, mask.count(0), D, bf, bt)
+        ring = RingCache.allocate(1, mask.count(1), n_sink, window, D, bf)
+        for t in (full.k, full.v, ring.k, ring.v):
+            t.normal_(generator=gen)
+        layers.append((mask, full, ring))
+    q = torch.randn((L, 1, Hq, D), device=dev, generator=gen).to(bf)
+    kv = torch.randn((L, 2, 1, 1, Hkv, D), device=dev, generator=gen).to(bf)
+    lens_before = torch.full((1,), T, dtype=torch.int32, device=dev)
+    lens_after = lens_before + 1
+    ws = torch.empty(aoh_decode_workspace_bytes(1, Hq, D, max_pages, n_sink + window) // 4 + 4,
+                     dtype=torch.float32, device=dev)
+    outs = torch.empty((L, 1, Hq, D), dtype=bf, device=dev)
+
+    def one_step():
+        for l, (mask, full, ring) in enumerate(layers):
+            aoh_kv_append(kv[l, 0], kv[l, 1], mask, lens_before, full, ring, n_sink, window)
+            aoh_decode(q[l], full, ring, mask, lens_after, n_sink, window, out=outs[l], workspace=ws)
+        lens_before.add_(1)
+        lens_after.add_(1)
+
+    def timed(fn):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        ev[0].record()
+        for _ in range(steps):
+            fn()
+        ev[1].record()
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]) / steps
+
+    one_step()
+    eager_ms = timed(one_step)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        one_step()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        one_step()
+    graph_ms = timed(g.replay)
+    by = L * decode_bytes([T + steps], Hkv - c["n_streaming"], c["n_streaming"], D, 2, n_sink, window)
+    res = {
+        "workload": "decode step through 28 layers of the Qwen2.5-7B attention shape, batch 1, context 262144, "
+                    "2 of 4 KV heads streaming per layer (n_sink 64, window 2048); per layer: append 1 token + decode",
+        "eager_ms_per_step": round(eager_ms, 4),
+        "graph_ms_per_step": round(graph_ms, 4),
+        "graph_speedup": round(eager_ms / graph_ms, 3),
+        "kv_gb_per_step": round(by / 1e9, 4),
+        "kv_gbps_graph": round(by / (graph_ms * 1e-3) / 1e9, 1),
+        "frac_of_hbm_peak_graph": round(by / (graph_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+    }
+    log(f"stack decode: eager {eager_ms:.3f} ms/step, graph {graph_ms:.3f} ms/step, "
+        f"{res['kv_gbps_graph']:.0f} GB/s with the graph")
     return res
 
 

@@ -103,9 +103,15 @@ aoh_status check_mask_params(int n_sink, int window) {
 }
 
 // Decode split plan.  A paged split is split_blocks_full 16-token blocks
-// (even, so a wave always reads whole 32-token chunks); about 512 splits per
-// KV head over the batch keep several waves per CU in flight.  The ring is cut
-// the same way with about 64 splits per KV head over the batch.
+// (even, so a wave always reads whole 32-token chunks).  The split count per
+// (sequence, KV head) aims at ~kTargetWaves paged waves over the whole launch
+// (8 per CU: enough loads in flight to stream HBM), never above kMaxSplits.
+// The ring is cut the same way with ~kTargetWaves / 8 waves.  n_ret (retrieval
+// KV heads) may be unknown (workspace sizing): then the plan for n_ret = 1 is
+// used, which has the most splits and so bounds every real plan.
+#ifndef AOH_DECODE_TARGET_WAVES
+#define AOH_DECODE_TARGET_WAVES 2048
+#endif
 struct SplitPlan {
   int split_blocks_full, n_splits_full;
   int split_blocks_ring, n_splits_ring;
@@ -113,24 +119,23 @@ struct SplitPlan {
   int max_splits;
 };
 
-#ifndef AOH_DECODE_SPLIT_TARGET
-#define AOH_DECODE_SPLIT_TARGET 512
-#endif
-
-SplitPlan plan_splits(int batch, int max_pages, int ring_cap) {
+SplitPlan plan_splits(int batch, int max_pages, int ring_cap, int n_ret, int n_str) {
   SplitPlan p;
-  const int target_full = std::max(1, AOH_DECODE_SPLIT_TARGET / batch);
+  const int64_t per_head = std::max<int64_t>(1, (int64_t)AOH_DECODE_TARGET_WAVES / ((int64_t)batch * std::max(n_ret, 1)));
+  const int target_full = (int)std::min<int64_t>(per_head, kMaxSplits);
   int sb = (int)std::max<int64_t>(2, ceil_div(max_pages, target_full));
   sb += sb & 1;
   p.split_blocks_full = sb;
   p.n_splits_full = (int)ceil_div(max_pages, sb);
   p.ring_blocks = (int)ceil_div(std::max(ring_cap, 1), kPageTokens);
-  const int target_ring = std::max(1, 64 / batch);
+  const int64_t per_head_ring =
+      std::max<int64_t>(1, (int64_t)(AOH_DECODE_TARGET_WAVES / 8) / ((int64_t)batch * std::max(n_str, 1)));
+  const int target_ring = (int)std::min<int64_t>(per_head_ring, kMaxSplits);
   int sbr = (int)std::max<int64_t>(2, ceil_div(p.ring_blocks, target_ring));
   sbr += sbr & 1;
   p.split_blocks_ring = sbr;
   p.n_splits_ring = (int)ceil_div(p.ring_blocks, sbr);
-  p.max_splits = std::max(p.n_splits_full, p.n_splits_ring);  // <= 513 < kMaxSplits by construction
+  p.max_splits = std::max(p.n_splits_full, p.n_splits_ring);  // <= kMaxSplits by construction
   return p;
 }
 
@@ -284,7 +289,7 @@ size_t aoh_decode_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t d_he
   if (batch < 1 || n_q_heads < 1 || (d_head != 64 && d_head != 128) || max_pages_per_seq < 1 ||
       ring_capacity < 0)
     return 0;
-  return workspace_bytes(batch, n_q_heads, d_head, plan_splits(batch, max_pages_per_seq, ring_capacity));
+  return workspace_bytes(batch, n_q_heads, d_head, plan_splits(batch, max_pages_per_seq, ring_capacity, 1, 1));
 }
 
 aoh_status aoh_decode(const aoh_tensor* q, const aoh_paged_cache* kv_full,
@@ -316,7 +321,9 @@ aoh_status aoh_decode(const aoh_tensor* q, const aoh_paged_cache* kv_full,
   if (dt == AOH_BF16 && gs > 16) return fail(AOH_ERR_UNSUPPORTED, "Hq/Hkv=%d > 16", gs);
   const int max_pages = hs.n_ret ? kv_full->max_pages_per_seq : 1;
   const int ring_cap = n_sink + window;
-  const SplitPlan sp = plan_splits((int)B, max_pages, ring_cap);
+  const SplitPlan sp = plan_splits((int)B, max_pages, ring_cap, hs.n_ret, hs.n_str);
+  // The workspace is sized for the n_ret = n_str = 1 plan, which bounds this one.
+  const SplitPlan sp_bound = plan_splits((int)B, max_pages, ring_cap, 1, 1);
 
   DecodeArgs a;
   std::memset(&a, 0, sizeof(a));
@@ -353,14 +360,14 @@ aoh_status aoh_decode(const aoh_tensor* q, const aoh_paged_cache* kv_full,
     return ok();
   }
 
-  const size_t need = workspace_bytes((int)B, (int)Hq, (int)D, sp);
+  const size_t need = workspace_bytes((int)B, (int)Hq, (int)D, sp_bound);
   if (!workspace) return fail(AOH_ERR_WORKSPACE, "workspace is null; %zu bytes needed", need);
   if (workspace_bytes_given < need)
     return fail(AOH_ERR_WORKSPACE, "workspace has %zu bytes; %zu needed", workspace_bytes_given, need);
   if (reinterpret_cast<uintptr_t>(workspace) % 16) return fail(AOH_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
   float* part_acc = reinterpret_cast<float*>(workspace);
-  float* part_ml = part_acc + (size_t)B * Hq * sp.max_splits * D;
-  a.part_acc = part_acc; a.part_ml = part_ml; a.max_splits = sp.max_splits;
+  float* part_ml = part_acc + (size_t)B * Hq * sp_bound.max_splits * D;
+  a.part_acc = part_acc; a.part_ml = part_ml; a.max_splits = sp_bound.max_splits;
   if ((int64_t)a.full.n_items + a.ring.n_items >= (1ll << 31)) return fail(AOH_ERR_UNSUPPORTED, "grid too large");
   {
     hipError_t e = launch_decode_split(a, (int)D, s);
@@ -370,7 +377,7 @@ aoh_status aoh_decode(const aoh_tensor* q, const aoh_paged_cache* kv_full,
   std::memset(&m, 0, sizeof(m));
   m.part_acc = part_acc; m.part_ml = part_ml; m.lens = lens;
   m.out = out->data; m.o_sb = out->stride[0]; m.o_sh = out->stride[1];
-  m.B = (int)B; m.Hq = (int)Hq; m.gs = gs; m.max_splits = sp.max_splits;
+  m.B = (int)B; m.Hq = (int)Hq; m.gs = gs; m.max_splits = sp_bound.max_splits;
   m.split_tokens_full = sp.split_blocks_full * kPageTokens;
   m.split_tokens_ring = sp.split_blocks_ring * kPageTokens;
   m.n_splits_full = sp.n_splits_full;

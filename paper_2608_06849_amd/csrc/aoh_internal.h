@@ -122,8 +122,11 @@ constexpr int kMaxSplits = 1024;
 #ifndef AOH_PREFILL_RB
 #define AOH_PREFILL_RB 1
 #endif
+#ifndef AOH_PREFILL_ROWS
+#define AOH_PREFILL_ROWS 256
+#endif
 constexpr int kPrefillRB = AOH_PREFILL_RB;
-constexpr int kPrefillRows = 256;
+constexpr int kPrefillRows = AOH_PREFILL_ROWS;
 constexpr int kPrefillRowsF32 = 64;
 
 }  // namespace aoh

@@ -289,22 +289,26 @@ __global__ __launch_bounds__(kWave) void decode_f32_kernel(DecodeArgs a, void* o
   else decode_f32_body<D, true>(a, a.ring, wg - n_full, out, o_sb, o_sh);
 }
 
-constexpr int kMergeThreads = 256;
+constexpr int kMergeDims = 32;      // output dimensions per merge workgroup
+constexpr int kMergeThreads = 512;  // kMergeDims x 16 split groups
 
-// Log-sum-exp merge of the split partials of one (sequence, query head).  The
-// per-split (m, l) are loaded by all threads at once and reduced in LDS; the
-// weighted sum over splits of acc[d] is spread over kMergeThreads / D groups
-// of D threads so many loads are in flight.
+// Log-sum-exp merge of the split partials of one (sequence, query head), for
+// one slice of kMergeDims output dimensions.  The per-split (m, l) are loaded
+// by all threads at once and reduced in LDS; the weighted sum over splits of
+// acc[d] is spread over kMergeThreads / kMergeDims groups (coalesced 128-byte
+// rows), so many loads are in flight even for a single long sequence.
 template <int D, bool OUT_F32>
 __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(MergeArgs a) {
-  constexpr int kGroups = kMergeThreads / D;
+  constexpr int kGroups = kMergeThreads / kMergeDims;
   constexpr int kWaves = kMergeThreads / kWave;
+  constexpr int kSlices = D / kMergeDims;
   __shared__ float s_w[kMaxSplits];
   __shared__ float s_red[kWaves];
-  __shared__ float s_acc[kGroups][D];
+  __shared__ float s_acc[kGroups][kMergeDims];
   const int wg = blockIdx.x;
-  const int hq = wg % a.Hq;
-  const int b = wg / a.Hq;
+  const int slice = wg % kSlices;
+  const int hq = (wg / kSlices) % a.Hq;
+  const int b = wg / (kSlices * a.Hq);
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1), wave = tid / kWave;
   const int g = hq / a.gs;
@@ -343,16 +347,17 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(MergeArgs a
 #pragma unroll
   for (int i = 0; i < kWaves; ++i) L += s_red[i];
 
-  const int d = tid % D, grp = tid / D;
+  const int dd = tid % kMergeDims, grp = tid / kMergeDims;
+  const int d = slice * kMergeDims + dd;
   float acc = 0.f;
 #pragma unroll 8
   for (int s = grp; s < ns; s += kGroups) acc += s_w[s] * a.part_acc[(base + s) * D + d];
-  s_acc[grp][d] = acc;
+  s_acc[grp][dd] = acc;
   __syncthreads();
   if (grp == 0) {
     float tot = 0.f;
 #pragma unroll
-    for (int i = 0; i < kGroups; ++i) tot += s_acc[i][d];
+    for (int i = 0; i < kGroups; ++i) tot += s_acc[i][dd];
     const float o = tot / L;
     if (OUT_F32) {
       reinterpret_cast<float*>(a.out)[(int64_t)b * a.o_sb + (int64_t)hq * a.o_sh + d] = o;
@@ -378,7 +383,7 @@ hipError_t launch_decode_f32(const DecodeArgs& a, int d, void* out, int64_t o_sb
 
 hipError_t launch_decode_merge(const MergeArgs& a, int dtype, int out_f32, int d, hipStream_t s) {
   (void)dtype;
-  const int grid = a.B * a.Hq;
+  const int grid = a.B * a.Hq * (d / kMergeDims);
   if (d == 64) {
     if (out_f32) hipLaunchKernelGGL((decode_merge_kernel<64, true>), dim3(grid), dim3(kMergeThreads), 0, s, a);
     else hipLaunchKernelGGL((decode_merge_kernel<64, false>), dim3(grid), dim3(kMergeThreads), 0, s, a);

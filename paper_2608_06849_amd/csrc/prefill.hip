@@ -234,16 +234,36 @@ __global__ __launch_bounds__(kWaves * kWave, kRB == 1 ? 2 : 1) void prefill_bf16
         for (int i = 0; i < 16; ++i) acc_o[rb][mb][i] *= alpha;
     }
   };
+#ifndef AOH_PREFILL_DOT2_SUM
+#define AOH_PREFILL_DOT2_SUM 1
+#endif
   auto block_exp = [&](int rb, const f32x16& sb, bf16x8& p_lo, bf16x8& p_hi) {
     const float m_use = (m_run[rb] == -INFINITY) ? 0.f : m_run[rb];
     float psum = 0.f;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const float p = fast_exp2(fmaf(sb[i], c, -m_use));
+#if !AOH_PREFILL_DOT2_SUM
       psum += p;
+#endif
       if (i < 8) p_lo[i] = f32_to_bf16(p);
       else p_hi[i - 8] = f32_to_bf16(p);
     }
+#if AOH_PREFILL_DOT2_SUM
+    // Row sum of the bf16 P actually fed to P.V: one dot2 with (1, 1) per pair.
+    const bf16x2 ones = {(bf16)1.f, (bf16)1.f};
+#define AOH_DOT2_PAIR(v, j) \
+  psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, j, j + 1), ones, psum, false)
+    AOH_DOT2_PAIR(p_lo, 0);
+    AOH_DOT2_PAIR(p_lo, 2);
+    AOH_DOT2_PAIR(p_lo, 4);
+    AOH_DOT2_PAIR(p_lo, 6);
+    AOH_DOT2_PAIR(p_hi, 0);
+    AOH_DOT2_PAIR(p_hi, 2);
+    AOH_DOT2_PAIR(p_hi, 4);
+    AOH_DOT2_PAIR(p_hi, 6);
+#undef AOH_DOT2_PAIR
+#endif
     l_run[rb] += psum;
   };
 
