@@ -36,20 +36,31 @@ def group_of(h, n_q_heads, n_kv_heads):
     return h // (n_q_heads // n_kv_heads)
 
 
-def visible_mask(q_pos, n_keys, streaming, n_sink, window):
+def visible_mask(q_pos, n_keys, streaming, n_sink, window, chunk=0):
     """Boolean [len(q_pos), n_keys]: key j is visible to the query at position i.
 
-    Retrieval: j <= i.  Streaming: j <= i and (j < n_sink or i - j < window).
+    Retrieval: j <= i.
+    Streaming, per-token band (chunk = 0): j <= i and (j < n_sink or i - j < window).
+    Streaming, chunk eviction (chunk = K >= 1; Sec. 5 chunked-prefill stage):
+    the prompt is processed in chunks of K tokens and after each chunk the cache
+    keeps only the sink tokens and the `window` most recent tokens, so a query
+    of the chunk starting at c = (i // K) * K sees the sink, the `window`
+    tokens before c, and its own chunk up to itself:
+        j <= i and (j < n_sink or j >= c - window).
     """
     i = np.asarray(q_pos, dtype=np.int64)[:, None]
     j = np.arange(n_keys, dtype=np.int64)[None, :]
     mask = j <= i
     if streaming:
-        mask = mask & ((j < n_sink) | (i - j < window))
+        if chunk:
+            lo = (i // chunk) * chunk - window
+            mask = mask & ((j < n_sink) | (j >= lo))
+        else:
+            mask = mask & ((j < n_sink) | (i - j < window))
     return mask
 
 
-def attend_rows(q_rows, q_pos, k, v, streaming, n_sink, window):
+def attend_rows(q_rows, q_pos, k, v, streaming, n_sink, window, chunk=0):
     """Attention output for a set of query rows of one head.
 
     q_rows [R, D] at absolute positions q_pos [R]; k, v [T, D] hold the keys and
@@ -63,7 +74,7 @@ def attend_rows(q_rows, q_pos, k, v, streaming, n_sink, window):
     v = np.asarray(v, dtype=np.float64)
     d = q_rows.shape[-1]
     s = (q_rows @ k.T) / np.sqrt(d)
-    mask = visible_mask(q_pos, k.shape[0], streaming, n_sink, window)
+    mask = visible_mask(q_pos, k.shape[0], streaming, n_sink, window, chunk)
     if not mask.any(axis=1).all():
         raise ValueError("a query row has no visible key")
     s = np.where(mask, s, -np.inf)
@@ -83,11 +94,12 @@ def attention_weights(q_rows, q_pos, k, streaming, n_sink, window):
     return p / p.sum(axis=1, keepdims=True)
 
 
-def prefill(q, k, v, head_is_streaming, n_sink, window, rows=None, row_block=512):
+def prefill(q, k, v, head_is_streaming, n_sink, window, rows=None, row_block=512, chunk=0):
     """Head-mixed causal prefill.
 
     q [B, T, Hq, D]; k, v [B, T, Hkv, D]; head_is_streaming [Hkv] (0/1).
     rows: optional sorted positions to evaluate (default: all T rows).
+    chunk: 0 for the per-token band mask, K >= 1 for chunk eviction.
     Returns [B, len(rows), Hq, D] float64 in the original query-head order.
     """
     q = np.asarray(q)
@@ -107,7 +119,7 @@ def prefill(q, k, v, head_is_streaming, n_sink, window, rows=None, row_block=512
                 hi = int(pos.max()) + 1  # keys beyond the last row are never visible
                 out[b, r0:r0 + len(pos), h, :] = attend_rows(
                     np.asarray(q[b, pos, h, :], dtype=np.float64), pos,
-                    kg[:hi], vg[:hi], bool(head_is_streaming[g]), n_sink, window)
+                    kg[:hi], vg[:hi], bool(head_is_streaming[g]), n_sink, window, chunk)
     return out
 
 
@@ -136,7 +148,7 @@ def decode(q, k_seq, v_seq, lens, head_is_streaming, n_sink, window):
     return out
 
 
-def brute_force(q, k, v, head_is_streaming, n_sink, window):
+def brute_force(q, k, v, head_is_streaming, n_sink, window, chunk=0):
     """Second, independent path for tiny inputs (T <= 64).
 
     Builds the dense visibility matrix with explicit Python loops from the
@@ -157,8 +169,14 @@ def brute_force(q, k, v, head_is_streaming, n_sink, window):
                 for j in range(t_n):
                     if j > i:
                         continue
-                    if stream and not (j < n_sink or j >= i - window + 1):
-                        continue
+                    if stream:
+                        if chunk:
+                            # the cache before i's chunk: sink + the window tokens before it
+                            chunk_start = i - i % chunk
+                            if not (j < n_sink or j >= chunk_start - window):
+                                continue
+                        elif not (j < n_sink or j >= i - window + 1):
+                            continue
                     keep.append(j)
                 w = []
                 for j in keep:

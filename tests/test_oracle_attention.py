@@ -178,9 +178,9 @@ def test_planted_mistakes_are_caught(monkeypatch):
         return np.allclose(o, _sdpa_causal(q, k, v), atol=1e-12)
 
     mutants = {
-        "window_off_by_one": lambda qp, n, s, ns, w: good_mask(qp, n, s, ns, w + 1),
-        "sink_off_by_one": lambda qp, n, s, ns, w: good_mask(qp, n, s, ns + 1, w),
-        "no_causal_limit": lambda qp, n, s, ns, w: np.ones((len(qp), n), bool),
+        "window_off_by_one": lambda qp, n, s, ns, w, chunk=0: good_mask(qp, n, s, ns, w + 1, chunk),
+        "sink_off_by_one": lambda qp, n, s, ns, w, chunk=0: good_mask(qp, n, s, ns + 1, w, chunk),
+        "no_causal_limit": lambda qp, n, s, ns, w, chunk=0: np.ones((len(qp), n), bool),
     }
     assert agree() and hand_sets_ok() and sdpa_ok()
     for name, fn in mutants.items():
@@ -191,3 +191,51 @@ def test_planted_mistakes_are_caught(monkeypatch):
     assert not (agree() and sdpa_ok()), "interleaved GQA grouping"
     monkeypatch.setattr(A, "group_of", good_group)
     assert agree() and sdpa_ok()
+
+
+def test_chunk_eviction_hand_listed_sets():
+    # chunk K = 4, n_sink = 1, window = 2 over 12 positions, written out by hand:
+    # chunk 0 (rows 0-3) sees everything causal; chunk 1 (rows 4-7) sees the sink,
+    # tokens 2,3 (the 2 before the chunk) and its own chunk; chunk 2 sees 0, 6, 7, own.
+    want = {0: {0}, 1: {0, 1}, 2: {0, 1, 2}, 3: {0, 1, 2, 3},
+            4: {0, 2, 3, 4}, 5: {0, 2, 3, 4, 5}, 6: {0, 2, 3, 4, 5, 6}, 7: {0, 2, 3, 4, 5, 6, 7},
+            8: {0, 6, 7, 8}, 9: {0, 6, 7, 8, 9}, 10: {0, 6, 7, 8, 9, 10}, 11: {0, 6, 7, 8, 9, 10, 11}}
+    m = A.visible_mask(np.arange(12), 12, True, 1, 2, chunk=4)
+    for i in range(12):
+        assert set(np.nonzero(m[i])[0].tolist()) == want[i], i
+
+
+@pytest.mark.parametrize("n_sink,window", [(0, 1), (3, 5), (8, 40)])
+def test_chunk_of_one_is_band_one_wider(n_sink, window):
+    # evicting after every token keeps `window` tokens plus the current one
+    t = 70
+    a = A.visible_mask(np.arange(t), t, True, n_sink, window, chunk=1)
+    b = A.visible_mask(np.arange(t), t, True, n_sink, window + 1)
+    assert np.array_equal(a, b)
+
+
+def test_chunk_covering_sequence_equals_dense():
+    b, t, hq, hkv, d = 1, 50, 4, 2, 16
+    q, k, v = _rand((b, t, hq, d), 30), _rand((b, t, hkv, d), 31), _rand((b, t, hkv, d), 32)
+    o = A.prefill(q, k, v, np.ones(hkv, np.uint8), 2, 5, chunk=64)
+    np.testing.assert_allclose(o, _sdpa_causal(q, k, v), rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("chunk", [1, 3, 8, 13])
+def test_chunk_eviction_brute_force_agrees(chunk):
+    b, t, hq, hkv, d = 1, 26, 4, 2, 8
+    q, k, v = _rand((b, t, hq, d), 33), _rand((b, t, hkv, d), 34), _rand((b, t, hkv, d), 35)
+    mask = np.array([1, 0], np.uint8)
+    o = A.prefill(q, k, v, mask, 2, 4, chunk=chunk)
+    ob = A.brute_force(q, k, v, mask, 2, 4, chunk=chunk)
+    np.testing.assert_allclose(o, ob, rtol=0, atol=1e-12)
+
+
+def test_chunk_eviction_sees_superset_of_band():
+    # the chunked mask keeps the band's keys plus the rest of the chunk's window
+    t, n_sink, window = 200, 4, 16
+    for chunk in (1, 5, 16, 37):
+        band = A.visible_mask(np.arange(t), t, True, n_sink, window)
+        ch = A.visible_mask(np.arange(t), t, True, n_sink, window, chunk=chunk)
+        assert np.all(ch >= band)
+        assert ch.sum(axis=1).max() <= n_sink + window + chunk
