@@ -23,9 +23,10 @@
  *   - Streaming mask: key j is visible to the query at position i when
  *     j <= i and (j < n_sink or i - j < window).  The window includes the
  *     current token, so a streaming query sees at most n_sink + window keys.
- *     In prefill this per-token sink + band mask is used for every row (it is
- *     the chunk-size-independent form of the paper's chunked eviction and
- *     equals what decode sees).  Retrieval mask: j <= i.
+ *     aoh_prefill applies this per-token sink + band mask to every row (the
+ *     chunk-size-independent form of the paper's chunked eviction, and what
+ *     decode sees); aoh_prefill_chunked applies the chunk-eviction form with a
+ *     given chunk size.  Retrieval mask: j <= i.
  *   - Supported: dtype bf16 (fp32 accumulation and softmax) or fp32
  *     (fp32 throughout); D in {64, 128}; Hq a multiple of Hkv with
  *     Hq / Hkv <= 16; Hkv <= 64.  n_sink >= 0, window >= 1.
@@ -133,6 +134,20 @@ typedef struct {
 aoh_status aoh_prefill(const aoh_tensor* q, const aoh_tensor* k, const aoh_tensor* v,
                        const uint8_t* head_is_streaming, int32_t n_sink, int32_t window,
                        aoh_tensor* out, void* stream);
+
+/*
+ * Prefill with the paper's chunk eviction for streaming heads (Sec. 5,
+ * chunked-prefill stage): the prompt is processed in chunks of `chunk` tokens
+ * and after each chunk a streaming head keeps only its n_sink sink tokens and
+ * its `window` most recent tokens.  A query at position i, in the chunk that
+ * starts at c = (i / chunk) * chunk, therefore sees the keys j <= i with
+ * j < n_sink or j >= c - window.  Retrieval heads are unaffected.  Arguments,
+ * layouts and errors as aoh_prefill; chunk >= 1 (chunk = 1 equals the per-token
+ * band of aoh_prefill with window + 1).
+ */
+aoh_status aoh_prefill_chunked(const aoh_tensor* q, const aoh_tensor* k, const aoh_tensor* v,
+                               const uint8_t* head_is_streaming, int32_t n_sink, int32_t window,
+                               int32_t chunk, aoh_tensor* out, void* stream);
 
 /*
  * Append n_new tokens per sequence to the caches (Sec. 5: retrieval heads

@@ -4,4 +4,4 @@ The compute lives in libaoh.so (HIP kernels behind the C interface of
 include/aoh.h); ``aoh`` is its ctypes binding.
 """
 from .aoh import (AohError, PagedCache, RingCache, aoh_decode, aoh_decode_workspace_bytes,  # noqa: F401
-                  aoh_kv_append, aoh_last_error, aoh_prefill, aoh_version, lib)
+                  aoh_kv_append, aoh_last_error, aoh_prefill, aoh_prefill_chunked, aoh_version, lib)

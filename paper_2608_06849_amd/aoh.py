@@ -48,7 +48,7 @@ class AohRingCache(ctypes.Structure):
 
 _lib = None
 
-EXPORTS = ("aoh_prefill", "aoh_kv_append", "aoh_decode_workspace_bytes", "aoh_decode",
+EXPORTS = ("aoh_prefill", "aoh_prefill_chunked", "aoh_kv_append", "aoh_decode_workspace_bytes", "aoh_decode",
            "aoh_last_error", "aoh_version")
 
 
@@ -63,6 +63,10 @@ def lib():
         L.aoh_prefill.argtypes = [P(AohTensor), P(AohTensor), P(AohTensor), ctypes.c_void_p,
                                   ctypes.c_int32, ctypes.c_int32, P(AohTensor), ctypes.c_void_p]
         L.aoh_prefill.restype = ctypes.c_int
+        L.aoh_prefill_chunked.argtypes = [P(AohTensor), P(AohTensor), P(AohTensor), ctypes.c_void_p,
+                                          ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, P(AohTensor),
+                                          ctypes.c_void_p]
+        L.aoh_prefill_chunked.restype = ctypes.c_int
         L.aoh_kv_append.argtypes = [P(AohTensor), P(AohTensor), ctypes.c_void_p, ctypes.c_void_p,
                                     P(AohPagedCache), P(AohRingCache), ctypes.c_int32, ctypes.c_int32,
                                     ctypes.c_void_p]
@@ -182,6 +186,17 @@ def aoh_prefill(q, k, v, head_is_streaming, n_sink, window, out=None, stream=Non
     m = _Mask(head_is_streaming)
     _check(lib().aoh_prefill(ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), m.ptr,
                              n_sink, window, ctypes.byref(od), _stream(stream)))
+    return out
+
+
+def aoh_prefill_chunked(q, k, v, head_is_streaming, n_sink, window, chunk, out=None, stream=None):
+    """Prefill with chunk eviction of `chunk` tokens for streaming heads (see aoh.h)."""
+    if out is None:
+        out = torch.empty_like(q)
+    qd, kd, vd, od = tensor_desc(q), tensor_desc(k), tensor_desc(v), tensor_desc(out)
+    m = _Mask(head_is_streaming)
+    _check(lib().aoh_prefill_chunked(ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), m.ptr,
+                                     n_sink, window, chunk, ctypes.byref(od), _stream(stream)))
     return out
 
 

@@ -153,9 +153,9 @@ int32_t aoh_version(void) { return 100; }
 
 const char* aoh_last_error(void) { return g_err; }
 
-aoh_status aoh_prefill(const aoh_tensor* q, const aoh_tensor* k, const aoh_tensor* v,
-                       const uint8_t* head_is_streaming, int32_t n_sink, int32_t window,
-                       aoh_tensor* out, void* stream) {
+static aoh_status prefill_impl(const aoh_tensor* q, const aoh_tensor* k, const aoh_tensor* v,
+                               const uint8_t* head_is_streaming, int32_t n_sink, int32_t window,
+                               int32_t chunk, aoh_tensor* out, void* stream) {
   aoh_status st;
   if ((st = check_tensor(q, "q", 4, AOH_BF16, AOH_F32))) return st;
   const int dt = q->dtype;
@@ -189,7 +189,7 @@ aoh_status aoh_prefill(const aoh_tensor* q, const aoh_tensor* k, const aoh_tenso
   a.v_sb = v->stride[0]; a.v_st = v->stride[1]; a.v_sh = v->stride[2];
   a.o_sb = out->stride[0]; a.o_st = out->stride[1]; a.o_sh = out->stride[2];
   a.B = (int)B; a.T = (int)T; a.gs = gs;
-  a.n_sink = n_sink; a.window = window;
+  a.n_sink = n_sink; a.window = window; a.chunk = chunk;
   a.n_qblocks = (int)n_qblocks;
   a.scale = (float)(1.0 / std::sqrt((double)D));
   a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)D));
@@ -209,6 +209,19 @@ aoh_status aoh_prefill(const aoh_tensor* q, const aoh_tensor* k, const aoh_tenso
     if (e != hipSuccess) return fail(AOH_ERR_HIP, "prefill streaming launch: %s", hipGetErrorString(e));
   }
   return ok();
+}
+
+aoh_status aoh_prefill(const aoh_tensor* q, const aoh_tensor* k, const aoh_tensor* v,
+                       const uint8_t* head_is_streaming, int32_t n_sink, int32_t window,
+                       aoh_tensor* out, void* stream) {
+  return prefill_impl(q, k, v, head_is_streaming, n_sink, window, 0, out, stream);
+}
+
+aoh_status aoh_prefill_chunked(const aoh_tensor* q, const aoh_tensor* k, const aoh_tensor* v,
+                               const uint8_t* head_is_streaming, int32_t n_sink, int32_t window,
+                               int32_t chunk, aoh_tensor* out, void* stream) {
+  if (chunk < 1) return fail(AOH_ERR_INVALID_ARG, "chunk=%d must be >= 1", chunk);
+  return prefill_impl(q, k, v, head_is_streaming, n_sink, window, chunk, out, stream);
 }
 
 static aoh_status check_paged(const aoh_paged_cache* c, int n_ret, int64_t B) {

@@ -25,6 +25,7 @@ struct PrefillArgs {
   int32_t B, T, gs;      // gs = query heads per KV head
   int32_t n_kv;          // KV heads in this launch
   int32_t n_sink, window;
+  int32_t chunk;         // streaming mask: 0 = per-token band, K >= 1 = chunk eviction
   int32_t n_qblocks;     // ceil(T / rows per block)
   float scale_log2;      // log2(e) / sqrt(D)
   float scale;           // 1 / sqrt(D)

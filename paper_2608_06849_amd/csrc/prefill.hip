@@ -3,7 +3,10 @@
 // Computes, per (batch, query head, query row i), the attention of the paper's
 // Sec. 5 (chunked-prefill stage): softmax over the visible keys of
 // q_i . k_j / sqrt(D), times V.  Retrieval heads see j <= i; streaming heads
-// see j <= i with j < n_sink or i - j < window.
+// see j <= i with j < n_sink or j >= lo(i), where lo(i) = i - window + 1 for
+// the per-token band and lo(i) = floor(i / K) K - window for chunk eviction
+// with chunks of K tokens (the cache before a chunk keeps the sink and the
+// window most recent tokens; the chunk sees those and itself).
 //
 // bf16 kernel (the hot one).  One workgroup = 4 waves = 128 query rows of one
 // query head; each wave owns 32 rows.  Key/value tiles of 64 keys are staged
@@ -58,6 +61,11 @@ struct PrefillLds {
 // this, so P stays below 2^8 and the O rescale is skipped on most tiles.
 constexpr float kRescaleThreshold = 8.0f;
 
+// First non-sink key visible to row i of a streaming head (may be negative).
+__device__ __forceinline__ int lo_of(int i, int chunk, int window) {
+  return chunk ? (i / chunk) * chunk - window : i - window + 1;
+}
+
 // Tile visit plan of one query block [i0, i0 + kPrefillRows).
 struct TilePlan {
   int n_sink_tiles;  // leading sink tiles visited before the band
@@ -69,7 +77,7 @@ struct TilePlan {
 };
 
 template <bool STREAM>
-__device__ __forceinline__ TilePlan make_plan(int i0, int rows, int T, int n_sink, int window) {
+__device__ __forceinline__ TilePlan make_plan(int i0, int rows, int T, int n_sink, int window, int chunk) {
   const int last_row = min(i0 + rows - 1, T - 1);
   const int last_tile = last_row / kBN;
   TilePlan p;
@@ -78,7 +86,7 @@ __device__ __forceinline__ TilePlan make_plan(int i0, int rows, int T, int n_sin
     p.band_first = 0;
     p.n_visit = last_tile + 1;
   } else {
-    const int band_lo = max(0, i0 - window + 1);
+    const int band_lo = max(0, lo_of(i0, chunk, window));  // lo is non-decreasing in i
     p.band_first = band_lo / kBN;
     const int sink_tiles = (n_sink + kBN - 1) / kBN;
     p.n_sink_tiles = min(sink_tiles, p.band_first);
@@ -115,8 +123,12 @@ __global__ __launch_bounds__(kWaves * kWave, kRB == 1 ? 2 : 1) void prefill_bf16
   const int i0 = qb * kPrefillRows;
   const int r0 = i0 + wave * kRowsPerWave;      // first row of this wave
   int my_row[kRB];                              // row of this lane in each 32-row block
+  int my_lo[kRB];                               // its first visible non-sink key (streaming)
 #pragma unroll
-  for (int rb = 0; rb < kRB; ++rb) my_row[rb] = r0 + 32 * rb + l32;
+  for (int rb = 0; rb < kRB; ++rb) {
+    my_row[rb] = r0 + 32 * rb + l32;
+    my_lo[rb] = lo_of(my_row[rb], a.chunk, a.window);
+  }
 
   const uint16_t* qp = reinterpret_cast<const uint16_t*>(a.q) + (int64_t)b * a.q_sb + (int64_t)h * a.q_sh;
   const uint16_t* kp = reinterpret_cast<const uint16_t*>(a.k) + (int64_t)b * a.k_sb + (int64_t)g * a.k_sh;
@@ -146,7 +158,7 @@ __global__ __launch_bounds__(kWaves * kWave, kRB == 1 ? 2 : 1) void prefill_bf16
       for (int i = 0; i < 16; ++i) acc_o[rb][mb][i] = 0.f;
   }
 
-  const TilePlan plan = make_plan<STREAM>(i0, kPrefillRows, T, a.n_sink, a.window);
+  const TilePlan plan = make_plan<STREAM>(i0, kPrefillRows, T, a.n_sink, a.window, a.chunk);
 
   // Cooperative staging of one stage (kStageTiles tiles of 64 keys): global ->
   // registers -> LDS (double buffered).  Per-thread row/column are fixed, so
@@ -214,7 +226,7 @@ __global__ __launch_bounds__(kWaves * kWave, kRB == 1 ? 2 : 1) void prefill_bf16
       if (MASKED) {
         const int key = key0 + 8 * (i >> 2) + 4 * h2 + (i & 3);
         bool vis = key <= my_row[rb];
-        if (STREAM) vis = vis && (key < a.n_sink || my_row[rb] - key < a.window);
+        if (STREAM) vis = vis && (key < a.n_sink || key >= my_lo[rb]);
         x = vis ? x : -INFINITY;
         sb[i] = x;
       }
@@ -367,11 +379,11 @@ __global__ __launch_bounds__(kWaves * kWave, kRB == 1 ? 2 : 1) void prefill_bf16
         const int kb = plan.tile(it) * kBN;
         // Is any element of this wave's rows x 64 keys visible?  Is every element?
         const bool wave_dead = (kb > r0 + kRowsPerWave - 1) ||
-                               (STREAM && kb >= a.n_sink && (r0 - (kb + kBN - 1)) >= a.window);
+                               (STREAM && kb >= a.n_sink && kb + kBN - 1 < lo_of(r0, a.chunk, a.window));
         if (!wave_dead) {
-          const bool need_mask = (kb + kBN - 1 > r0) ||
-                                 (STREAM && !(kb + kBN - 1 < a.n_sink ||
-                                              (r0 + kRowsPerWave - 1) - kb < a.window));
+          const bool need_mask =
+              (kb + kBN - 1 > r0) ||
+              (STREAM && !(kb + kBN - 1 < a.n_sink || kb >= lo_of(r0 + kRowsPerWave - 1, a.chunk, a.window)));
           if (need_mask) tile_step(buf, u, kb, std::true_type{});
           else tile_step(buf, u, kb, std::false_type{});
         }
@@ -450,7 +462,7 @@ __global__ __launch_bounds__(kPrefillRowsF32) void prefill_f32_kernel(PrefillArg
   float m = -INFINITY, l = 0.f;
   int lo = 0, sink_end = 0;
   if (STREAM) {
-    lo = max(0, i - a.window + 1);
+    lo = max(0, lo_of(i, a.chunk, a.window));
     sink_end = min(a.n_sink, lo);
   }
   auto visit = [&](int j) {

@@ -107,6 +107,22 @@ def test_prefill_validation(case, status, msg):
     assert msg in err
 
 
+@pytest.mark.parametrize("chunk,status,msg", [
+    (0, A.AOH_ERR_INVALID_ARG, "chunk"),
+    (-3, A.AOH_ERR_INVALID_ARG, "chunk"),
+    (64, A.AOH_ERR_INVALID_ARG, "window"),   # chunk valid, window 0 still rejected
+])
+def test_prefill_chunked_validation(chunk, status, msg):
+    q, k, v, out = _good()
+    buf = ctypes.create_string_buffer(b"\x00\x01", 2)
+    st = A.lib().aoh_prefill_chunked(ctypes.byref(q), ctypes.byref(k), ctypes.byref(v),
+                                     ctypes.cast(buf, ctypes.c_void_p), 4, 0 if chunk == 64 else 32, chunk,
+                                     ctypes.byref(out), None)
+    err = A.aoh_last_error()
+    assert st == status, err
+    assert msg in err
+
+
 def test_decode_workspace_size_and_checks():
     L = A.lib()
     n = A.aoh_decode_workspace_bytes(8, 32, 128, 8196, 1088)

@@ -7,7 +7,7 @@ import torch
 
 import synth
 from oracle import attention as OA
-from paper_2608_06849_amd import aoh_prefill
+from paper_2608_06849_amd import aoh_prefill, aoh_prefill_chunked
 from tests.helpers import assert_parity, bits, f64, to_dtype
 
 pytestmark = pytest.mark.gpu
@@ -105,5 +105,44 @@ def test_deterministic():
     q, k, v = _inputs(1, 777, 8, 2, 128, torch.bfloat16, seed=9)
     a = aoh_prefill(q, k, v, [0, 1], 4, 50)
     b = aoh_prefill(q, k, v, [0, 1], 4, 50)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits(a), bits(b))
+
+
+CHUNK_CASES = [
+    # B, T, Hq, Hkv, D, mask, n_sink, window, chunk
+    (1, 700, 8, 2, 128, [1, 0], 4, 100, 1),       # one-token chunks
+    (2, 300, 8, 2, 128, [0, 1], 4, 32, 7),        # chunk not a divisor of any tile size
+    (1, 1000, 14, 2, 128, [1, 1], 64, 128, 64),   # chunk = a quarter of a query block
+    (1, 1300, 4, 4, 64, [1, 0, 1, 1], 0, 50, 100),
+    (1, 2500, 4, 1, 128, [1], 16, 256, 1024),     # chunk spans four query blocks
+    (1, 513, 4, 2, 128, [1, 0], 8, 64, 600),      # one chunk covers the prompt -> dense
+    (1, 1, 4, 2, 128, [1, 0], 4, 32, 16),         # single token
+]
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+@pytest.mark.parametrize("B,T,Hq,Hkv,D,mask,n_sink,window,chunk", CHUNK_CASES)
+def test_chunked_prefill_matches_oracle(B, T, Hq, Hkv, D, mask, n_sink, window, chunk, dtype):
+    q, k, v = _inputs(B, T, Hq, Hkv, D, dtype, seed=T * 5 + chunk)
+    out = aoh_prefill_chunked(q, k, v, mask, n_sink, window, chunk)
+    torch.cuda.synchronize()
+    want = OA.prefill(f64(q), f64(k), f64(v), mask, n_sink, window, chunk=chunk)
+    assert_parity(out, want, dtype, f"chunked prefill {B,T,Hq,Hkv,D,mask,n_sink,window,chunk}")
+
+
+def test_chunk_one_equals_band_one_wider():
+    # with one-token chunks a query sees the window tokens before it plus itself
+    q, k, v = _inputs(1, 900, 8, 2, 128, torch.bfloat16, seed=21)
+    a = aoh_prefill_chunked(q, k, v, [1, 0], 4, 63, 1)
+    b = aoh_prefill(q, k, v, [1, 0], 4, 64)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits(a), bits(b))
+
+
+def test_chunk_at_least_prompt_is_full_causal():
+    q, k, v = _inputs(1, 600, 4, 2, 128, torch.bfloat16, seed=22)
+    a = aoh_prefill_chunked(q, k, v, [1, 1], 4, 32, 600)
+    b = aoh_prefill(q, k, v, [0, 0], 4, 32)
     torch.cuda.synchronize()
     assert np.array_equal(bits(a), bits(b))
