@@ -195,6 +195,49 @@ aoh_status aoh_decode(const aoh_tensor* q, const aoh_paged_cache* kv_full,
                       const int32_t* lens, int32_t n_sink, int32_t window, aoh_tensor* out,
                       void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * The AoH head classifier (Sec. 4, Eqs. 2-7 and Algorithm 1; group-level
+ * classification in the "GQA Extension" appendix).  It is offline work: it
+ * produces the head_is_streaming arrays that the calls above take.
+ *
+ * For query head h of layer l, with KV group g = h / (Hq/Hkv), the score is
+ * the effective rank of the kernel attention matrix M_h = W_K^g^T W_Q^h:
+ *   sigma_k = sqrt(max(lambda_k((W_Q W_Q^T)(W_K W_K^T)), 0)),
+ *   p_k = sigma_k / sum_j sigma_j,  eff_rank = exp(-sum_{p_k > 0} p_k log p_k).
+ * A group's score is the mean of its query heads' scores; in every layer the
+ * n_retrieval groups with the lowest scores are retrieval groups (0), the rest
+ * streaming (1).  On equal scores the lower group index is taken first, so
+ * exactly n_retrieval groups are retrieval (the paper's k = ceil((1 - s) G)
+ * for a target sparsity s is the caller's choice of n_retrieval).
+ *
+ *   w_q: [L][Hq * d_head][d_model] bf16, DEVICE; query head h owns rows
+ *        h*d_head .. h*d_head + d_head - 1 of each layer (PyTorch Linear
+ *        weight layout: output features x input features).
+ *   w_k: [L][Hkv * d_head][d_model] bf16, DEVICE; group g owns rows likewise.
+ *   d_head in {64, 128}; d_model a multiple of 64; Hq a multiple of Hkv;
+ *   Hkv <= 64; 0 <= n_retrieval <= Hkv.
+ *   head_rank:         DEVICE double [L][Hq]   (written)
+ *   group_score:       DEVICE double [L][Hkv]  (written)
+ *   head_is_streaming: DEVICE uint8  [L][Hkv]  (written, 0/1)
+ *   workspace: DEVICE, at least aoh_classify_workspace_bytes(L, Hq, Hkv,
+ *   d_head) bytes, 16-byte aligned, caller-owned scratch.
+ * The Gram matrices W W^T are formed from the bf16 weights with fp32
+ * accumulation; everything after them is fp64.  Errors as for the calls above.
+ */
+size_t aoh_classify_workspace_bytes(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, int32_t d_head);
+
+/*
+ * Retrieval groups per layer for a target sparsity s in [0, 1]:
+ * k = ceil((1 - s) G) (Sec. 4, group-level classification), with products
+ * that land within 1e-9 G above an integer rounded down to it.  Returns -1 for
+ * invalid arguments (message in aoh_last_error).
+ */
+int32_t aoh_retrieval_group_count(int32_t n_kv_heads, double sparsity);
+
+aoh_status aoh_classify(const aoh_tensor* w_q, const aoh_tensor* w_k, int32_t d_head, int32_t n_retrieval,
+                        double* head_rank, double* group_score, uint8_t* head_is_streaming,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
 /* Message for the last non-OK status returned on this thread ("" if none). */
 const char* aoh_last_error(void);
 

@@ -13,8 +13,10 @@ Modules
                  ring, and the expected cache image after a series of appends.
   accounting  -- visible-pair counts, FLOP/byte counts and the KV-cache bytes
                  formula that reproduces the paper's memory tables.
+  classifier  -- the effective-rank head classifier (proxy spectrum, effective
+                 rank, group mean, lowest-k retrieval selection).
 
 Parity status of each function is stated in its docstring; every function is
 pinned by a ``-m "not gpu"`` test (see tests/test_oracle_*.py).
 """
-from . import attention, cache_model, accounting  # noqa: F401
+from . import attention, cache_model, accounting, classifier  # noqa: F401

@@ -49,6 +49,7 @@ class AohRingCache(ctypes.Structure):
 _lib = None
 
 EXPORTS = ("aoh_prefill", "aoh_prefill_chunked", "aoh_kv_append", "aoh_decode_workspace_bytes", "aoh_decode",
+           "aoh_classify_workspace_bytes", "aoh_classify", "aoh_retrieval_group_count",
            "aoh_last_error", "aoh_version")
 
 
@@ -77,6 +78,14 @@ def lib():
                                  ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, P(AohTensor),
                                  ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
         L.aoh_decode.restype = ctypes.c_int
+        L.aoh_classify_workspace_bytes.argtypes = [ctypes.c_int32] * 4
+        L.aoh_classify_workspace_bytes.restype = ctypes.c_size_t
+        L.aoh_classify.argtypes = [P(AohTensor), P(AohTensor), ctypes.c_int32, ctypes.c_int32,
+                                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                   ctypes.c_size_t, ctypes.c_void_p]
+        L.aoh_classify.restype = ctypes.c_int
+        L.aoh_retrieval_group_count.argtypes = [ctypes.c_int32, ctypes.c_double]
+        L.aoh_retrieval_group_count.restype = ctypes.c_int32
         L.aoh_last_error.argtypes = []
         L.aoh_last_error.restype = ctypes.c_char_p
         L.aoh_version.argtypes = []
@@ -233,6 +242,41 @@ def aoh_decode(q, kv_full, kv_ring, head_is_streaming, lens, n_sink, window, out
                             _ptr(lens), n_sink, window, ctypes.byref(od), ctypes.c_void_p(ws_ptr),
                             ws_bytes, _stream(stream)))
     return out
+
+
+def aoh_classify_workspace_bytes(n_layers, n_q_heads, n_kv_heads, d_head):
+    return int(lib().aoh_classify_workspace_bytes(n_layers, n_q_heads, n_kv_heads, d_head))
+
+
+def aoh_retrieval_group_count(n_kv_heads, sparsity):
+    """Retrieval groups per layer for a target sparsity s (the library's ceil((1 - s) G))."""
+    k = int(lib().aoh_retrieval_group_count(n_kv_heads, float(sparsity)))
+    if k < 0:
+        raise AohError(AOH_ERR_INVALID_ARG, aoh_last_error())
+    return k
+
+
+def aoh_classify(w_q, w_k, d_head, n_retrieval, head_rank=None, group_score=None, head_is_streaming=None,
+                 workspace=None, stream=None):
+    """Head classification of every layer: w_q [L, Hq*d_head, d_model], w_k
+    [L, Hkv*d_head, d_model] (bf16, device).  Returns (head_rank [L, Hq] f64,
+    group_score [L, Hkv] f64, head_is_streaming [L, Hkv] u8), device tensors."""
+    L, hq, hkv = w_q.shape[0], w_q.shape[1] // d_head, w_k.shape[1] // d_head
+    dev = w_q.device
+    if head_rank is None:
+        head_rank = torch.empty((L, hq), dtype=torch.float64, device=dev)
+    if group_score is None:
+        group_score = torch.empty((L, hkv), dtype=torch.float64, device=dev)
+    if head_is_streaming is None:
+        head_is_streaming = torch.empty((L, hkv), dtype=torch.uint8, device=dev)
+    if workspace is None:
+        n = aoh_classify_workspace_bytes(L, hq, hkv, d_head)
+        workspace = torch.empty(max(n, 16), dtype=torch.uint8, device=dev)
+    qd, kd = tensor_desc(w_q), tensor_desc(w_k)
+    _check(lib().aoh_classify(ctypes.byref(qd), ctypes.byref(kd), d_head, n_retrieval, _ptr(head_rank),
+                              _ptr(group_score), _ptr(head_is_streaming), _ptr(workspace),
+                              workspace.numel() * workspace.element_size(), _stream(stream)))
+    return head_rank, group_score, head_is_streaming
 
 
 def aoh_last_error():

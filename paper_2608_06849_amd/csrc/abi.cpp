@@ -404,4 +404,68 @@ aoh_status aoh_decode(const aoh_tensor* q, const aoh_paged_cache* kv_full,
   return ok();
 }
 
+static size_t classify_ws(int64_t L, int64_t hq, int64_t hkv, int64_t d) {
+  const size_t gram = (size_t)(L * (hq + hkv) * d * d) * sizeof(float);
+  return gram + (size_t)(L * hkv * d * d) * sizeof(double);
+}
+
+int32_t aoh_retrieval_group_count(int32_t n_kv_heads, double sparsity) {
+  if (n_kv_heads < 1 || !(sparsity >= 0.0 && sparsity <= 1.0)) {
+    fail(AOH_ERR_INVALID_ARG, "need n_kv_heads >= 1 and 0 <= sparsity <= 1");
+    return -1;
+  }
+  // k = ceil((1 - s) G); the small offset keeps e.g. (1 - 0.7) * 10 = 3.0000000000000004 at 3
+  const double x = (1.0 - sparsity) * n_kv_heads;
+  return (int32_t)std::ceil(x - 1e-9 * n_kv_heads);
+}
+
+size_t aoh_classify_workspace_bytes(int32_t n_layers, int32_t n_q_heads, int32_t n_kv_heads, int32_t d_head) {
+  if (n_layers < 1 || n_q_heads < 1 || n_kv_heads < 1 || (d_head != 64 && d_head != 128)) return 0;
+  return classify_ws(n_layers, n_q_heads, n_kv_heads, d_head);
+}
+
+aoh_status aoh_classify(const aoh_tensor* w_q, const aoh_tensor* w_k, int32_t d_head, int32_t n_retrieval,
+                        double* head_rank, double* group_score, uint8_t* head_is_streaming,
+                        void* workspace, size_t workspace_bytes_given, void* stream) {
+  aoh_status st;
+  if ((st = check_tensor(w_q, "w_q", 3, AOH_BF16, AOH_BF16))) return st;
+  if ((st = check_tensor(w_k, "w_k", 3, AOH_BF16, AOH_BF16))) return st;
+  if (d_head != 64 && d_head != 128) return fail(AOH_ERR_UNSUPPORTED, "d_head=%d; supported: 64, 128", d_head);
+  const int64_t L = w_q->shape[0], dm = w_q->shape[2];
+  if (w_k->shape[0] != L || w_k->shape[2] != dm)
+    return fail(AOH_ERR_INVALID_ARG, "w_q and w_k must have the same layers and d_model");
+  if (w_q->shape[1] % d_head || w_k->shape[1] % d_head)
+    return fail(AOH_ERR_INVALID_ARG, "rows of w_q / w_k must be a multiple of d_head");
+  const int64_t Hq = w_q->shape[1] / d_head, Hkv = w_k->shape[1] / d_head;
+  if (Hq % Hkv) return fail(AOH_ERR_UNSUPPORTED, "Hq=%lld is not a multiple of Hkv=%lld", (long long)Hq, (long long)Hkv);
+  if (Hkv > kMaxKvHeads) return fail(AOH_ERR_UNSUPPORTED, "Hkv=%lld > %d", (long long)Hkv, kMaxKvHeads);
+  if (dm % 64) return fail(AOH_ERR_UNSUPPORTED, "d_model=%lld must be a multiple of 64", (long long)dm);
+  if (n_retrieval < 0 || n_retrieval > Hkv)
+    return fail(AOH_ERR_INVALID_ARG, "n_retrieval=%d outside [0, %lld]", n_retrieval, (long long)Hkv);
+  if (!head_rank || !group_score || !head_is_streaming)
+    return fail(AOH_ERR_INVALID_ARG, "null output pointer");
+  if (reinterpret_cast<uintptr_t>(head_rank) % 8 || reinterpret_cast<uintptr_t>(group_score) % 8)
+    return fail(AOH_ERR_INVALID_ARG, "head_rank / group_score must be 8-byte aligned");
+  if (L * (Hq + Hkv) >= (1ll << 31)) return fail(AOH_ERR_UNSUPPORTED, "too many layers");
+  const size_t need = classify_ws(L, Hq, Hkv, d_head);
+  if (!workspace) return fail(AOH_ERR_WORKSPACE, "workspace is null; %zu bytes needed", need);
+  if (workspace_bytes_given < need)
+    return fail(AOH_ERR_WORKSPACE, "workspace has %zu bytes; %zu needed", workspace_bytes_given, need);
+  if (reinterpret_cast<uintptr_t>(workspace) % 16) return fail(AOH_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
+
+  ClassifyArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.wq = w_q->data; a.wq_sl = w_q->stride[0]; a.wq_sr = w_q->stride[1];
+  a.wk = w_k->data; a.wk_sl = w_k->stride[0]; a.wk_sr = w_k->stride[1];
+  a.L = (int)L; a.Hq = (int)Hq; a.Hkv = (int)Hkv; a.gs = (int)(Hq / Hkv);
+  a.d_model = (int)dm; a.n_retrieval = n_retrieval;
+  a.gram = reinterpret_cast<float*>(workspace);
+  a.chol = reinterpret_cast<double*>(reinterpret_cast<char*>(workspace) +
+                                     (size_t)(L * (Hq + Hkv) * d_head * d_head) * sizeof(float));
+  a.head_rank = head_rank; a.group_score = group_score; a.head_is_streaming = head_is_streaming;
+  hipError_t e = launch_classify(a, d_head, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(AOH_ERR_HIP, "classify launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
 }  // extern "C"

@@ -107,6 +107,23 @@ struct AppendArgs {
   uint8_t rank[kMaxKvHeads];    // rank of each KV head inside its cache
 };
 
+// The head classifier over L layers.  Weights are bf16 [L][H * D][d_model]
+// slices (layer stride *_sl, row stride *_sr, unit column stride).
+struct ClassifyArgs {
+  const void* wq;
+  const void* wk;
+  int64_t wq_sl, wq_sr;
+  int64_t wk_sl, wk_sr;
+  int32_t L, Hq, Hkv, gs;
+  int32_t d_model;             // multiple of 64
+  int32_t n_retrieval;         // retrieval groups per layer
+  float* gram;                 // workspace [L][Hq + Hkv][D][D]
+  double* chol;                // workspace [L][Hkv][D][D]
+  double* head_rank;           // [L][Hq]
+  double* group_score;         // [L][Hkv]
+  uint8_t* head_is_streaming;  // [L][Hkv]
+};
+
 // Launchers (return the launch status; no synchronisation).
 hipError_t launch_prefill(const PrefillArgs& a, int dtype, int out_f32, int d, bool streaming,
                           hipStream_t s);
@@ -114,6 +131,7 @@ hipError_t launch_decode_split(const DecodeArgs& a, int d, hipStream_t s);
 hipError_t launch_decode_merge(const MergeArgs& a, int dtype, int out_f32, int d, hipStream_t s);
 hipError_t launch_decode_f32(const DecodeArgs& a, int d, void* out, int64_t o_sb, int64_t o_sh, hipStream_t s);
 hipError_t launch_append(const AppendArgs& a, int dtype, int d, hipStream_t s);
+hipError_t launch_classify(const ClassifyArgs& a, int d, hipStream_t s);
 
 // Largest number of splits per (sequence, head) the merge pass accepts.
 constexpr int kMaxSplits = 1024;

@@ -108,6 +108,10 @@ CONFIGS = {
     "varlen_sweep": dict(n_seq=16, len_lo=4096, len_hi=65536, hq=32, hkv=8, d=128, dtype="bf16",
                          sparsity_pct=[25, 50, 75], windows=[512, 4096], n_sink=64, needles=8,
                          decode_steps=32, seed=4),
+    # Projection weights for the head classifier (bf16, PyTorch Linear layout).
+    "classify_tiny": dict(layers=2, hq=4, hkv=2, d=64, d_model=256, sparsity=0.5, seed=5),
+    "qwen25_classify": dict(layers=28, hq=28, hkv=4, d=128, d_model=3584, sparsity=0.5, seed=6),
+    "llama31_classify": dict(layers=32, hq=32, hkv=8, d=128, d_model=4096, sparsity=0.5, seed=7),
 }
 
 
@@ -205,3 +209,20 @@ def sweep_sequence(b, length):
     v = gaussian_bthd(1, length, hkv, d, seed * 1000 + b, "v")
     needles = plant_needles(k, [length], c["needles"], c["n_sink"], max(c["windows"]), seed, seq_ids=[b])
     return dict(q=q, k=k, v=v, needles=needles[0])
+
+
+def projection_weights(name, layer):
+    """W_Q [hq * d, d_model] and W_K [hkv * d, d_model] (float32) of one layer
+    of a classifier workload.  Every head's d x d_model slice is a Gaussian
+    matrix / sqrt(d_model) whose row r is scaled by (r + 1) ** -alpha, with
+    alpha ~ U[0.05, 1.2] drawn per (layer, head), so the heads' spectra range
+    from nearly flat to steeply decaying.  Keys (seed, "wq"/"wk", layer, head)."""
+    c = CONFIGS[name]
+    d, dm = c["d"], c["d_model"]
+    out = []
+    for kind, n in (("wq", c["hq"]), ("wk", c["hkv"])):
+        w = gaussian_blocks((n, d, dm), c["seed"] * 1000 + layer, kind, 1, scale=dm ** -0.5)
+        alpha = rng(c["seed"], kind + "-alpha", layer).uniform(0.05, 1.2, n)
+        w *= (np.arange(1, d + 1)[None, :, None] ** -alpha[:, None, None]).astype(np.float32)
+        out.append(w.reshape(n * d, dm))
+    return out[0], out[1]

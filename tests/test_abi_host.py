@@ -171,3 +171,62 @@ def test_append_validation():
     st = L.aoh_kv_append(ctypes.byref(k), ctypes.byref(v), ctypes.cast(mask, ctypes.c_void_p),
                          None, ctypes.byref(full), ctypes.byref(ring), 4, 32, None)
     assert st == A.AOH_ERR_INVALID_ARG and "start_pos" in A.aoh_last_error()
+
+
+def _classify(wq, wk, d_head=64, k=1, ws=FAKE, ws_bytes=1 << 40, outs=(FAKE, FAKE, FAKE)):
+    st = A.lib().aoh_classify(ctypes.byref(wq), ctypes.byref(wk), d_head, k,
+                              *[ctypes.c_void_p(o) for o in outs], ctypes.c_void_p(ws), ws_bytes, None)
+    return st, A.aoh_last_error()
+
+
+@pytest.mark.parametrize("case,status,msg", [
+    ("f32", A.AOH_ERR_UNSUPPORTED, "dtype"),
+    ("d96", A.AOH_ERR_UNSUPPORTED, "d_head"),
+    ("rows", A.AOH_ERR_INVALID_ARG, "multiple of d_head"),
+    ("gqa", A.AOH_ERR_UNSUPPORTED, "multiple"),
+    ("dmodel", A.AOH_ERR_UNSUPPORTED, "multiple of 64"),
+    ("layers", A.AOH_ERR_INVALID_ARG, "same layers"),
+    ("k_big", A.AOH_ERR_INVALID_ARG, "n_retrieval"),
+    ("k_neg", A.AOH_ERR_INVALID_ARG, "n_retrieval"),
+    ("no_ws", A.AOH_ERR_WORKSPACE, "null"),
+    ("small_ws", A.AOH_ERR_WORKSPACE, "needed"),
+    ("null_out", A.AOH_ERR_INVALID_ARG, "null output"),
+])
+def test_classify_validation(case, status, msg):
+    wq, wk = _t((2, 4 * 64, 256)), _t((2, 2 * 64, 256))
+    kw = {}
+    if case == "f32":
+        wq = _t((2, 4 * 64, 256), dtype=A.AOH_F32)
+    elif case == "d96":
+        kw["d_head"] = 96
+    elif case == "rows":
+        wq = _t((2, 4 * 64 + 8, 256))
+    elif case == "gqa":
+        wq = _t((2, 3 * 64, 256))
+    elif case == "dmodel":
+        wq, wk = _t((2, 4 * 64, 200)), _t((2, 2 * 64, 200))
+    elif case == "layers":
+        wk = _t((3, 2 * 64, 256))
+    elif case == "k_big":
+        kw["k"] = 3
+    elif case == "k_neg":
+        kw["k"] = -1
+    elif case == "no_ws":
+        kw["ws"] = 0
+    elif case == "small_ws":
+        kw["ws_bytes"] = A.aoh_classify_workspace_bytes(2, 4, 2, 64) - 1
+    elif case == "null_out":
+        kw["outs"] = (FAKE, 0, FAKE)
+    st, err = _classify(wq, wk, **kw)
+    assert st == status, err
+    assert msg in err
+
+
+def test_classify_workspace_and_group_count():
+    assert A.aoh_classify_workspace_bytes(28, 28, 4, 128) == 28 * 32 * 128 * 128 * 4 + 28 * 4 * 128 * 128 * 8
+    assert A.aoh_classify_workspace_bytes(1, 4, 2, 96) == 0
+    from oracle import accounting as ACC
+    for g in (1, 2, 4, 8, 10, 28, 64):
+        for s in (0.0, 0.1, 0.25, 0.3, 0.5, 0.7, 0.75, 0.9, 1.0):
+            assert A.aoh_retrieval_group_count(g, s) == ACC.n_retrieval_groups(g, s), (g, s)
+    assert A.lib().aoh_retrieval_group_count(4, 1.5) == -1
