@@ -98,39 +98,14 @@ __global__ __launch_bounds__(64 * (D / 32)) void gram_kernel(ClassifyArgs a) {
 constexpr int kEigThreads = 256;
 constexpr int kEigWaves = kEigThreads / kWave;
 
-// Right-looking Cholesky of G_K (fp64, in LDS).  A pivot <= 0 (W_K of lower
-// rank than d_head, up to rounding) zeroes its column, which keeps L L^T equal
-// to G_K on the range of W_K.
-template <int D>
-__global__ __launch_bounds__(kEigThreads) void chol_kernel(ClassifyArgs a) {
-  __shared__ double A[D][D + 1];
-  const int n_heads = a.Hq + a.Hkv;
-  const int grp = blockIdx.x % a.Hkv;
-  const int layer = blockIdx.x / a.Hkv;
-  const float* g = a.gram + ((int64_t)layer * n_heads + a.Hq + grp) * D * D;
-  const int t = threadIdx.x;
-  for (int e = t; e < D * D; e += kEigThreads) A[e / D][e % D] = (double)g[e];
-  __syncthreads();
-  for (int k = 0; k < D; ++k) {
-    const double dkk = A[k][k];
-    const double lkk = dkk > 0.0 ? sqrt(dkk) : 0.0;
-    const double inv = lkk > 0.0 ? 1.0 / lkk : 0.0;
-    for (int i = k + 1 + t; i < D; i += kEigThreads) A[i][k] *= inv;
-    __syncthreads();
-    if (t == 0) A[k][k] = lkk;
-    // trailing update of the lower triangle: rows i > k, columns k < j <= i
-    const int wave = t >> 6, lane = t & 63;
-    for (int i = k + 1 + wave; i < D; i += kEigWaves) {
-      const double lik = A[i][k];
-      for (int j = k + 1 + lane; j <= i; j += kWave) A[i][j] -= lik * A[j][k];
-    }
-    __syncthreads();
-  }
-  double* out = a.chol + ((int64_t)layer * a.Hkv + grp) * D * D;
-  for (int e = t; e < D * D; e += kEigThreads) {
-    const int i = e / D, j = e % D;
-    out[e] = j <= i ? A[i][j] : 0.0;
-  }
+// DPP move of a double (both 32-bit halves take the same lane pattern); lanes
+// outside row_mask receive 0.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ double dpp_f64(double v) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)u, CTRL, ROW_MASK, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(u >> 32), CTRL, ROW_MASK, 0xf, false);
+  return __builtin_bit_cast(double, ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
 }
 
 __device__ __forceinline__ double wave_sum_f64(double v) {
@@ -139,27 +114,89 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
   return v;
 }
 
-// Number of eigenvalues of the symmetric tridiagonal (d, e) below x (Sturm
-// count from the LDL^T pivots; a pivot smaller than pivmin in magnitude is
-// replaced by -pivmin).
+// The fp64 D x D matrices of the two kernels below live in registers: row i
+// belongs to the TPR = 256 / D adjacent threads t = TPR * i ... TPR * i + TPR - 1,
+// each holding CPT = D / TPR consecutive columns.  By symmetry a row doubles
+// as a column, so each elimination step publishes one row through LDS and
+// every update is local to its owner.
+
+// Right-looking Cholesky of G_K = L L^T.  Step k: the owners of row k publish
+// it, every thread takes pivot and multiplier from it, writes its element of
+// column k of L and updates its own row.  A pivot <= 0 (W_K of lower rank
+// than d_head, up to rounding) zeroes its column, which keeps L L^T equal to
+// G_K on the range of W_K.  The update runs over whole rows: left of the
+// pivot the published row holds entries already eliminated to rounding level,
+// which only touch columns that are not read again.
 template <int D>
-__device__ __forceinline__ int sturm_count(const double* d, const double* e2, double x, double pivmin) {
-  double q = d[0] - x;
-  if (fabs(q) < pivmin) q = -pivmin;
-  int c = q < 0.0;
-  for (int i = 1; i < D; ++i) {
-    q = (d[i] - x) - e2[i - 1] / q;
-    if (fabs(q) < pivmin) q = -pivmin;
-    c += q < 0.0;
+__global__ __launch_bounds__(kEigThreads) void chol_kernel(ClassifyArgs a) {
+  constexpr int TPR = kEigThreads / D, CPT = D / TPR;
+  __shared__ double rowbuf[2][D];
+  const int n_heads = a.Hq + a.Hkv;
+  const int grp = blockIdx.x % a.Hkv;
+  const int layer = blockIdx.x / a.Hkv;
+  const float* g = a.gram + ((int64_t)layer * n_heads + a.Hq + grp) * D * D;
+  double* out = a.chol + ((int64_t)layer * a.Hkv + grp) * D * D;
+  const int t = threadIdx.x;
+  const int i = t / TPR, base = (t % TPR) * CPT;
+  double r[CPT];
+#pragma unroll
+  for (int c = 0; c < CPT; ++c) r[c] = (double)g[(int64_t)i * D + base + c];
+  for (int k = 0; k < D; ++k) {
+    double* rb = rowbuf[k & 1];
+    if (i == k)
+#pragma unroll
+      for (int c = 0; c < CPT; ++c) rb[base + c] = r[c];
+    __syncthreads();
+    const double piv = rb[k];
+    const double aik = rb[i];
+    const bool live = piv > 0.0 && i > k;
+    const double lkk = piv > 0.0 ? sqrt(piv) : 0.0;
+    if (t % TPR == 0) out[(int64_t)i * D + k] = live ? aik / lkk : (i == k ? lkk : 0.0);
+    const double s = live ? aik / piv : 0.0;  // L[i][k] / L[k][k]
+#pragma unroll
+    for (int c = 0; c < CPT; ++c) r[c] = fma(-s, rb[base + c], r[c]);
   }
-  return c;
+}
+
+// Counts of eigenvalues of the symmetric tridiagonal (d, e2 = e^2) below x0
+// and x1 (Sturm counts from the LDL^T pivots q, two independent chains).  A
+// pivot smaller than pivmin in magnitude is replaced by -pivmin.  1/q is the
+// hardware reciprocal refined by one Newton step; the count is backward
+// stable, so its rounding only perturbs d and e by a few ulps.
+template <int D>
+__device__ __forceinline__ void sturm_count2(const double* d, const double* e2, double x0, double x1,
+                                             double pivmin, int& c0, int& c1) {
+  double q0 = d[0] - x0, q1 = d[0] - x1;
+  q0 = fabs(q0) < pivmin ? -pivmin : q0;
+  q1 = fabs(q1) < pivmin ? -pivmin : q1;
+  int n0 = q0 < 0.0, n1 = q1 < 0.0;
+  for (int i = 1; i < D; ++i) {
+    const double di = d[i], ei = e2[i - 1];
+    double r0 = __builtin_amdgcn_rcp(q0), r1 = __builtin_amdgcn_rcp(q1);
+    r0 = fma(r0, fma(-q0, r0, 1.0), r0);
+    r1 = fma(r1, fma(-q1, r1, 1.0), r1);
+    q0 = fma(-ei, r0, di - x0);
+    q1 = fma(-ei, r1, di - x1);
+    q0 = fabs(q0) < pivmin ? -pivmin : q0;
+    q1 = fabs(q1) < pivmin ? -pivmin : q1;
+    n0 += q0 < 0.0;
+    n1 += q1 < 0.0;
+  }
+  c0 = n0;
+  c1 = n1;
 }
 
 template <int D>
-__global__ __launch_bounds__(kEigThreads) void spectrum_kernel(ClassifyArgs a) {
-  constexpr int R = D / 16;  // rows and columns per thread in the fp64 products
-  __shared__ double A[D][D + 1];
-  __shared__ double vv[D], pp[D], dd[D], ee[D];
+__global__ __launch_bounds__(kEigThreads, 2) void spectrum_kernel(ClassifyArgs a) {
+  constexpr int TPR = kEigThreads / D, CPT = D / TPR;
+  constexpr int JC = 64;               // columns per chunk of the congruence products
+  constexpr int NJ = D / JC;
+  constexpr int RT = D / 16, CT = JC / 16;  // chunk tile per thread
+  constexpr int SIDES = kEigThreads / D;    // threads per eigenvalue in the bisection
+  constexpr int NPT = 2 * SIDES;            // points per bisection round
+  __shared__ double buf[D][JC + 1];
+  __shared__ double rowbuf[2][D], vbuf[2][D], pp[2][D];
+  __shared__ double dd[D], ee[D];
   __shared__ double red[kEigWaves];
 
   const int n_heads = a.Hq + a.Hkv;
@@ -170,148 +207,192 @@ __global__ __launch_bounds__(kEigThreads) void spectrum_kernel(ClassifyArgs a) {
   const double* L = a.chol + ((int64_t)layer * a.Hkv + grp) * D * D;
   const int t = threadIdx.x;
   const int wave = t >> 6, lane = t & 63;
+  const int i = t / TPR, base = (t % TPR) * CPT;  // row owned in the register layout
 
-  for (int e = t; e < D * D; e += kEigThreads) A[e / D][e % D] = (double)qq[e];
-  __syncthreads();
-
-  // T = QQ L  (thread tile: rows R*(t/16) + r, columns t%16 + 16c)
-  const int r0 = R * (t / 16), c0 = t % 16;
-  double acc[R][R];
+  // B = L^T (QQ L), one chunk of JC columns at a time: T = QQ L[:, J] in
+  // registers, through LDS, then B[:, J] = L^T T; the chunk of B goes to its
+  // row owners' registers.  QQ is exactly symmetric, so row k of QQ serves as
+  // its column k.
+  double arow[CPT];
+  const int rg = t / 16, c16 = t % 16;
 #pragma unroll
-  for (int r = 0; r < R; ++r)
+  for (int J = 0; J < NJ; ++J) {
+    double acc[RT][CT];
 #pragma unroll
-    for (int c = 0; c < R; ++c) acc[r][c] = 0.0;
-  for (int k = 0; k < D; ++k) {
-    double lk[R], ar[R];
+    for (int r = 0; r < RT; ++r)
 #pragma unroll
-    for (int c = 0; c < R; ++c) lk[c] = L[(int64_t)k * D + c0 + 16 * c];
+      for (int c = 0; c < CT; ++c) acc[r][c] = 0.0;
+    for (int k = 0; k < D; ++k) {
+      double qk[RT], lk[CT];
 #pragma unroll
-    for (int r = 0; r < R; ++r) ar[r] = A[r0 + r][k];
+      for (int r = 0; r < RT; ++r) qk[r] = (double)qq[(int64_t)k * D + rg * RT + r];
 #pragma unroll
-    for (int r = 0; r < R; ++r)
+      for (int c = 0; c < CT; ++c) lk[c] = L[(int64_t)k * D + J * JC + c16 + 16 * c];
 #pragma unroll
-      for (int c = 0; c < R; ++c) acc[r][c] = fma(ar[r], lk[c], acc[r][c]);
-  }
-  __syncthreads();
+      for (int r = 0; r < RT; ++r)
 #pragma unroll
-  for (int r = 0; r < R; ++r)
-#pragma unroll
-    for (int c = 0; c < R; ++c) A[r0 + r][c0 + 16 * c] = acc[r][c];
-  __syncthreads();
-
-  // B = L^T T
-#pragma unroll
-  for (int r = 0; r < R; ++r)
-#pragma unroll
-    for (int c = 0; c < R; ++c) acc[r][c] = 0.0;
-  for (int k = 0; k < D; ++k) {
-    double lk[R], tc[R];
-#pragma unroll
-    for (int r = 0; r < R; ++r) lk[r] = L[(int64_t)k * D + r0 + r];
-#pragma unroll
-    for (int c = 0; c < R; ++c) tc[c] = A[k][c0 + 16 * c];
-#pragma unroll
-    for (int r = 0; r < R; ++r)
-#pragma unroll
-      for (int c = 0; c < R; ++c) acc[r][c] = fma(lk[r], tc[c], acc[r][c]);
-  }
-  __syncthreads();
-#pragma unroll
-  for (int r = 0; r < R; ++r)
-#pragma unroll
-    for (int c = 0; c < R; ++c) A[r0 + r][c0 + 16 * c] = acc[r][c];
-  __syncthreads();
-  // exact symmetry for the two-sided updates below
-  for (int e = t; e < D * D; e += kEigThreads) {
-    const int i = e / D, j = e % D;
-    if (i < j) {
-      const double s = 0.5 * (A[i][j] + A[j][i]);
-      A[i][j] = s;
-      A[j][i] = s;
+        for (int c = 0; c < CT; ++c) acc[r][c] = fma(qk[r], lk[c], acc[r][c]);
     }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < RT; ++r)
+#pragma unroll
+      for (int c = 0; c < CT; ++c) buf[rg * RT + r][c16 + 16 * c] = acc[r][c];
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < RT; ++r)
+#pragma unroll
+      for (int c = 0; c < CT; ++c) acc[r][c] = 0.0;
+    for (int k = 0; k < D; ++k) {
+      double lk[RT], tk[CT];
+#pragma unroll
+      for (int r = 0; r < RT; ++r) lk[r] = L[(int64_t)k * D + rg * RT + r];
+#pragma unroll
+      for (int c = 0; c < CT; ++c) tk[c] = buf[k][c16 + 16 * c];
+#pragma unroll
+      for (int r = 0; r < RT; ++r)
+#pragma unroll
+        for (int c = 0; c < CT; ++c) acc[r][c] = fma(lk[r], tk[c], acc[r][c]);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < RT; ++r)
+#pragma unroll
+      for (int c = 0; c < CT; ++c) buf[rg * RT + r][c16 + 16 * c] = acc[r][c];
+    __syncthreads();
+    if (base / JC == J)
+#pragma unroll
+      for (int c = 0; c < CPT; ++c) arow[c] = buf[i][base % JC + c];
   }
-  __syncthreads();
 
-  // Householder tridiagonalisation: step k reflects rows/columns k+1..D-1 so
-  // that column k has zeros below its subdiagonal.  Every wave computes the
-  // column norm and the scalar K itself (same data, same order), so no extra
-  // barrier is needed for them and all waves take the same branch.
+  // Householder tridiagonalisation (Golub and Van Loan, Alg. 8.3.1): step k
+  // takes x = row k right of the diagonal (= column k below it), v = x - alpha
+  // e_1 with |alpha| = |x|, p = beta A v, K = beta p.v / 2, and
+  // A <- A - v p^T - (p - 2 K v) v^T on rows and columns k+1.. (v and p are
+  // zero elsewhere, so the update runs over whole rows).  Every wave derives
+  // alpha, beta and K from LDS itself, so all waves take the same branch.
   for (int k = 0; k < D - 2; ++k) {
-    const int m = D - k - 1;
-    const double x0 = A[k + 1][k];
+    const int b = k & 1;
+    double* rb = rowbuf[b];
+    double* vb = vbuf[b];
+    double* pb = pp[b];
+    if (i == k)
+#pragma unroll
+      for (int c = 0; c < CPT; ++c) rb[base + c] = arow[c];
+    __syncthreads();
+    const double x0 = rb[k + 1];
     double part = 0.0;
-    for (int i = 1 + lane; i < m; i += kWave) {
-      const double x = A[k + 1 + i][k];
-      part = fma(x, x, part);
-    }
+    for (int j = k + 2 + lane; j < D; j += kWave) part = fma(rb[j], rb[j], part);
     const double xn2 = wave_sum_f64(part);
+    if (t == 0) dd[k] = rb[k];
     if (xn2 == 0.0) {
-      if (t == 0) { dd[k] = A[k][k]; ee[k] = x0; }
+      if (t == 0) ee[k] = x0;
       continue;
     }
     const double nx = sqrt(fma(x0, x0, xn2));
     const double alpha = x0 > 0.0 ? -nx : nx;
     const double v0 = x0 - alpha;
     const double beta = 2.0 / fma(v0, v0, xn2);
-    if (t == 0) { dd[k] = A[k][k]; ee[k] = alpha; }
+    if (t == 0) ee[k] = alpha;
     if (wave == 0)
-      for (int i = lane; i < m; i += kWave) vv[i] = i == 0 ? v0 : A[k + 1 + i][k];
+      for (int j = lane; j < D; j += kWave) vb[j] = j <= k ? 0.0 : (j == k + 1 ? v0 : rb[j]);
     __syncthreads();
-    if (t < m) {
-      double p = 0.0;
-      for (int j = 0; j < m; ++j) p = fma(A[k + 1 + j][k + 1 + t], vv[j], p);
-      pp[t] = beta * p;
+    double p0 = 0.0, p1 = 0.0;
+#pragma unroll
+    for (int c = 0; c < CPT; c += 2) {
+      p0 = fma(arow[c], vb[base + c], p0);
+      p1 = fma(arow[c + 1], vb[base + c + 1], p1);
     }
+    double prow = p0 + p1;
+    prow += dpp_f64<0xB1, 0xf>(prow);              // partner lane t ^ 1
+    if (TPR == 4) prow += dpp_f64<0x4E, 0xf>(prow);  // lanes t ^ 2
+    const double pi = i > k ? beta * prow : 0.0;
+    if (t % TPR == 0) pb[i] = pi;
     __syncthreads();
     double pv = 0.0;
-    for (int i = lane; i < m; i += kWave) pv = fma(pp[i], vv[i], pv);
+    for (int j = lane; j < D; j += kWave) pv = fma(pb[j], vb[j], pv);
     const double K = 0.5 * beta * wave_sum_f64(pv);
-    for (int i = wave; i < m; i += kEigWaves) {
-      const double vi = vv[i], wi = pp[i] - K * vi;
-      for (int j = lane; j < m; j += kWave) {
-        const double vj = vv[j], wj = pp[j] - K * vj;
-        A[k + 1 + i][k + 1 + j] -= vi * wj + wi * vj;
-      }
+    const double vi = vb[i];
+    const double ci = fma(-2.0 * K, vi, pi);
+    // in groups of 16 columns, so that the LDS operands are not all held at once
+#pragma unroll
+    for (int c0 = 0; c0 < CPT; c0 += 16) {
+#pragma unroll
+      for (int c = c0; c < c0 + 16; ++c) arow[c] = fma(-vi, pb[base + c], fma(-ci, vb[base + c], arow[c]));
+      __builtin_amdgcn_sched_barrier(0);
     }
-    __syncthreads();
-  }
-  if (t == 0) {
-    dd[D - 2] = A[D - 2][D - 2];
-    dd[D - 1] = A[D - 1][D - 1];
-    ee[D - 2] = A[D - 1][D - 2];
   }
   __syncthreads();
-  double* e2 = pp;  // squared off-diagonal
+  if (i == D - 2)
+#pragma unroll
+    for (int c = 0; c < CPT; ++c) rowbuf[0][base + c] = arow[c];
+  if (i == D - 1)
+#pragma unroll
+    for (int c = 0; c < CPT; ++c) rowbuf[1][base + c] = arow[c];
+  __syncthreads();
+  if (t == 0) {
+    dd[D - 2] = rowbuf[0][D - 2];
+    ee[D - 2] = rowbuf[0][D - 1];
+    dd[D - 1] = rowbuf[1][D - 1];
+  }
+  __syncthreads();
+  double* e2 = pp[0];  // squared off-diagonal
   if (t < D - 1) e2[t] = ee[t] * ee[t];
   __syncthreads();
 
   // Gershgorin interval and the pivot floor (every thread, same order)
   double lo = dd[0] - fabs(ee[0]), hi = dd[0] + fabs(ee[0]), emax2 = 0.0;
-  for (int i = 1; i < D; ++i) {
-    const double r = fabs(ee[i - 1]) + (i < D - 1 ? fabs(ee[i]) : 0.0);
-    lo = fmin(lo, dd[i] - r);
-    hi = fmax(hi, dd[i] + r);
+  for (int j = 1; j < D; ++j) {
+    const double r = fabs(ee[j - 1]) + (j < D - 1 ? fabs(ee[j]) : 0.0);
+    lo = fmin(lo, dd[j] - r);
+    hi = fmax(hi, dd[j] + r);
   }
-  for (int i = 0; i < D - 1; ++i) emax2 = fmax(emax2, e2[i]);
+  for (int j = 0; j < D - 1; ++j) emax2 = fmax(emax2, e2[j]);
   const double eps = 2.220446049250313e-16;
   const double pivmin = 2.2250738585072014e-308 * fmax(1.0, emax2);
   const double tnorm = fmax(fabs(lo), fabs(hi));
   const double atol = eps * tnorm;
 
-  double sigma = 0.0;
-  if (t < D) {
-    // eigenvalue number t (ascending): count(a) <= t < count(b)
-    double lo_t = lo - 2.0 * atol - pivmin, hi_t = hi + 2.0 * atol + pivmin;
-    for (int it = 0; it < 160; ++it) {
-      if (hi_t - lo_t <= 2.0 * eps * fmax(fabs(lo_t), fabs(hi_t)) + atol) break;
-      const double mid = lo_t + 0.5 * (hi_t - lo_t);
-      if (mid <= lo_t || mid >= hi_t) break;
-      if (sturm_count<D>(dd, e2, mid, pivmin) > t) hi_t = mid; else lo_t = mid;
+  // Multisection: eigenvalue e (ascending) is bracketed by [blo, bhi] with
+  // count(blo) <= e < count(bhi); each round the SIDES threads of e evaluate
+  // NPT interior points (two chains each) and all of them keep the
+  // sub-interval holding e.  Every eigenvalue runs the same number of rounds,
+  // enough to shrink the Gershgorin width below atol.
+  const int e = t % D, side = t / D;
+  int* cnt = reinterpret_cast<int*>(&buf[0][0]);  // [2][NPT][D], free after the products
+  double blo = lo - 2.0 * atol - pivmin, bhi = hi + 2.0 * atol + pivmin;
+  int rounds = 0;
+  {
+    double w = bhi - blo;
+    const double target = fmax(atol, 4.0 * pivmin);
+    while (w > target && rounds < 64) {
+      w /= (NPT + 1);
+      ++rounds;
     }
-    // eigenvalues at or below the rounding floor of the reduction are zero
-    // (a rank-deficient W_Q or W_K leaves only such values), so they add no
-    // term to the entropy; for the zero matrix every eigenvalue is zero
-    const double lam = 0.5 * (lo_t + hi_t);
+  }
+  for (int it = 0; it < rounds; ++it) {
+    int* cb = cnt + (it & 1) * NPT * D;
+    const double step = (bhi - blo) / (NPT + 1);
+    const double xa = blo + step * (2 * side + 1), xb = blo + step * (2 * side + 2);
+    int ca, cbn;
+    sturm_count2<D>(dd, e2, xa, xb, pivmin, ca, cbn);
+    cb[(2 * side) * D + e] = ca;
+    cb[(2 * side + 1) * D + e] = cbn;
+    __syncthreads();
+    int m = 0;
+    while (m < NPT && cb[m * D + e] <= e) ++m;
+    const double nlo = m == 0 ? blo : blo + step * m;
+    const double nhi = m == NPT ? bhi : blo + step * (m + 1);
+    blo = nlo;
+    bhi = nhi;
+  }
+
+  // eigenvalues at or below the rounding floor of the reduction are zero
+  // (a rank-deficient W_Q or W_K leaves only such values), so they add no
+  // term to the entropy; for the zero matrix every eigenvalue is zero
+  double sigma = 0.0;
+  if (side == 0) {
+    const double lam = 0.5 * (blo + bhi);
     sigma = (tnorm > 0.0 && lam > D * atol) ? sqrt(lam) : 0.0;
   }
 
