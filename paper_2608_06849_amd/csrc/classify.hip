@@ -31,14 +31,18 @@ constexpr int kGramBK = 64;  // d_model columns per main-loop iteration
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 x) { return __builtin_bit_cast(bf16x8, x); }
 
 // G = W W^T for one d x d_model slice (W row-major, row stride rs elements).
-// Wave w owns 32-row block w as the A operand and computes the 32x32 tiles
-// (w, c) for c >= w; each tile is written with its transpose, so G is exactly
-// symmetric.  The sum over d_model is order-free, so every lane loads 64
-// contiguous bytes of its row per iteration and both operands use the same
-// k mapping (k = k0 + 32 * half + 8 * s + j for MFMA step s, element j).
+// The slice is streamed through LDS 64 columns at a time: every thread loads
+// 64 contiguous bytes of one row (two threads per row), one stage ahead of the
+// MFMAs.  Wave w owns 32-row block w as the A operand and computes the 32x32
+// tiles (w, c) for c >= w; each tile is written with its transpose, so G is
+// exactly symmetric.  The sum over d_model is order-free, so both operands use
+// the same k mapping (k = k0 + 32 * half + 8 * s + j for MFMA step s, element j).
+constexpr int kGramRowPad = kGramBK + 8;  // bf16 per LDS row (bank spread)
+
 template <int D>
 __global__ __launch_bounds__(64 * (D / 32)) void gram_kernel(ClassifyArgs a) {
   constexpr int NRB = D / 32;
+  __shared__ __align__(16) bf16 stage[2][D][kGramRowPad];
   const int n_heads = a.Hq + a.Hkv;
   const int u = blockIdx.x % n_heads;
   const int layer = blockIdx.x / n_heads;
@@ -51,34 +55,51 @@ __global__ __launch_bounds__(64 * (D / 32)) void gram_kernel(ClassifyArgs a) {
     w = static_cast<const bf16*>(a.wk) + layer * a.wk_sl + (int64_t)(u - a.Hq) * D * a.wk_sr;
     rs = a.wk_sr;
   }
-  const int wave = threadIdx.x >> 6;
-  const int lane = threadIdx.x & 63;
+  const int t = threadIdx.x;
+  const int wave = t >> 6;
+  const int lane = t & 63;
   const int l32 = lane & 31;
   const int half = lane >> 5;
-
-  const bf16* rowa = w + (int64_t)(32 * wave + l32) * rs + 32 * half;
-  const bf16* rowb[NRB];
-#pragma unroll
-  for (int c = 0; c < NRB; ++c) rowb[c] = w + (int64_t)(32 * c + l32) * rs + 32 * half;
+  const int lrow = t >> 1, lcol = (t & 1) * 32;  // this thread's part of a stage
+  const bf16* src = w + (int64_t)lrow * rs + lcol;
 
   f32x16 acc[NRB];
 #pragma unroll
   for (int c = 0; c < NRB; ++c) acc[c] = f32x16{};
 
-  for (int k0 = 0; k0 < a.d_model; k0 += kGramBK) {
-    u32x4 xa[4], xb[NRB][4];
+  u32x4 ld[4];
+  auto gload = [&](int k0) {
 #pragma unroll
-    for (int s = 0; s < 4; ++s) xa[s] = ld16(rowa + k0 + 8 * s);
+    for (int s = 0; s < 4; ++s) ld[s] = ld16(src + k0 + 8 * s);
+  };
+  auto lstore = [&](int buf) {
 #pragma unroll
-    for (int c = 0; c < NRB; ++c)
-      if (c >= wave)
+    for (int s = 0; s < 4; ++s) st16(&stage[buf][lrow][lcol + 8 * s], ld[s]);
+  };
+  auto compute = [&](int buf) {
 #pragma unroll
-        for (int s = 0; s < 4; ++s) xb[c][s] = ld16(rowb[c] + k0 + 8 * s);
-#pragma unroll
-    for (int s = 0; s < 4; ++s)
+    for (int s = 0; s < 4; ++s) {
+      const bf16x8 xa = as_bf16x8(*reinterpret_cast<const u32x4*>(&stage[buf][32 * wave + l32][32 * half + 8 * s]));
 #pragma unroll
       for (int c = 0; c < NRB; ++c)
-        if (c >= wave) acc[c] = mfma32(as_bf16x8(xa[s]), as_bf16x8(xb[c][s]), acc[c]);
+        if (c >= wave) {
+          const bf16x8 xb = as_bf16x8(*reinterpret_cast<const u32x4*>(&stage[buf][32 * c + l32][32 * half + 8 * s]));
+          acc[c] = mfma32(xa, xb, acc[c]);
+        }
+    }
+  };
+
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  const int n_it = a.d_model / kGramBK;
+  for (int it = 0; it < n_it; ++it) {
+    const int cur = it & 1;
+    const bool more = it + 1 < n_it;
+    if (more) gload((it + 1) * kGramBK);
+    compute(cur);
+    if (more) lstore(cur ^ 1);
+    __syncthreads();
   }
 
   float* g = a.gram + ((int64_t)layer * n_heads + u) * D * D;
