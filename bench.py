@@ -12,6 +12,9 @@ one 32768-token sequence, n_sink 64, window 1024):
 `value` is the useful prefill FLOPs of a step (4 D per visible query-key pair)
 divided by the step time.
 
+A classifier leg times the offline head classification of all 28 layers of a
+Qwen2.5-7B-shaped model (seeded synthetic projection weights).
+
 A decode leg runs the Llama-3-8B-shaped batch (32 query heads, 8 KV heads of
 which 4 streaming, batch 8, 131072-token contexts on a paged cache of shuffled
 16-token pages, ring n_sink 64 + window 1024) for 64 single-token steps and
@@ -68,6 +71,7 @@ def parse():
     ap.add_argument("--no-all-retrieval", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-stack-decode", action="store_true")
+    ap.add_argument("--no-classify", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (for scaling HBM counters)")
     return ap.parse_args()
@@ -247,6 +251,10 @@ def main():
         stack = stack_decode_leg(args, torch, synth, PagedCache, RingCache, aoh_decode, aoh_decode_workspace_bytes,
                                  aoh_kv_append, decode_bytes)
 
+    cls = None
+    if not args.no_classify:
+        cls = classify_leg(args, torch, synth)
+
     # ------------------------------------------------------------------ CPU baseline (oracle)
     cpu = None
     if not args.no_cpu_baseline:
@@ -291,6 +299,7 @@ def main():
         },
         "decode": dec,
         "stack_decode": stack,
+        "classify": cls,
         "cpu_baseline": cpu,
         "paper_context": "paper (hardware unstated, end-to-end model latency, bf16, batch 1): prefill/decode "
                          "latency reduction up to 41.4%/66.0% and 50.0% KV saving at 256K, 50% sparsity",
@@ -464,6 +473,52 @@ def stack_decode_leg(args, torch, synth, PagedCache, RingCache, aoh_decode, aoh_
     log(f"stack decode: eager {eager_ms:.3f} ms/step, graph {graph_ms:.3f} ms/step, "
         f"{res['kv_gbps_graph']:.0f} GB/s with the graph")
     return res
+
+
+def classify_leg(args, torch, synth):
+    """Offline head classification of a whole Qwen2.5-7B-shaped model (28
+    layers, 28 query / 4 KV heads, d_head 128, d_model 3584, bf16 weights):
+    Gram matrices, Cholesky, spectra, effective ranks and labels on the GPU."""
+    from paper_2608_06849_amd import aoh_classify, aoh_classify_workspace_bytes, aoh_retrieval_group_count
+    name = "qwen25_classify"
+    c = synth.CONFIGS[name]
+    L, hq, hkv, d, dm = c["layers"], c["hq"], c["hkv"], c["d"], c["d_model"]
+    t0 = time.time()
+    wq = torch.empty((L, hq * d, dm), dtype=torch.bfloat16, device="cuda")
+    wk = torch.empty((L, hkv * d, dm), dtype=torch.bfloat16, device="cuda")
+    for l in range(L):
+        a, b = synth.projection_weights(name, l)
+        wq[l].copy_(torch.from_numpy(a).to(torch.bfloat16))
+        wk[l].copy_(torch.from_numpy(b).to(torch.bfloat16))
+    k = aoh_retrieval_group_count(hkv, c["sparsity"])
+    hr = torch.empty((L, hq), dtype=torch.float64, device="cuda")
+    gsc = torch.empty((L, hkv), dtype=torch.float64, device="cuda")
+    lab = torch.empty((L, hkv), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(aoh_classify_workspace_bytes(L, hq, hkv, d), dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    log(f"classifier weights ready in {time.time() - t0:.1f}s")
+    for _ in range(2):
+        aoh_classify(wq, wk, d, k, hr, gsc, lab, workspace=ws)
+    n = max(3, args.steps)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(n):
+        aoh_classify(wq, wk, d, k, hr, gsc, lab, workspace=ws)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / n
+    wbytes = (wq.numel() + wk.numel()) * 2
+    log(f"classify {L} layers: {ms:.3f} ms ({wbytes / (ms * 1e-3) / 1e12:.2f} TB/s of weights)")
+    return {
+        "workload": f"Qwen2.5-7B-shaped projections: {L} layers x ({hq} q + {hkv} KV heads), d_head {d}, "
+                    f"d_model {dm}, bf16; {k} of {hkv} groups retrieval per layer",
+        "ms": round(ms, 4),
+        "heads_per_s": round(L * hq / (ms * 1e-3)),
+        "weight_bytes": wbytes,
+        "weight_tb_per_s": round(wbytes / (ms * 1e-3) / 1e12, 3),
+        "streaming_groups": int(lab.sum().item()),
+    }
 
 
 def cpu_baseline(q, k, v, mask, n_sink, window, T, D, gs, target_s=15.0):
