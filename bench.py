@@ -6,8 +6,8 @@
 Step = one pass of the whole hot path over the Qwen2.5-7B-shaped layer
 (28 query heads, 4 KV heads of which 1 and 3 are streaming, d_head 128, bf16,
 one 32768-token sequence, n_sink 64, window 1024):
-  head scheduling -> retrieval prefill launch -> streaming prefill launch
-  -> bulk append of the prompt's K/V into the paged cache and the ring
+  head scheduling -> retrieval prefill launch -> streaming prefill launch,
+  both writing the prompt's K/V into the paged cache and the ring as they go
   -> one decode step (append the next token, split-K decode, merge).
 `value` is the useful prefill FLOPs of a step (4 D per visible query-key pair)
 divided by the step time.
@@ -134,7 +134,7 @@ def main():
 
     import synth
     from paper_2608_06849_amd import (PagedCache, RingCache, aoh_decode, aoh_decode_workspace_bytes,
-                                      aoh_kv_append, aoh_prefill)
+                                      aoh_kv_append, aoh_prefill, aoh_prefill_append)
     from paper_2608_06849_amd import aoh as A
 
     if not torch.cuda.is_available():
@@ -161,7 +161,6 @@ def main():
     bt = torch.arange(max_pages, dtype=torch.int32)[None]
     full = PagedCache.allocate(max_pages, n_ret, D, bf, bt)
     ring = RingCache.allocate(1, n_str, n_sink, window, D, bf)
-    start0 = torch.zeros(1, dtype=torch.int32, device=dev)
     startT = torch.full((1,), T, dtype=torch.int32, device=dev)
     lensT1 = torch.full((1,), T + 1, dtype=torch.int32, device=dev)
     ws = torch.empty(aoh_decode_workspace_bytes(1, Hq, D, max_pages, n_sink + window) // 4 + 4,
@@ -176,10 +175,9 @@ def main():
     def step(m=mask, f=full, r=ring, ev=None):
         if ev is not None:
             ev[0].record()
-        aoh_prefill(q, k, v, m, n_sink, window, out=out)
+        aoh_prefill_append(q, k, v, m, n_sink, window, f, r, out=out)
         if ev is not None:
             ev[1].record()
-        aoh_kv_append(k, v, m, start0, f, r, n_sink, window)
         aoh_kv_append(kv_next[0], kv_next[1], m, startT, f, r, n_sink, window)
         aoh_decode(q_dec, f, r, m, lensT1, n_sink, window, out=dec_out, workspace=ws)
         if ev is not None:
@@ -277,7 +275,7 @@ def main():
         "config": {
             "workload": "Qwen2.5-7B-shaped attention layer: prefill 32768 tokens, 28 q heads / 4 KV heads "
                         "(KV heads 1,3 streaming), d_head 128, n_sink 64, window 1024; step = schedule + "
-                        "prefill (2 launches) + bulk KV append + 1 decode step",
+                        "prefill writing the caches (2 launches) + 1 decode step",
             "global_batch": 1, "seq_len": T, "parallelism": "none (1 GPU)",
         },
         "prefill": {

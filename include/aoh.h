@@ -150,6 +150,23 @@ aoh_status aoh_prefill_chunked(const aoh_tensor* q, const aoh_tensor* k, const a
                                int32_t chunk, aoh_tensor* out, void* stream);
 
 /*
+ * Prefill of a new prompt that also fills the caches (Sec. 5: the prefill stage
+ * leaves retrieval heads with their O(T) K/V states and streaming heads with
+ * their sink + recent cache).  Output as aoh_prefill (chunk = 0) or
+ * aoh_prefill_chunked (chunk >= 1); in addition the prompt's K/V occupy
+ * positions 0..T-1 of every sequence b, written exactly as
+ * aoh_kv_append(k, v, head_is_streaming, start_pos = 0, kv_full, kv_ring, ...)
+ * would write them (bit-exact; the paged cache needs pages mapped for
+ * positions 0..T-1).  For bf16 the prefill kernels write the caches from the
+ * K/V tiles they already stage, so the prompt's K/V are read once; fp32 runs
+ * the append as a separate launch.  Errors as aoh_prefill and aoh_kv_append.
+ */
+aoh_status aoh_prefill_append(const aoh_tensor* q, const aoh_tensor* k, const aoh_tensor* v,
+                              const uint8_t* head_is_streaming, int32_t n_sink, int32_t window,
+                              int32_t chunk, const aoh_paged_cache* kv_full, const aoh_ring_cache* kv_ring,
+                              aoh_tensor* out, void* stream);
+
+/*
  * Append n_new tokens per sequence to the caches (Sec. 5: retrieval heads
  * retain every token; streaming heads evict all but the sink and recent
  * tokens).  Token t of k_new/v_new has position start_pos[b] + t.

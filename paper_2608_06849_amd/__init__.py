@@ -5,4 +5,4 @@ include/aoh.h); ``aoh`` is its ctypes binding.
 """
 from .aoh import (AohError, PagedCache, RingCache, aoh_classify, aoh_classify_workspace_bytes,  # noqa: F401
                   aoh_decode, aoh_decode_workspace_bytes, aoh_kv_append, aoh_last_error, aoh_prefill,
-                  aoh_prefill_chunked, aoh_retrieval_group_count, aoh_version, lib)
+                  aoh_prefill_append, aoh_prefill_chunked, aoh_retrieval_group_count, aoh_version, lib)

@@ -48,7 +48,7 @@ class AohRingCache(ctypes.Structure):
 
 _lib = None
 
-EXPORTS = ("aoh_prefill", "aoh_prefill_chunked", "aoh_kv_append", "aoh_decode_workspace_bytes", "aoh_decode",
+EXPORTS = ("aoh_prefill", "aoh_prefill_chunked", "aoh_prefill_append", "aoh_kv_append", "aoh_decode_workspace_bytes", "aoh_decode",
            "aoh_classify_workspace_bytes", "aoh_classify", "aoh_retrieval_group_count",
            "aoh_last_error", "aoh_version")
 
@@ -68,6 +68,10 @@ def lib():
                                           ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, P(AohTensor),
                                           ctypes.c_void_p]
         L.aoh_prefill_chunked.restype = ctypes.c_int
+        L.aoh_prefill_append.argtypes = [P(AohTensor), P(AohTensor), P(AohTensor), ctypes.c_void_p,
+                                         ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, P(AohPagedCache),
+                                         P(AohRingCache), P(AohTensor), ctypes.c_void_p]
+        L.aoh_prefill_append.restype = ctypes.c_int
         L.aoh_kv_append.argtypes = [P(AohTensor), P(AohTensor), ctypes.c_void_p, ctypes.c_void_p,
                                     P(AohPagedCache), P(AohRingCache), ctypes.c_int32, ctypes.c_int32,
                                     ctypes.c_void_p]
@@ -206,6 +210,21 @@ def aoh_prefill_chunked(q, k, v, head_is_streaming, n_sink, window, chunk, out=N
     m = _Mask(head_is_streaming)
     _check(lib().aoh_prefill_chunked(ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), m.ptr,
                                      n_sink, window, chunk, ctypes.byref(od), _stream(stream)))
+    return out
+
+
+def aoh_prefill_append(q, k, v, head_is_streaming, n_sink, window, kv_full, kv_ring, chunk=0, out=None,
+                       stream=None):
+    """Prefill of a new prompt that also writes its K/V into the caches (see aoh.h)."""
+    if out is None:
+        out = torch.empty_like(q)
+    qd, kd, vd, od = tensor_desc(q), tensor_desc(k), tensor_desc(v), tensor_desc(out)
+    fd = kv_full.desc() if kv_full is not None else None
+    rd = kv_ring.desc() if kv_ring is not None else None
+    m = _Mask(head_is_streaming)
+    _check(lib().aoh_prefill_append(ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), m.ptr, n_sink, window,
+                                    chunk, ctypes.byref(fd) if fd else None, ctypes.byref(rd) if rd else None,
+                                    ctypes.byref(od), _stream(stream)))
     return out
 
 

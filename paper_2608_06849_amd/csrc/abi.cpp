@@ -153,9 +153,15 @@ int32_t aoh_version(void) { return 100; }
 
 const char* aoh_last_error(void) { return g_err; }
 
+static aoh_status check_paged(const aoh_paged_cache* c, int n_ret, int64_t B);
+static aoh_status check_ring(const aoh_ring_cache* c, int n_str, int n_sink, int window);
+
+// Prefill; with append set, also writes the prompt's K/V (positions 0..T-1 of
+// every sequence) into kv_full / kv_ring.
 static aoh_status prefill_impl(const aoh_tensor* q, const aoh_tensor* k, const aoh_tensor* v,
                                const uint8_t* head_is_streaming, int32_t n_sink, int32_t window,
-                               int32_t chunk, aoh_tensor* out, void* stream) {
+                               int32_t chunk, bool append, const aoh_paged_cache* kv_full,
+                               const aoh_ring_cache* kv_ring, aoh_tensor* out, void* stream) {
   aoh_status st;
   if ((st = check_tensor(q, "q", 4, AOH_BF16, AOH_F32))) return st;
   const int dt = q->dtype;
@@ -180,6 +186,11 @@ static aoh_status prefill_impl(const aoh_tensor* q, const aoh_tensor* k, const a
   const int rows = dt == AOH_BF16 ? kPrefillRows : kPrefillRowsF32;
   const int64_t n_qblocks = ceil_div(T, rows);
   if (n_qblocks * Hq * B >= (1ll << 31)) return fail(AOH_ERR_UNSUPPORTED, "grid too large");
+  if (append) {
+    if ((st = check_paged(kv_full, hs.n_ret, B))) return st;
+    if ((st = check_ring(kv_ring, hs.n_str, n_sink, window))) return st;
+    if (B > 65535) return fail(AOH_ERR_UNSUPPORTED, "batch too large");
+  }
 
   PrefillArgs a;
   std::memset(&a, 0, sizeof(a));
@@ -195,18 +206,55 @@ static aoh_status prefill_impl(const aoh_tensor* q, const aoh_tensor* k, const a
   a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)D));
   const int out_f32 = out->dtype == AOH_F32 && dt == AOH_BF16;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  // The bf16 kernel writes the caches itself; the fp32 path appends after.
+  const bool fused = append && dt == AOH_BF16;
   // Retrieval launch first: its causal work dominates (O(T^2) vs O(T(n_sink+window))).
   if (hs.n_ret) {
     a.n_kv = hs.n_ret;
     std::memcpy(a.kv_heads, hs.ret, hs.n_ret);
+    if (fused) {
+      a.append = 1;
+      a.ck = kv_full->k; a.cv = kv_full->v; a.block_table = kv_full->block_table;
+      a.max_pages = kv_full->max_pages_per_seq; a.num_pages = (int)kv_full->num_pages;
+      a.n_cache = hs.n_ret; a.ring_blocks = 0;
+    }
     hipError_t e = launch_prefill(a, dt, out_f32, (int)D, false, s);
     if (e != hipSuccess) return fail(AOH_ERR_HIP, "prefill retrieval launch: %s", hipGetErrorString(e));
   }
   if (hs.n_str) {
     a.n_kv = hs.n_str;
     std::memcpy(a.kv_heads, hs.str, hs.n_str);
+    if (fused) {
+      a.append = 1;
+      a.ck = kv_ring->k; a.cv = kv_ring->v; a.block_table = nullptr;
+      a.max_pages = 0; a.num_pages = 0;
+      a.n_cache = hs.n_str; a.ring_blocks = (int)ceil_div(kv_ring->capacity, kPageTokens);
+    }
     hipError_t e = launch_prefill(a, dt, out_f32, (int)D, true, s);
     if (e != hipSuccess) return fail(AOH_ERR_HIP, "prefill streaming launch: %s", hipGetErrorString(e));
+  }
+  if (append && !fused) {
+    AppendArgs ap;
+    std::memset(&ap, 0, sizeof(ap));
+    ap.k_new = k->data; ap.v_new = v->data;
+    ap.k_sb = k->stride[0]; ap.k_st = k->stride[1]; ap.k_sh = k->stride[2];
+    ap.v_sb = v->stride[0]; ap.v_st = v->stride[1]; ap.v_sh = v->stride[2];
+    ap.start_pos = nullptr;  // the prompt starts at position 0
+    ap.B = (int)B; ap.n_new = (int)T; ap.Hkv = (int)Hkv;
+    if (hs.n_ret) {
+      ap.pk = kv_full->k; ap.pv = kv_full->v; ap.block_table = kv_full->block_table;
+      ap.max_pages = kv_full->max_pages_per_seq; ap.num_pages = (int)kv_full->num_pages; ap.n_ret = hs.n_ret;
+    }
+    if (hs.n_str) {
+      ap.rk = kv_ring->k; ap.rv = kv_ring->v; ap.n_str = hs.n_str;
+      ap.ring_blocks = (int)ceil_div(kv_ring->capacity, kPageTokens);
+    }
+    ap.n_sink = n_sink; ap.window = window;
+    ap.n_chunks = (int)ceil_div(T, kPageTokens);
+    ap.streaming_mask = hs.streaming_mask;
+    std::memcpy(ap.rank, hs.rank, sizeof(ap.rank));
+    hipError_t e = launch_append(ap, dt, (int)D, s);
+    if (e != hipSuccess) return fail(AOH_ERR_HIP, "append launch: %s", hipGetErrorString(e));
   }
   return ok();
 }
@@ -214,14 +262,22 @@ static aoh_status prefill_impl(const aoh_tensor* q, const aoh_tensor* k, const a
 aoh_status aoh_prefill(const aoh_tensor* q, const aoh_tensor* k, const aoh_tensor* v,
                        const uint8_t* head_is_streaming, int32_t n_sink, int32_t window,
                        aoh_tensor* out, void* stream) {
-  return prefill_impl(q, k, v, head_is_streaming, n_sink, window, 0, out, stream);
+  return prefill_impl(q, k, v, head_is_streaming, n_sink, window, 0, false, nullptr, nullptr, out, stream);
 }
 
 aoh_status aoh_prefill_chunked(const aoh_tensor* q, const aoh_tensor* k, const aoh_tensor* v,
                                const uint8_t* head_is_streaming, int32_t n_sink, int32_t window,
                                int32_t chunk, aoh_tensor* out, void* stream) {
   if (chunk < 1) return fail(AOH_ERR_INVALID_ARG, "chunk=%d must be >= 1", chunk);
-  return prefill_impl(q, k, v, head_is_streaming, n_sink, window, chunk, out, stream);
+  return prefill_impl(q, k, v, head_is_streaming, n_sink, window, chunk, false, nullptr, nullptr, out, stream);
+}
+
+aoh_status aoh_prefill_append(const aoh_tensor* q, const aoh_tensor* k, const aoh_tensor* v,
+                              const uint8_t* head_is_streaming, int32_t n_sink, int32_t window,
+                              int32_t chunk, const aoh_paged_cache* kv_full, const aoh_ring_cache* kv_ring,
+                              aoh_tensor* out, void* stream) {
+  if (chunk < 0) return fail(AOH_ERR_INVALID_ARG, "chunk=%d must be >= 0", chunk);
+  return prefill_impl(q, k, v, head_is_streaming, n_sink, window, chunk, true, kv_full, kv_ring, out, stream);
 }
 
 static aoh_status check_paged(const aoh_paged_cache* c, int n_ret, int64_t B) {

@@ -29,6 +29,16 @@ struct PrefillArgs {
   int32_t n_qblocks;     // ceil(T / rows per block)
   float scale_log2;      // log2(e) / sqrt(D)
   float scale;           // 1 / sqrt(D)
+  // Fused append of the prompt (positions 0..T-1) into this launch's cache:
+  // the paged cache for the retrieval launch, the ring for the streaming one.
+  // The cache rank of kv_heads[j] is j.
+  int32_t append;
+  void* ck;
+  void* cv;
+  const int32_t* block_table;   // paged cache only
+  int32_t max_pages, num_pages; // paged cache only
+  int32_t n_cache;              // KV heads stored in the cache
+  int32_t ring_blocks;          // ring only: Cpad / 16
   uint8_t kv_heads[kMaxKvHeads];
 };
 
@@ -87,7 +97,7 @@ struct AppendArgs {
   const void* v_new;
   int64_t k_sb, k_st, k_sh;
   int64_t v_sb, v_st, v_sh;
-  const int32_t* start_pos;
+  const int32_t* start_pos;     // device [B]; nullptr: every sequence starts at 0
   int32_t B, n_new, Hkv;
   // paged cache
   void* pk;

@@ -95,7 +95,7 @@ __device__ __forceinline__ TilePlan make_plan(int i0, int rows, int T, int n_sin
   return p;
 }
 
-template <int D, bool STREAM, bool OUT_F32>
+template <int D, bool STREAM, bool OUT_F32, bool APPEND>
 __global__ __launch_bounds__(kWaves * kWave, kRB == 1 ? 2 : 1) void prefill_bf16_kernel(PrefillArgs a) {
   __shared__ __align__(16) PrefillLds<D> lds[2];
   constexpr int kChunksPerRow = D / 8;                     // 16-byte chunks per key row
@@ -210,6 +210,64 @@ __global__ __launch_bounds__(kWaves * kWave, kRB == 1 ? 2 : 1) void prefill_bf16
         *reinterpret_cast<u32x4*>(&buf.k[kBN * u + st_row[r]][st_col[r]]) = kst[u][r];
         *reinterpret_cast<u32x4*>(&buf.v[kBN * u + st_row[r]][st_col[r]]) = vst[u][r];
       }
+  };
+
+  // Fused append: the first query head of each group writes the K/V tiles of
+  // its block's own rows [i0, i0 + rows) into the cache, from the LDS stage
+  // that already holds them, so every position is written exactly once.
+  // Retrieval: paged cache (K token-major, V dimension-major per page; pages
+  // outside the block table are skipped).  Streaming: the ring keeps a
+  // position only if no later prompt position maps to its slot.
+  const bool writer = APPEND && (qh_local % a.gs) == 0;
+  const int crank = qh_local / a.gs;
+  auto write_tile = [&](const PrefillLds<D>& buf, int u, int kb) {
+    constexpr int kCh = D / 8;
+    uint16_t* ck = static_cast<uint16_t*>(a.ck);
+    uint16_t* cv = static_cast<uint16_t*>(a.cv);
+    if (!STREAM) {
+      for (int e = tid; e < kBN * kCh; e += kWaves * kWave) {
+        const int row = e / kCh, col = (e % kCh) * 8;
+        const int p = kb + row;
+        const int lp = p / kPageTokens;
+        if (p >= T || lp >= a.max_pages) continue;
+        const int page = a.block_table[(int64_t)b * a.max_pages + lp];
+        if (page < 0 || page >= a.num_pages) continue;
+        uint16_t* dst = ck + (((int64_t)page * a.n_cache + crank) * kPageTokens + p % kPageTokens) * D + col;
+        st16(dst, *reinterpret_cast<const u32x4*>(&buf.k[kBN * u + row][col]));
+      }
+      for (int e = tid; e < (kBN / kPageTokens) * D * 2; e += kWaves * kWave) {
+        const int pg = e / (2 * D), d = (e / 2) % D, hf = e % 2;
+        const int p0 = kb + kPageTokens * pg + 8 * hf;
+        const int lp = p0 / kPageTokens;
+        if (p0 >= T || lp >= a.max_pages) continue;
+        const int page = a.block_table[(int64_t)b * a.max_pages + lp];
+        if (page < 0 || page >= a.num_pages) continue;
+        uint16_t* dst = cv + (((int64_t)page * a.n_cache + crank) * D + d) * kPageTokens + 8 * hf;
+        const int row0 = kBN * u + kPageTokens * pg + 8 * hf;
+        if (p0 + 8 <= T) {
+          u32x4 w;
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            w[j] = (uint32_t)buf.v[row0 + 2 * j][d] | ((uint32_t)buf.v[row0 + 2 * j + 1][d] << 16);
+          st16(dst, w);
+        } else {
+          for (int j = 0; p0 + j < T; ++j) dst[j] = buf.v[row0 + j][d];
+        }
+      }
+    } else {
+      for (int e = tid; e < kBN * kCh; e += kWaves * kWave) {
+        const int row = e / kCh, col = (e % kCh) * 8;
+        const int p = kb + row;
+        if (p >= T || !(p < a.n_sink || p >= T - a.window)) continue;
+        const int slot = p < a.n_sink ? p : a.n_sink + (p - a.n_sink) % a.window;
+        const int64_t unit = ((int64_t)b * a.n_cache + crank) * a.ring_blocks + slot / kPageTokens;
+        const int r = slot % kPageTokens;
+        st16(ck + unit * (kPageTokens * D) + r * D + col, *reinterpret_cast<const u32x4*>(&buf.k[kBN * u + row][col]));
+        uint16_t* rv = cv + unit * (kPageTokens * D);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) rv[(col + j) * kPageTokens + r] = buf.v[kBN * u + row][col + j];
+      }
+    }
   };
 
   const float c = a.scale_log2;
@@ -372,6 +430,14 @@ __global__ __launch_bounds__(kWaves * kWave, kRB == 1 ? 2 : 1) void prefill_bf16
   __syncthreads();
   for (int st = 0; st < n_stage; ++st) {
     const PrefillLds<D>& buf = lds[st & 1];
+    if (APPEND && writer)
+      for (int u = 0; u < kStageTiles; ++u) {
+        const int it = st * kStageTiles + u;
+        if (it < plan.n_visit) {
+          const int kb = plan.tile(it) * kBN;
+          if (kb >= i0 && kb < i0 + kPrefillRows) write_tile(buf, u, kb);
+        }
+      }
 #pragma unroll
     for (int u = 0; u < kStageTiles; ++u) {
       const int it = st * kStageTiles + u;
@@ -491,7 +557,10 @@ __global__ __launch_bounds__(kPrefillRowsF32) void prefill_f32_kernel(PrefillArg
 template <int D, bool STREAM, bool OUT_F32>
 static hipError_t launch_bf16(const PrefillArgs& a, hipStream_t s) {
   const int grid = a.n_qblocks * a.n_kv * a.gs * a.B;
-  hipLaunchKernelGGL((prefill_bf16_kernel<D, STREAM, OUT_F32>), dim3(grid), dim3(kWaves * kWave), 0, s, a);
+  if (a.append)
+    hipLaunchKernelGGL((prefill_bf16_kernel<D, STREAM, OUT_F32, true>), dim3(grid), dim3(kWaves * kWave), 0, s, a);
+  else
+    hipLaunchKernelGGL((prefill_bf16_kernel<D, STREAM, OUT_F32, false>), dim3(grid), dim3(kWaves * kWave), 0, s, a);
   return hipGetLastError();
 }
 

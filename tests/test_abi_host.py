@@ -230,3 +230,23 @@ def test_classify_workspace_and_group_count():
         for s in (0.0, 0.1, 0.25, 0.3, 0.5, 0.7, 0.75, 0.9, 1.0):
             assert A.aoh_retrieval_group_count(g, s) == ACC.n_retrieval_groups(g, s), (g, s)
     assert A.lib().aoh_retrieval_group_count(4, 1.5) == -1
+
+
+def test_prefill_append_validation():
+    q, k, v, out = _good()
+    buf = ctypes.create_string_buffer(b"\x00\x01", 2)
+    fn = A.lib().aoh_prefill_append
+    st = fn(ctypes.byref(q), ctypes.byref(k), ctypes.byref(v), ctypes.cast(buf, ctypes.c_void_p), 4, 32, -1,
+            None, None, ctypes.byref(out), None)
+    assert st == A.AOH_ERR_INVALID_ARG and "chunk" in A.aoh_last_error()
+    st = fn(ctypes.byref(q), ctypes.byref(k), ctypes.byref(v), ctypes.cast(buf, ctypes.c_void_p), 4, 32, 0,
+            None, None, ctypes.byref(out), None)
+    assert st == A.AOH_ERR_INVALID_ARG and "kv_full is null" in A.aoh_last_error()
+    full = A.AohPagedCache(FAKE, FAKE, FAKE, 10, 20, 1)
+    st = fn(ctypes.byref(q), ctypes.byref(k), ctypes.byref(v), ctypes.cast(buf, ctypes.c_void_p), 4, 32, 0,
+            ctypes.byref(full), None, ctypes.byref(out), None)
+    assert st == A.AOH_ERR_INVALID_ARG and "kv_ring is null" in A.aoh_last_error()
+    ring = A.AohRingCache(FAKE, FAKE, 1, 35)
+    st = fn(ctypes.byref(q), ctypes.byref(k), ctypes.byref(v), ctypes.cast(buf, ctypes.c_void_p), 4, 32, 0,
+            ctypes.byref(full), ctypes.byref(ring), ctypes.byref(out), None)
+    assert st == A.AOH_ERR_INVALID_ARG and "capacity" in A.aoh_last_error()
