@@ -19,4 +19,4 @@ Modules
 Parity status of each function is stated in its docstring; every function is
 pinned by a ``-m "not gpu"`` test (see tests/test_oracle_*.py).
 """
-from . import attention, cache_model, accounting, classifier  # noqa: F401
+from . import attention, cache_model, accounting, classifier, h2share  # noqa: F401
