@@ -213,6 +213,84 @@ aoh_status aoh_decode(const aoh_tensor* q, const aoh_paged_cache* kv_full,
                       void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * ---------------------------------------------------------------- H2Share
+ * AoH-guided cross-layer sparse attention (paper section "AoH-Guided Sparse
+ * Attention: H2Share" and its Inference Phase; GQA appendix, group-level head
+ * mapping).  Layers are grouped into blocks; the first layer of a block (the
+ * anchor) runs full attention for its retrieval heads and selects, per
+ * retrieval KV group, the top_k token positions of highest attention; the
+ * other layers of the block (reuse layers) let each retrieval group attend
+ * only to its OWN K/V at the positions selected by its mapped anchor group.
+ * Only integer positions cross layers.  Streaming groups use sink + window in
+ * every layer.  Readings taken where the paper is open: a group's selection
+ * score is the mean over its query heads of the attention probabilities of
+ * the step; ties go to the lower position; selection happens on every step.
+ */
+
+/*
+ * Offline head mapping between an anchor layer and a reuse layer (Eq. sim,
+ * evaluated in d_head space by the trace identities of the trace-reduction
+ * appendix):
+ *   head_sim[h][h'] = <M_h, M_h'>_F / (|M_h|_F |M_h'|_F),  M_h = W_K^g^T W_Q^h,
+ *   group_sim[g][g'] = mean of head_sim over the query heads of g and g',
+ *   mapping[g'] = rank (among the anchor's retrieval groups, ascending id) of
+ *                 the anchor retrieval group g maximising group_sim[g][g']
+ *                 (lower g on ties); -1 for streaming reuse groups.
+ *   w_q_*: [Hq * d_head][d_model] bf16, w_k_*: [Hkv * d_head][d_model] bf16,
+ *   DEVICE, one layer each (PyTorch Linear layout), same shapes in both layers;
+ *   d_head in {64, 128}; d_model a multiple of 64; Hkv <= 64.
+ *   anchor_is_streaming, reuse_is_streaming: HOST, Hkv bytes; the anchor needs
+ *   at least one retrieval group.
+ *   head_sim: DEVICE double [Hq][Hq]; group_sim: DEVICE double [Hkv][Hkv];
+ *   mapping: DEVICE int32 [Hkv] (all written).
+ *   workspace: DEVICE, aoh_head_mapping_workspace_bytes(Hq, Hkv, d_head) bytes.
+ */
+size_t aoh_head_mapping_workspace_bytes(int32_t n_q_heads, int32_t n_kv_heads, int32_t d_head);
+aoh_status aoh_head_mapping(const aoh_tensor* w_q_anchor, const aoh_tensor* w_k_anchor,
+                            const aoh_tensor* w_q_reuse, const aoh_tensor* w_k_reuse, int32_t d_head,
+                            const uint8_t* anchor_is_streaming, const uint8_t* reuse_is_streaming,
+                            double* head_sim, double* group_sim, int32_t* mapping, void* workspace,
+                            size_t workspace_bytes, void* stream);
+
+/*
+ * Anchor-layer decode step: exactly aoh_decode (same arguments, same out),
+ * and in addition, for every sequence b and the r-th retrieval KV group g
+ * (ascending id), indices[b][r][0..top_k) = the top_k positions p < lens[b]
+ * of highest score sum_{h in g} P_h(p) / (Hq/Hkv), P_h the attention
+ * probabilities of query head h in this step, in ascending order; ties to the
+ * lower position; when lens[b] <= top_k every position, then -1.
+ *   indices: DEVICE int32 [B][n_retrieval_groups][top_k]; top_k >= 1; bf16 only.
+ *   workspace: aoh_decode_anchor_workspace_bytes(B, Hq, D, max_pages, ring_capacity).
+ */
+size_t aoh_decode_anchor_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t d_head,
+                                         int32_t max_pages_per_seq, int32_t ring_capacity);
+aoh_status aoh_decode_anchor(const aoh_tensor* q, const aoh_paged_cache* kv_full,
+                             const aoh_ring_cache* kv_ring, const uint8_t* head_is_streaming,
+                             const int32_t* lens, int32_t n_sink, int32_t window, int32_t top_k,
+                             int32_t* indices, aoh_tensor* out, void* workspace, size_t workspace_bytes,
+                             void* stream);
+
+/*
+ * Reuse-layer decode step: streaming groups as aoh_decode; retrieval group g
+ * (query heads of g) attends to this layer's own cache at the positions
+ * indices[b][mapping[g]][0..top_k) (entries < 0 or >= lens[b] are skipped):
+ *   out[b,h,:] = sum_{p in list} softmax_p(q[b,h] . k[b,p,g] / sqrt(D)) v[b,p,g].
+ *   indices: DEVICE int32 [B][n_lists][top_k] (an anchor step's output);
+ *   mapping: HOST int32 [Hkv], list row for each retrieval group (as written
+ *   by aoh_head_mapping), ignored for streaming groups.
+ *   Lists are expected in the anchor's form: valid entries first (the first
+ *   min(lens[b], top_k)).  bf16 only.
+ *   workspace: aoh_decode_reuse_workspace_bytes(B, Hq, D, top_k, ring_capacity).
+ */
+size_t aoh_decode_reuse_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t d_head, int32_t top_k,
+                                        int32_t ring_capacity);
+aoh_status aoh_decode_reuse(const aoh_tensor* q, const aoh_paged_cache* kv_full,
+                            const aoh_ring_cache* kv_ring, const uint8_t* head_is_streaming,
+                            const int32_t* lens, int32_t n_sink, int32_t window, const int32_t* indices,
+                            int32_t n_lists, int32_t top_k, const int32_t* mapping, aoh_tensor* out,
+                            void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * The AoH head classifier (Sec. 4, Eqs. 2-7 and Algorithm 1; group-level
  * classification in the "GQA Extension" appendix).  It is offline work: it
  * produces the head_is_streaming arrays that the calls above take.

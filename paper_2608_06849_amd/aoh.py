@@ -50,6 +50,8 @@ _lib = None
 
 EXPORTS = ("aoh_prefill", "aoh_prefill_chunked", "aoh_prefill_append", "aoh_kv_append", "aoh_decode_workspace_bytes", "aoh_decode",
            "aoh_classify_workspace_bytes", "aoh_classify", "aoh_retrieval_group_count",
+           "aoh_head_mapping_workspace_bytes", "aoh_head_mapping", "aoh_decode_anchor_workspace_bytes",
+           "aoh_decode_anchor", "aoh_decode_reuse_workspace_bytes", "aoh_decode_reuse",
            "aoh_last_error", "aoh_version")
 
 
@@ -90,6 +92,26 @@ def lib():
         L.aoh_classify.restype = ctypes.c_int
         L.aoh_retrieval_group_count.argtypes = [ctypes.c_int32, ctypes.c_double]
         L.aoh_retrieval_group_count.restype = ctypes.c_int32
+        L.aoh_head_mapping_workspace_bytes.argtypes = [ctypes.c_int32] * 3
+        L.aoh_head_mapping_workspace_bytes.restype = ctypes.c_size_t
+        L.aoh_head_mapping.argtypes = [P(AohTensor)] * 4 + [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                                            ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+        L.aoh_head_mapping.restype = ctypes.c_int
+        L.aoh_decode_anchor_workspace_bytes.argtypes = [ctypes.c_int32] * 5
+        L.aoh_decode_anchor_workspace_bytes.restype = ctypes.c_size_t
+        L.aoh_decode_anchor.argtypes = [P(AohTensor), P(AohPagedCache), P(AohRingCache), ctypes.c_void_p,
+                                        ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                        ctypes.c_void_p, P(AohTensor), ctypes.c_void_p, ctypes.c_size_t,
+                                        ctypes.c_void_p]
+        L.aoh_decode_anchor.restype = ctypes.c_int
+        L.aoh_decode_reuse_workspace_bytes.argtypes = [ctypes.c_int32] * 5
+        L.aoh_decode_reuse_workspace_bytes.restype = ctypes.c_size_t
+        L.aoh_decode_reuse.argtypes = [P(AohTensor), P(AohPagedCache), P(AohRingCache), ctypes.c_void_p,
+                                       ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                       ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, P(AohTensor),
+                                       ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+        L.aoh_decode_reuse.restype = ctypes.c_int
         L.aoh_last_error.argtypes = []
         L.aoh_last_error.restype = ctypes.c_char_p
         L.aoh_version.argtypes = []
@@ -296,6 +318,85 @@ def aoh_classify(w_q, w_k, d_head, n_retrieval, head_rank=None, group_score=None
                               _ptr(group_score), _ptr(head_is_streaming), _ptr(workspace),
                               workspace.numel() * workspace.element_size(), _stream(stream)))
     return head_rank, group_score, head_is_streaming
+
+
+def _ws(workspace, n_bytes, device):
+    if workspace is None:
+        workspace = torch.empty(max(n_bytes, 16), dtype=torch.uint8, device=device)
+    return workspace, workspace.numel() * workspace.element_size()
+
+
+def aoh_head_mapping_workspace_bytes(n_q_heads, n_kv_heads, d_head):
+    return int(lib().aoh_head_mapping_workspace_bytes(n_q_heads, n_kv_heads, d_head))
+
+
+def aoh_head_mapping(w_q_anchor, w_k_anchor, w_q_reuse, w_k_reuse, d_head, anchor_is_streaming,
+                     reuse_is_streaming, workspace=None, stream=None):
+    """Cross-layer head/group similarity and the group mapping (see aoh.h).
+    Returns device tensors (head_sim [Hq, Hq] f64, group_sim [Hkv, Hkv] f64, mapping [Hkv] i32)."""
+    hq, hkv = w_q_anchor.shape[0] // d_head, w_k_anchor.shape[0] // d_head
+    dev = w_q_anchor.device
+    head_sim = torch.empty((hq, hq), dtype=torch.float64, device=dev)
+    group_sim = torch.empty((hkv, hkv), dtype=torch.float64, device=dev)
+    mapping = torch.empty(hkv, dtype=torch.int32, device=dev)
+    workspace, wsb = _ws(workspace, aoh_head_mapping_workspace_bytes(hq, hkv, d_head), dev)
+    ds = [tensor_desc(t) for t in (w_q_anchor, w_k_anchor, w_q_reuse, w_k_reuse)]
+    ma, mr = _Mask(anchor_is_streaming), _Mask(reuse_is_streaming)
+    _check(lib().aoh_head_mapping(*[ctypes.byref(d) for d in ds], d_head, ma.ptr, mr.ptr, _ptr(head_sim),
+                                  _ptr(group_sim), _ptr(mapping), _ptr(workspace), wsb, _stream(stream)))
+    return head_sim, group_sim, mapping
+
+
+def aoh_decode_anchor_workspace_bytes(batch, n_q_heads, d_head, max_pages_per_seq, ring_capacity):
+    return int(lib().aoh_decode_anchor_workspace_bytes(batch, n_q_heads, d_head, max_pages_per_seq, ring_capacity))
+
+
+def aoh_decode_anchor(q, kv_full, kv_ring, head_is_streaming, lens, n_sink, window, top_k, indices=None, out=None,
+                      workspace=None, stream=None):
+    """Anchor-layer decode step; returns (out, indices [B, n_retrieval_groups, top_k] int32)."""
+    if out is None:
+        out = torch.empty_like(q)
+    n_ret = sum(1 for x in head_is_streaming if not x)
+    if indices is None:
+        indices = torch.empty((q.shape[0], max(n_ret, 1), top_k), dtype=torch.int32, device=q.device)
+    max_pages = kv_full.block_table.shape[1] if kv_full is not None else 1
+    cap = kv_ring.capacity if kv_ring is not None else n_sink + window
+    workspace, wsb = _ws(workspace, aoh_decode_anchor_workspace_bytes(q.shape[0], q.shape[1], q.shape[2], max_pages,
+                                                                      cap), q.device)
+    qd, od = tensor_desc(q), tensor_desc(out)
+    fd = kv_full.desc() if kv_full is not None else None
+    rd = kv_ring.desc() if kv_ring is not None else None
+    m = _Mask(head_is_streaming)
+    _check(lib().aoh_decode_anchor(ctypes.byref(qd), ctypes.byref(fd) if fd else None,
+                                   ctypes.byref(rd) if rd else None, m.ptr, _ptr(lens), n_sink, window, top_k,
+                                   _ptr(indices), ctypes.byref(od), _ptr(workspace), wsb, _stream(stream)))
+    return out, indices
+
+
+def aoh_decode_reuse_workspace_bytes(batch, n_q_heads, d_head, top_k, ring_capacity):
+    return int(lib().aoh_decode_reuse_workspace_bytes(batch, n_q_heads, d_head, top_k, ring_capacity))
+
+
+def aoh_decode_reuse(q, kv_full, kv_ring, head_is_streaming, lens, n_sink, window, indices, mapping, out=None,
+                     workspace=None, stream=None):
+    """Reuse-layer decode step with borrowed positions indices [B, n_lists, top_k] (device int32) and
+    mapping (host sequence of Hkv list rows)."""
+    if out is None:
+        out = torch.empty_like(q)
+    n_lists, top_k = indices.shape[1], indices.shape[2]
+    cap = kv_ring.capacity if kv_ring is not None else n_sink + window
+    workspace, wsb = _ws(workspace, aoh_decode_reuse_workspace_bytes(q.shape[0], q.shape[1], q.shape[2], top_k, cap),
+                         q.device)
+    mp = (ctypes.c_int32 * len(mapping))(*[int(x) for x in mapping])
+    qd, od = tensor_desc(q), tensor_desc(out)
+    fd = kv_full.desc() if kv_full is not None else None
+    rd = kv_ring.desc() if kv_ring is not None else None
+    m = _Mask(head_is_streaming)
+    _check(lib().aoh_decode_reuse(ctypes.byref(qd), ctypes.byref(fd) if fd else None,
+                                  ctypes.byref(rd) if rd else None, m.ptr, _ptr(lens), n_sink, window, _ptr(indices),
+                                  n_lists, top_k, ctypes.cast(mp, ctypes.c_void_p), ctypes.byref(od), _ptr(workspace),
+                                  wsb, _stream(stream)))
+    return out
 
 
 def aoh_last_error():

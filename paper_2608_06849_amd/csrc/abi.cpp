@@ -361,10 +361,32 @@ size_t aoh_decode_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t d_he
   return workspace_bytes(batch, n_q_heads, d_head, plan_splits(batch, max_pages_per_seq, ring_capacity, 1, 1));
 }
 
-aoh_status aoh_decode(const aoh_tensor* q, const aoh_paged_cache* kv_full,
-                      const aoh_ring_cache* kv_ring, const uint8_t* head_is_streaming,
-                      const int32_t* lens, int32_t n_sink, int32_t window, aoh_tensor* out,
-                      void* workspace, size_t workspace_bytes_given, void* stream) {
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Anchor extras: scores [B][Hq][16 * max_pages] and final (m, l) [B][Hq][2].
+static size_t anchor_extra(int64_t B, int64_t Hq, int64_t max_pages) {
+  return align256((size_t)(B * Hq * max_pages * kPageTokens) * sizeof(float)) +
+         align256((size_t)(B * Hq * 2) * sizeof(float));
+}
+
+// H2Share roles of a decode call (Sec. "AoH-Guided Sparse Attention"): plain,
+// anchor layer (also selects top-k positions), reuse layer (retrieval heads
+// attend to borrowed positions).
+enum DecodeMode { kPlain = 0, kAnchor = 1, kReuse = 2 };
+
+struct DecodeExtra {
+  int mode = kPlain;
+  int32_t top_k = 0;          // anchor: positions to select; reuse: entries per list
+  int32_t* sel_out = nullptr; // anchor output [B][n_ret][top_k]
+  const int32_t* sel_in = nullptr;  // reuse input [B][n_lists][top_k]
+  int32_t n_lists = 0;
+  const int32_t* mapping = nullptr;  // reuse: HOST [Hkv], list rank per retrieval group
+};
+
+static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_full, const aoh_ring_cache* kv_ring,
+                              const uint8_t* head_is_streaming, const int32_t* lens, int32_t n_sink,
+                              int32_t window, aoh_tensor* out, void* workspace, size_t workspace_bytes_given,
+                              void* stream, const DecodeExtra& x) {
   aoh_status st;
   if ((st = check_tensor(q, "q", 3, AOH_BF16, AOH_F32))) return st;
   const int dt = q->dtype;
@@ -388,11 +410,32 @@ aoh_status aoh_decode(const aoh_tensor* q, const aoh_paged_cache* kv_full,
   if ((st = check_ring(kv_ring, hs.n_str, n_sink, window))) return st;
   const int gs = (int)(Hq / Hkv);
   if (dt == AOH_BF16 && gs > 16) return fail(AOH_ERR_UNSUPPORTED, "Hq/Hkv=%d > 16", gs);
+  if (x.mode != kPlain) {
+    if (dt != AOH_BF16) return fail(AOH_ERR_UNSUPPORTED, "anchor/reuse decode needs bf16");
+    if (x.top_k < 1 || x.top_k > (1 << 30)) return fail(AOH_ERR_INVALID_ARG, "top_k=%d must be >= 1", x.top_k);
+  }
+  if (x.mode == kAnchor && hs.n_ret && !x.sel_out) return fail(AOH_ERR_INVALID_ARG, "indices: null pointer");
+  uint8_t sel_rank[kMaxKvHeads] = {0};
+  if (x.mode == kReuse && hs.n_ret) {
+    if (!x.sel_in) return fail(AOH_ERR_INVALID_ARG, "indices: null pointer");
+    if (!x.mapping) return fail(AOH_ERR_INVALID_ARG, "mapping: null pointer");
+    if (x.n_lists < 1 || x.n_lists > kMaxKvHeads) return fail(AOH_ERR_INVALID_ARG, "n_lists=%d outside [1, 64]", x.n_lists);
+    for (int j = 0; j < hs.n_ret; ++j) {
+      const int32_t r = x.mapping[hs.ret[j]];
+      if (r < 0 || r >= x.n_lists)
+        return fail(AOH_ERR_INVALID_ARG, "mapping[%d]=%d: a retrieval group needs a list in [0, %d)", hs.ret[j], r,
+                    x.n_lists);
+      sel_rank[j] = (uint8_t)r;
+    }
+  }
   const int max_pages = hs.n_ret ? kv_full->max_pages_per_seq : 1;
   const int ring_cap = n_sink + window;
-  const SplitPlan sp = plan_splits((int)B, max_pages, ring_cap, hs.n_ret, hs.n_str);
+  // Reuse: the paged items run over the borrowed list, cut like a cache of
+  // ceil(top_k / 16) blocks.
+  const int plan_pages = x.mode == kReuse ? (int)ceil_div(x.top_k, kPageTokens) : max_pages;
+  const SplitPlan sp = plan_splits((int)B, plan_pages, ring_cap, hs.n_ret, hs.n_str);
   // The workspace is sized for the n_ret = n_str = 1 plan, which bounds this one.
-  const SplitPlan sp_bound = plan_splits((int)B, max_pages, ring_cap, 1, 1);
+  const SplitPlan sp_bound = plan_splits((int)B, plan_pages, ring_cap, 1, 1);
 
   DecodeArgs a;
   std::memset(&a, 0, sizeof(a));
@@ -429,7 +472,8 @@ aoh_status aoh_decode(const aoh_tensor* q, const aoh_paged_cache* kv_full,
     return ok();
   }
 
-  const size_t need = workspace_bytes((int)B, (int)Hq, (int)D, sp_bound);
+  const size_t base_need = workspace_bytes((int)B, (int)Hq, (int)D, sp_bound);
+  const size_t need = x.mode == kAnchor ? align256(base_need) + anchor_extra(B, Hq, max_pages) : base_need;
   if (!workspace) return fail(AOH_ERR_WORKSPACE, "workspace is null; %zu bytes needed", need);
   if (workspace_bytes_given < need)
     return fail(AOH_ERR_WORKSPACE, "workspace has %zu bytes; %zu needed", workspace_bytes_given, need);
@@ -437,9 +481,22 @@ aoh_status aoh_decode(const aoh_tensor* q, const aoh_paged_cache* kv_full,
   float* part_acc = reinterpret_cast<float*>(workspace);
   float* part_ml = part_acc + (size_t)B * Hq * sp_bound.max_splits * D;
   a.part_acc = part_acc; a.part_ml = part_ml; a.max_splits = sp_bound.max_splits;
+  float* scores = nullptr;
+  float* ml = nullptr;
+  if (x.mode == kAnchor) {
+    char* w = reinterpret_cast<char*>(workspace) + align256(base_need);
+    scores = reinterpret_cast<float*>(w);
+    ml = reinterpret_cast<float*>(w + align256((size_t)(B * Hq * max_pages * kPageTokens) * sizeof(float)));
+    a.scores = scores;
+    a.score_len = max_pages * kPageTokens;
+  }
+  if (x.mode == kReuse) {
+    a.sel = x.sel_in; a.n_sel = x.top_k; a.n_lists = x.n_lists;
+    std::memcpy(a.sel_rank, sel_rank, sizeof(sel_rank));
+  }
   if ((int64_t)a.full.n_items + a.ring.n_items >= (1ll << 31)) return fail(AOH_ERR_UNSUPPORTED, "grid too large");
   {
-    hipError_t e = launch_decode_split(a, (int)D, s);
+    hipError_t e = launch_decode_split(a, (int)D, x.mode, s);
     if (e != hipSuccess) return fail(AOH_ERR_HIP, "decode split launch: %s", hipGetErrorString(e));
   }
   MergeArgs m;
@@ -451,12 +508,137 @@ aoh_status aoh_decode(const aoh_tensor* q, const aoh_paged_cache* kv_full,
   m.split_tokens_ring = sp.split_blocks_ring * kPageTokens;
   m.n_splits_full = sp.n_splits_full;
   m.n_splits_ring = sp.n_splits_ring;
-  m.max_len = max_pages * kPageTokens;
+  // reuse: a retrieval head's "length" is its number of borrowed entries
+  m.max_len = x.mode == kReuse ? x.top_k : max_pages * kPageTokens;
   m.ring_cap = ring_cap;
   m.streaming_mask = hs.streaming_mask;
+  m.ml_out = ml;
   const int out_f32 = out->dtype == AOH_F32;
   hipError_t e = launch_decode_merge(m, dt, out_f32, (int)D, s);
   if (e != hipSuccess) return fail(AOH_ERR_HIP, "decode merge launch: %s", hipGetErrorString(e));
+  if (x.mode == kAnchor && hs.n_ret) {
+    TopkArgs t;
+    std::memset(&t, 0, sizeof(t));
+    t.scores = scores; t.ml = ml; t.lens = lens; t.sel = x.sel_out;
+    t.B = (int)B; t.Hq = (int)Hq; t.gs = gs; t.n_kv = hs.n_ret;
+    t.score_len = max_pages * kPageTokens;
+    t.n_sel = x.top_k;
+    std::memcpy(t.kv_heads, hs.ret, hs.n_ret);
+    if (B > 65535) return fail(AOH_ERR_UNSUPPORTED, "batch too large");
+    e = launch_topk(t, s);
+    if (e != hipSuccess) return fail(AOH_ERR_HIP, "top-k launch: %s", hipGetErrorString(e));
+  }
+  return ok();
+}
+
+aoh_status aoh_decode(const aoh_tensor* q, const aoh_paged_cache* kv_full,
+                      const aoh_ring_cache* kv_ring, const uint8_t* head_is_streaming,
+                      const int32_t* lens, int32_t n_sink, int32_t window, aoh_tensor* out,
+                      void* workspace, size_t workspace_bytes_given, void* stream) {
+  return decode_impl(q, kv_full, kv_ring, head_is_streaming, lens, n_sink, window, out, workspace,
+                     workspace_bytes_given, stream, DecodeExtra());
+}
+
+size_t aoh_decode_anchor_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t d_head,
+                                         int32_t max_pages_per_seq, int32_t ring_capacity) {
+  const size_t base = aoh_decode_workspace_bytes(batch, n_q_heads, d_head, max_pages_per_seq, ring_capacity);
+  if (!base) return 0;
+  return align256(base) + anchor_extra(batch, n_q_heads, max_pages_per_seq);
+}
+
+aoh_status aoh_decode_anchor(const aoh_tensor* q, const aoh_paged_cache* kv_full,
+                             const aoh_ring_cache* kv_ring, const uint8_t* head_is_streaming,
+                             const int32_t* lens, int32_t n_sink, int32_t window, int32_t top_k,
+                             int32_t* indices, aoh_tensor* out, void* workspace, size_t workspace_bytes_given,
+                             void* stream) {
+  DecodeExtra x;
+  x.mode = kAnchor; x.top_k = top_k; x.sel_out = indices;
+  return decode_impl(q, kv_full, kv_ring, head_is_streaming, lens, n_sink, window, out, workspace,
+                     workspace_bytes_given, stream, x);
+}
+
+size_t aoh_decode_reuse_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t d_head, int32_t top_k,
+                                        int32_t ring_capacity) {
+  if (top_k < 1) return 0;
+  return aoh_decode_workspace_bytes(batch, n_q_heads, d_head, (int32_t)ceil_div(top_k, kPageTokens), ring_capacity);
+}
+
+aoh_status aoh_decode_reuse(const aoh_tensor* q, const aoh_paged_cache* kv_full,
+                            const aoh_ring_cache* kv_ring, const uint8_t* head_is_streaming,
+                            const int32_t* lens, int32_t n_sink, int32_t window, const int32_t* indices,
+                            int32_t n_lists, int32_t top_k, const int32_t* mapping, aoh_tensor* out,
+                            void* workspace, size_t workspace_bytes_given, void* stream) {
+  DecodeExtra x;
+  x.mode = kReuse; x.top_k = top_k; x.sel_in = indices; x.n_lists = n_lists; x.mapping = mapping;
+  return decode_impl(q, kv_full, kv_ring, head_is_streaming, lens, n_sink, window, out, workspace,
+                     workspace_bytes_given, stream, x);
+}
+
+static size_t mapping_ws(int64_t hq, int64_t hkv, int64_t d) {
+  return align256((size_t)(2 * (hq + hkv) * d * d) * sizeof(float)) +
+         align256((size_t)(hkv * hkv * d * d) * sizeof(float)) + align256((size_t)(hq * hq) * sizeof(double)) +
+         align256((size_t)(2 * hq) * sizeof(double));
+}
+
+size_t aoh_head_mapping_workspace_bytes(int32_t n_q_heads, int32_t n_kv_heads, int32_t d_head) {
+  if (n_q_heads < 1 || n_kv_heads < 1 || (d_head != 64 && d_head != 128)) return 0;
+  return mapping_ws(n_q_heads, n_kv_heads, d_head);
+}
+
+aoh_status aoh_head_mapping(const aoh_tensor* w_q_anchor, const aoh_tensor* w_k_anchor,
+                            const aoh_tensor* w_q_reuse, const aoh_tensor* w_k_reuse, int32_t d_head,
+                            const uint8_t* anchor_is_streaming, const uint8_t* reuse_is_streaming,
+                            double* head_sim, double* group_sim, int32_t* mapping, void* workspace,
+                            size_t workspace_bytes_given, void* stream) {
+  aoh_status st;
+  const aoh_tensor* ws4[4] = {w_q_anchor, w_k_anchor, w_q_reuse, w_k_reuse};
+  const char* names[4] = {"w_q_anchor", "w_k_anchor", "w_q_reuse", "w_k_reuse"};
+  for (int i = 0; i < 4; ++i)
+    if ((st = check_tensor(ws4[i], names[i], 2, AOH_BF16, AOH_BF16))) return st;
+  if (d_head != 64 && d_head != 128) return fail(AOH_ERR_UNSUPPORTED, "d_head=%d; supported: 64, 128", d_head);
+  const int64_t dm = w_q_anchor->shape[1];
+  for (int i = 1; i < 4; ++i)
+    if (ws4[i]->shape[1] != dm) return fail(AOH_ERR_INVALID_ARG, "all weights need the same d_model");
+  if (w_q_reuse->shape[0] != w_q_anchor->shape[0] || w_k_reuse->shape[0] != w_k_anchor->shape[0])
+    return fail(AOH_ERR_INVALID_ARG, "anchor and reuse layers need the same head counts");
+  if (w_q_anchor->shape[0] % d_head || w_k_anchor->shape[0] % d_head)
+    return fail(AOH_ERR_INVALID_ARG, "rows of w_q / w_k must be a multiple of d_head");
+  const int64_t Hq = w_q_anchor->shape[0] / d_head, Hkv = w_k_anchor->shape[0] / d_head;
+  if (Hq % Hkv) return fail(AOH_ERR_UNSUPPORTED, "Hq=%lld is not a multiple of Hkv=%lld", (long long)Hq, (long long)Hkv);
+  if (Hkv > kMaxKvHeads) return fail(AOH_ERR_UNSUPPORTED, "Hkv=%lld > %d", (long long)Hkv, kMaxKvHeads);
+  if (Hq * Hq >= (1ll << 31)) return fail(AOH_ERR_UNSUPPORTED, "too many heads");
+  if (dm % 64) return fail(AOH_ERR_UNSUPPORTED, "d_model=%lld must be a multiple of 64", (long long)dm);
+  if (!head_sim || !group_sim || !mapping) return fail(AOH_ERR_INVALID_ARG, "null output pointer");
+  if (reinterpret_cast<uintptr_t>(head_sim) % 8 || reinterpret_cast<uintptr_t>(group_sim) % 8)
+    return fail(AOH_ERR_INVALID_ARG, "head_sim / group_sim must be 8-byte aligned");
+  HeadSchedule ha, hr;
+  if ((st = schedule_heads(anchor_is_streaming, (int)Hkv, &ha))) return st;
+  if ((st = schedule_heads(reuse_is_streaming, (int)Hkv, &hr))) return st;
+  if (ha.n_ret == 0) return fail(AOH_ERR_INVALID_ARG, "the anchor layer has no retrieval group");
+  const size_t need = mapping_ws(Hq, Hkv, d_head);
+  if (!workspace) return fail(AOH_ERR_WORKSPACE, "workspace is null; %zu bytes needed", need);
+  if (workspace_bytes_given < need)
+    return fail(AOH_ERR_WORKSPACE, "workspace has %zu bytes; %zu needed", workspace_bytes_given, need);
+  if (reinterpret_cast<uintptr_t>(workspace) % 16) return fail(AOH_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
+
+  SimilarityArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.wq_a = w_q_anchor->data; a.wk_a = w_k_anchor->data; a.wq_r = w_q_reuse->data; a.wk_r = w_k_reuse->data;
+  a.wq_a_sr = w_q_anchor->stride[0]; a.wk_a_sr = w_k_anchor->stride[0];
+  a.wq_r_sr = w_q_reuse->stride[0]; a.wk_r_sr = w_k_reuse->stride[0];
+  a.Hq = (int)Hq; a.Hkv = (int)Hkv; a.gs = (int)(Hq / Hkv); a.d_model = (int)dm;
+  char* w = reinterpret_cast<char*>(workspace);
+  a.gram = reinterpret_cast<float*>(w);
+  w += align256((size_t)(2 * (Hq + Hkv) * d_head * d_head) * sizeof(float));
+  a.kx = reinterpret_cast<float*>(w);
+  w += align256((size_t)(Hkv * Hkv * d_head * d_head) * sizeof(float));
+  a.num = reinterpret_cast<double*>(w);
+  w += align256((size_t)(Hq * Hq) * sizeof(double));
+  a.n2 = reinterpret_cast<double*>(w);
+  a.head_sim = head_sim; a.group_sim = group_sim; a.mapping = mapping;
+  a.anchor_streaming = ha.streaming_mask; a.reuse_streaming = hr.streaming_mask;
+  hipError_t e = launch_similarity(a, d_head, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(AOH_ERR_HIP, "head mapping launch: %s", hipGetErrorString(e));
   return ok();
 }
 

@@ -73,6 +73,16 @@ struct DecodeArgs {
   float scale;
   CacheView full;
   CacheView ring;
+  // Anchor layer (H2Share): scaled scores of the paged-cache heads,
+  // [B][Hq][score_len] in log2 units, for positions < lens.
+  float* scores;
+  int32_t score_len;
+  // Reuse layer (H2Share): paged-cache items attend to borrowed positions
+  // sel[b][sel_rank[j]][0..n_sel) (ascending, -1 = none) of KV head j of the
+  // list, in chunks of split_blocks * 16 list entries per split.
+  const int32_t* sel;
+  int32_t n_sel, n_lists;
+  uint8_t sel_rank[kMaxKvHeads];
 };
 
 struct MergeArgs {
@@ -90,6 +100,7 @@ struct MergeArgs {
   int32_t max_len;              // 16 * pages per sequence: lens are clamped to it
   int32_t ring_cap;
   uint64_t streaming_mask;      // bit g set = KV head g streaming
+  float* ml_out;                // anchor layer: final (m, l) of each paged-cache head, [B][Hq][2]
 };
 
 struct AppendArgs {
@@ -137,11 +148,45 @@ struct ClassifyArgs {
 // Launchers (return the launch status; no synchronisation).
 hipError_t launch_prefill(const PrefillArgs& a, int dtype, int out_f32, int d, bool streaming,
                           hipStream_t s);
-hipError_t launch_decode_split(const DecodeArgs& a, int d, hipStream_t s);
+// mode: 0 plain, 1 anchor (also writes scores), 2 reuse (sparse paged items)
+hipError_t launch_decode_split(const DecodeArgs& a, int d, int mode, hipStream_t s);
 hipError_t launch_decode_merge(const MergeArgs& a, int dtype, int out_f32, int d, hipStream_t s);
 hipError_t launch_decode_f32(const DecodeArgs& a, int d, void* out, int64_t o_sb, int64_t o_sh, hipStream_t s);
 hipError_t launch_append(const AppendArgs& a, int dtype, int d, hipStream_t s);
 hipError_t launch_classify(const ClassifyArgs& a, int d, hipStream_t s);
+
+// Top-k selection of an anchor decode step (H2Share): per (sequence, paged
+// KV head j of the list), the n_sel positions of highest group-mean attention
+// probability, ascending, padded with -1.
+struct TopkArgs {
+  float* scores;                // [B][Hq][score_len]; the group's first head row is reused for keys
+  const float* ml;              // [B][Hq][2] final (m, l)
+  const int32_t* lens;
+  int32_t* sel;                 // [B][n_kv][n_sel]
+  int32_t B, Hq, gs, n_kv;
+  int32_t score_len;            // positions per row (16 * pages per sequence)
+  int32_t n_sel;
+  uint8_t kv_heads[kMaxKvHeads];
+};
+hipError_t launch_topk(const TopkArgs& a, hipStream_t s);
+
+// Cross-layer head similarity (H2Share): grams of both layers are in gram
+// ([2][Hq + Hkv][D][D]: anchor, reuse), KX[g][g'] = W_K^g W_K'^g'^T in kx,
+// num[h][h'] = <W_Q^h W_Q'^h'^T, KX[g(h)][g(h')]>_F.
+struct SimilarityArgs {
+  const void* wq_a; const void* wk_a; const void* wq_r; const void* wk_r;
+  int64_t wq_a_sr, wk_a_sr, wq_r_sr, wk_r_sr;   // row strides
+  int32_t Hq, Hkv, gs, d_model;
+  float* gram;
+  float* kx;                    // [Hkv][Hkv][D][D]
+  double* num;                  // [Hq][Hq]
+  double* n2;                   // [2][Hq] squared Frobenius norms (anchor, reuse)
+  double* head_sim;             // [Hq][Hq] out
+  double* group_sim;            // [Hkv][Hkv] out
+  int32_t* mapping;             // [Hkv] out: anchor retrieval rank, -1 for streaming reuse groups
+  uint64_t anchor_streaming, reuse_streaming;
+};
+hipError_t launch_similarity(const SimilarityArgs& a, int d, hipStream_t s);
 
 // Largest number of splits per (sequence, head) the merge pass accepts.
 constexpr int kMaxSplits = 1024;

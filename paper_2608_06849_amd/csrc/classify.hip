@@ -463,6 +463,188 @@ __global__ __launch_bounds__(kWave) void select_kernel(ClassifyArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Cross-layer head similarity of H2Share (Eq. sim, by the trace identities of
+// the trace-reduction appendix): for anchor layer l and reuse layer l',
+//   <M_h, M_h'>_F = tr(W_Q^h W_Q'^h'^T . W_K'^g' W_K^g^T)
+//                 = sum_ab (W_Q^h W_Q'^h'^T)[a][b] (W_K^g W_K'^g'^T)[a][b],
+//   |M_h|_F^2     = sum_ab (W_Q W_Q^T)[a][b] (W_K W_K^T)[a][b]  (symmetric Grams).
+
+// C = A B^T for a d x d_model slice A of one weight and a slice B of another
+// (bf16 MFMA, fp32 accumulation), the slab of 64 columns of both staged in
+// LDS.  Wave w computes the 32-row block w against all column blocks.
+// STORE: C goes to kx[(g * Hkv + g') * D * D]; otherwise the tile is multiplied
+// elementwise with kx of the heads' groups and summed into num[h][h'].
+template <int D, bool STORE>
+__global__ __launch_bounds__(64 * (D / 32)) void cross_kernel(SimilarityArgs a) {
+  constexpr int NRB = D / 32;
+  __shared__ __align__(16) bf16 stage[2][2][D][kGramRowPad];
+  __shared__ double red[NRB];
+  const int n = STORE ? a.Hkv : a.Hq;
+  const int u = blockIdx.x / n, v = blockIdx.x % n;  // (anchor unit, reuse unit)
+  const bf16* wa = STORE ? static_cast<const bf16*>(a.wk_a) + (int64_t)u * D * a.wk_a_sr
+                         : static_cast<const bf16*>(a.wq_a) + (int64_t)u * D * a.wq_a_sr;
+  const bf16* wb = STORE ? static_cast<const bf16*>(a.wk_r) + (int64_t)v * D * a.wk_r_sr
+                         : static_cast<const bf16*>(a.wq_r) + (int64_t)v * D * a.wq_r_sr;
+  const int64_t rsa = STORE ? a.wk_a_sr : a.wq_a_sr, rsb = STORE ? a.wk_r_sr : a.wq_r_sr;
+  const int t = threadIdx.x;
+  const int wave = t >> 6, lane = t & 63, l32 = lane & 31, half = lane >> 5;
+  const int lrow = t >> 1, lcol = (t & 1) * 32;
+  const bf16* srca = wa + (int64_t)lrow * rsa + lcol;
+  const bf16* srcb = wb + (int64_t)lrow * rsb + lcol;
+
+  f32x16 acc[NRB];
+#pragma unroll
+  for (int c = 0; c < NRB; ++c) acc[c] = f32x16{};
+  u32x4 la[4], lb[4];
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int s2 = 0; s2 < 4; ++s2) {
+      la[s2] = ld16(srca + k0 + 8 * s2);
+      lb[s2] = ld16(srcb + k0 + 8 * s2);
+    }
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int s2 = 0; s2 < 4; ++s2) {
+      st16(&stage[buf][0][lrow][lcol + 8 * s2], la[s2]);
+      st16(&stage[buf][1][lrow][lcol + 8 * s2], lb[s2]);
+    }
+  };
+  auto compute = [&](int buf) {
+#pragma unroll
+    for (int s2 = 0; s2 < 4; ++s2) {
+      const bf16x8 xa = as_bf16x8(*reinterpret_cast<const u32x4*>(&stage[buf][0][32 * wave + l32][32 * half + 8 * s2]));
+#pragma unroll
+      for (int c = 0; c < NRB; ++c) {
+        const bf16x8 xb = as_bf16x8(*reinterpret_cast<const u32x4*>(&stage[buf][1][32 * c + l32][32 * half + 8 * s2]));
+        acc[c] = mfma32(xa, xb, acc[c]);
+      }
+    }
+  };
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  const int n_it = a.d_model / kGramBK;
+  for (int it = 0; it < n_it; ++it) {
+    const int cur = it & 1;
+    const bool more = it + 1 < n_it;
+    if (more) gload((it + 1) * kGramBK);
+    compute(cur);
+    if (more) lstore(cur ^ 1);
+    __syncthreads();
+  }
+
+  if (STORE) {
+    float* out = a.kx + (int64_t)(u * a.Hkv + v) * D * D;
+#pragma unroll
+    for (int c = 0; c < NRB; ++c)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int m = 32 * wave + 8 * (i / 4) + 4 * half + (i % 4);
+        out[(int64_t)m * D + 32 * c + l32] = acc[c][i];
+      }
+  } else {
+    const float* kx = a.kx + (int64_t)((u / a.gs) * a.Hkv + v / a.gs) * D * D;
+    double sum = 0.0;
+#pragma unroll
+    for (int c = 0; c < NRB; ++c)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int m = 32 * wave + 8 * (i / 4) + 4 * half + (i % 4);
+        sum += (double)acc[c][i] * (double)kx[(int64_t)m * D + 32 * c + l32];
+      }
+    sum = wave_sum_f64(sum);
+    if (lane == 0) red[wave] = sum;
+    __syncthreads();
+    if (t == 0) {
+      double tot = 0.0;
+#pragma unroll
+      for (int w = 0; w < NRB; ++w) tot += red[w];
+      a.num[(int64_t)u * a.Hq + v] = tot;
+    }
+  }
+}
+
+// |M_h|_F^2 of every query head of both layers from the Grams:
+// blockIdx.x = layer * Hq + h.
+template <int D>
+__global__ __launch_bounds__(kEigThreads) void norm_kernel(SimilarityArgs a) {
+  __shared__ double red[kEigWaves];
+  const int layer = blockIdx.x / a.Hq, h = blockIdx.x % a.Hq;
+  const int n_heads = a.Hq + a.Hkv;
+  const float* qq = a.gram + ((int64_t)layer * n_heads + h) * D * D;
+  const float* kk = a.gram + ((int64_t)layer * n_heads + a.Hq + h / a.gs) * D * D;
+  double sum = 0.0;
+  for (int e = threadIdx.x; e < D * D; e += kEigThreads) sum += (double)qq[e] * (double)kk[e];
+  sum = wave_sum_f64(sum);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = sum;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double tot = 0.0;
+#pragma unroll
+    for (int w = 0; w < kEigWaves; ++w) tot += red[w];
+    a.n2[blockIdx.x] = tot;
+  }
+}
+
+// Normalisation, group means and the mapping (one workgroup).
+__global__ __launch_bounds__(kEigThreads) void mapping_kernel(SimilarityArgs a) {
+  const int hq = a.Hq, hkv = a.Hkv, gs = a.gs;
+  const double* n2 = a.n2;  // [2][Hq] squared norms
+  for (int e = threadIdx.x; e < hq * hq; e += kEigThreads) {
+    const int h = e / hq, h2 = e % hq;
+    a.head_sim[e] = a.num[e] / (sqrt(n2[h]) * sqrt(n2[hq + h2]));
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < hkv * hkv; e += kEigThreads) {
+    const int g = e / hkv, g2 = e % hkv;
+    double sum = 0.0;
+    for (int i = 0; i < gs; ++i)
+      for (int j = 0; j < gs; ++j) sum += a.head_sim[(int64_t)(g * gs + i) * hq + g2 * gs + j];
+    a.group_sim[e] = sum / (gs * gs);
+  }
+  __syncthreads();
+  const int g2 = threadIdx.x;
+  if (g2 < hkv) {
+    int best = -1, rank = -1, r = 0;
+    if (!((a.reuse_streaming >> g2) & 1ull)) {
+      for (int g = 0; g < hkv; ++g) {
+        if ((a.anchor_streaming >> g) & 1ull) continue;
+        if (best < 0 || a.group_sim[g * hkv + g2] > a.group_sim[best * hkv + g2]) {
+          best = g;
+          rank = r;
+        }
+        ++r;
+      }
+    }
+    a.mapping[g2] = rank;
+  }
+}
+
+template <int D>
+hipError_t launch_similarity_d(const SimilarityArgs& a, hipStream_t s) {
+  // Grams of both layers (the classifier's kernel, one layer each)
+  for (int layer = 0; layer < 2; ++layer) {
+    ClassifyArgs c;
+    __builtin_memset(&c, 0, sizeof(c));
+    c.wq = layer ? a.wq_r : a.wq_a;
+    c.wk = layer ? a.wk_r : a.wk_a;
+    c.wq_sr = layer ? a.wq_r_sr : a.wq_a_sr;
+    c.wk_sr = layer ? a.wk_r_sr : a.wk_a_sr;
+    c.L = 1; c.Hq = a.Hq; c.Hkv = a.Hkv; c.gs = a.gs; c.d_model = a.d_model;
+    c.gram = a.gram + (int64_t)layer * (a.Hq + a.Hkv) * D * D;
+    hipLaunchKernelGGL(gram_kernel<D>, dim3(a.Hq + a.Hkv), dim3(64 * (D / 32)), 0, s, c);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((cross_kernel<D, true>), dim3(a.Hkv * a.Hkv), dim3(64 * (D / 32)), 0, s, a);
+  hipLaunchKernelGGL((cross_kernel<D, false>), dim3(a.Hq * a.Hq), dim3(64 * (D / 32)), 0, s, a);
+  hipLaunchKernelGGL(norm_kernel<D>, dim3(2 * a.Hq), dim3(kEigThreads), 0, s, a);
+  hipLaunchKernelGGL(mapping_kernel, dim3(1), dim3(kEigThreads), 0, s, a);
+  return hipGetLastError();
+}
+
 template <int D>
 hipError_t launch_classify_d(const ClassifyArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(gram_kernel<D>, dim3(a.L * (a.Hq + a.Hkv)), dim3(64 * (D / 32)), 0, s, a);
@@ -480,6 +662,10 @@ hipError_t launch_classify_d(const ClassifyArgs& a, hipStream_t s) {
 
 hipError_t launch_classify(const ClassifyArgs& a, int d, hipStream_t s) {
   return d == 128 ? launch_classify_d<128>(a, s) : launch_classify_d<64>(a, s);
+}
+
+hipError_t launch_similarity(const SimilarityArgs& a, int d, hipStream_t s) {
+  return d == 128 ? launch_similarity_d<128>(a, s) : launch_similarity_d<64>(a, s);
 }
 
 }  // namespace aoh

@@ -24,7 +24,7 @@
 
 namespace aoh {
 
-template <int D, bool RING>
+template <int D, bool RING, bool SCORES = false>
 __device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const CacheView& cv, int item) {
   constexpr int kKSteps = D / 32;   // 32-dim k-steps for Q K^T
   constexpr int kDimBlocks = D / 16;
@@ -148,6 +148,18 @@ __device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const Cac
         x[4 * X + i] = v;
         mx = fmaxf(mx, v);
       }
+    if (SCORES && head_ok) {
+      // anchor layer: keep the scaled scores for the top-k selection
+      float* sp = a.scores + ((int64_t)b * a.Hq + hq) * a.score_len + tok0;
+      if (!partial) {
+        *reinterpret_cast<f32x4*>(sp) = f32x4{x[0], x[1], x[2], x[3]};
+        *reinterpret_cast<f32x4*>(sp + 4) = f32x4{x[4], x[5], x[6], x[7]};
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (tok0 + j < tok_end) sp[j] = x[j];
+      }
+    }
     mx = wave_xor_max(mx, 16);
     mx = wave_xor_max(mx, 32);
     const float m_new = fmaxf(m_run, mx);  // finite: every chunk holds a valid token
@@ -199,12 +211,162 @@ __device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const Cac
 }
 
 
-// One launch for both cache types: paged-cache items first, ring items last.
+// Reuse layer of H2Share: one wave per (sequence, paged KV head, split of its
+// borrowed position list).  The same 16x16x32 MFMA structure as the dense
+// body, on gathered tokens: each lane loads the K rows of its two MFMA rows
+// from their own pages (16-byte loads), and the V^T operand element by
+// element from the dimension-major pages (the 8 tokens of a lane group are in
+// general on 8 different pages).  List entries < 0 or beyond the sequence
+// are masked out.
 template <int D>
+__device__ __forceinline__ void decode_sparse_body(const DecodeArgs& a, const CacheView& cv, int item) {
+  constexpr int kKSteps = D / 32;
+  constexpr int kDimBlocks = D / 16;
+  const int split = item % cv.n_splits;
+  const int rest = item / cv.n_splits;
+  const int kvl = rest % cv.n_kv;
+  const int b = rest / cv.n_kv;
+  const int g = cv.kv_heads[kvl];
+  const int lane = threadIdx.x;
+  const int col = lane & 15;
+  const int G = lane >> 4;
+  const int len = a.lens[b];
+  const int n_valid = min(len, cv.max_pages * kPage);
+  const int split_len = cv.split_blocks * kPage;
+  const int e0 = split * split_len;
+  const int e_end = min(e0 + split_len, a.n_sel);
+  if (e0 >= e_end) return;
+  const int32_t* list = a.sel + ((int64_t)b * a.n_lists + a.sel_rank[kvl]) * a.n_sel;
+
+  const bool head_ok = col < a.gs;
+  const int hq = g * a.gs + col;
+  bf16x8 qreg[kKSteps];
+  {
+    const uint16_t* qp = reinterpret_cast<const uint16_t*>(a.q) + (int64_t)b * a.q_sb + (int64_t)hq * a.q_sh;
+#pragma unroll
+    for (int s = 0; s < kKSteps; ++s) {
+      u32x4 x = {0u, 0u, 0u, 0u};
+      if (head_ok) x = ld16(qp + 32 * s + 8 * G);
+      qreg[s] = __builtin_bit_cast(bf16x8, x);
+    }
+  }
+  const uint16_t* kc = reinterpret_cast<const uint16_t*>(cv.k);
+  const uint16_t* vc = reinterpret_cast<const uint16_t*>(cv.v);
+  // cache unit of a position (page of the block table); invalid -> unit 0
+  auto unit_of = [&](int pos) -> int64_t {
+    if (pos < 0 || pos >= n_valid) return 0;
+    int page = cv.block_table[(int64_t)b * cv.max_pages + pos / kPage];
+    page = (page < 0 || page >= cv.num_pages) ? 0 : page;
+    return (int64_t)page * cv.n_kv + kvl;
+  };
+  const int m = lane & 15;
+  const int slot_k0 = 8 * (m >> 2) + (m & 3);  // chunk slot of MFMA row m, token block 0 (+4 for block 1)
+
+  f32x4 acc[kDimBlocks];
+#pragma unroll
+  for (int nb = 0; nb < kDimBlocks; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY;
+  float l_run = 0.f;
+
+  for (int c0 = e0; c0 < e_end; c0 += 32) {
+    // the chunk's 32 list entries, one per lane of the low half
+    const int my_e = c0 + (lane & 31);
+    const int my_pos = my_e < e_end ? list[my_e] : -1;
+    u32x4 kcur[2][kKSteps];
+#pragma unroll
+    for (int X = 0; X < 2; ++X) {
+      const int pos = __shfl(my_pos, slot_k0 + 4 * X, kWave);
+      const int64_t kb = unit_of(pos) * (kPage * D) + (int64_t)((pos < 0 ? 0 : pos) % kPage) * D;
+#pragma unroll
+      for (int s = 0; s < kKSteps; ++s) kcur[X][s] = ld16(kc + kb + 32 * s + 8 * G);
+    }
+    int vpos[8];
+    bool vok[8];
+    int64_t vb[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      vpos[j] = __shfl(my_pos, 8 * G + j, kWave);
+      vok[j] = vpos[j] >= 0 && vpos[j] < n_valid;
+      vb[j] = unit_of(vpos[j]) * (kPage * D) + (vok[j] ? vpos[j] % kPage : 0);
+    }
+    bf16x8 vcur[kDimBlocks];
+#pragma unroll
+    for (int nb = 0; nb < kDimBlocks; ++nb)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const uint16_t raw = vc[vb[j] + (int64_t)(16 * nb + (lane & 15)) * kPage];
+        vcur[nb][j] = vok[j] ? __builtin_bit_cast(bf16, raw) : (bf16)0.f;
+      }
+
+    f32x4 sc[2];
+#pragma unroll
+    for (int X = 0; X < 2; ++X) {
+      sc[X] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < kKSteps; ++s) sc[X] = mfma16(__builtin_bit_cast(bf16x8, kcur[X][s]), qreg[s], sc[X]);
+    }
+    float x[8];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int X = 0; X < 2; ++X)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int j = 4 * X + i;  // chunk slot 8G + j
+        float v = sc[X][i] * a.scale_log2;
+        if (!vok[j]) v = -INFINITY;
+        x[j] = v;
+        mx = fmaxf(mx, v);
+      }
+    mx = wave_xor_max(mx, 16);
+    mx = wave_xor_max(mx, 32);
+    const float m_new = fmaxf(m_run, mx);
+    if (m_new == -INFINITY) continue;  // no valid entry in this chunk (wave-uniform)
+    const float alpha = fast_exp2(m_run - m_new);
+    m_run = m_new;
+    bf16x8 pop;
+    float psum = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float p = fast_exp2(x[j] - m_new);
+      psum += p;
+      pop[j] = f32_to_bf16(p);
+    }
+    l_run = l_run * alpha + psum;
+#pragma unroll
+    for (int nb = 0; nb < kDimBlocks; ++nb) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[nb][i] *= alpha;
+      acc[nb] = mfma16(vcur[nb], pop, acc[nb]);
+    }
+  }
+
+  float l_tot = wave_xor_sum(l_run, 16);
+  l_tot = wave_xor_sum(l_tot, 32);
+  if (head_ok) {
+    const int64_t slot = ((int64_t)b * a.Hq + hq) * a.max_splits + split;
+    float* pa = a.part_acc + slot * D;
+#pragma unroll
+    for (int nb = 0; nb < kDimBlocks; ++nb)
+      *reinterpret_cast<f32x4*>(pa + 16 * nb + 4 * G) = acc[nb];
+    if (G == 0) {
+      a.part_ml[slot * 2 + 0] = m_run;
+      a.part_ml[slot * 2 + 1] = l_tot;
+    }
+  }
+}
+
+// One launch for both cache types: paged-cache items first, ring items last.
+// MODE 0: plain decode; 1: anchor layer (paged items also keep their scores);
+// 2: reuse layer (paged items attend to borrowed positions only).
+template <int D, int MODE>
 __global__ __launch_bounds__(kWave) void decode_split_bf16_kernel(DecodeArgs a) {
   const int wg = blockIdx.x;
-  if (wg < a.full.n_items) decode_split_body<D, false>(a, a.full, wg);
-  else decode_split_body<D, true>(a, a.ring, wg - a.full.n_items);
+  if (wg < a.full.n_items) {
+    if (MODE == 2) decode_sparse_body<D>(a, a.full, wg);
+    else decode_split_body<D, false, MODE == 1>(a, a.full, wg);
+  } else {
+    decode_split_body<D, true>(a, a.ring, wg - a.full.n_items);
+  }
 }
 
 // fp32 decode: one workgroup of 64 threads per (sequence, query head) of the
@@ -354,6 +516,10 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(MergeArgs a
   for (int s = grp; s < ns; s += kGroups) acc += s_w[s] * a.part_acc[(base + s) * D + d];
   s_acc[grp][dd] = acc;
   __syncthreads();
+  if (a.ml_out && !streaming && slice == 0 && tid == 0) {
+    a.ml_out[((int64_t)b * a.Hq + hq) * 2 + 0] = mx;
+    a.ml_out[((int64_t)b * a.Hq + hq) * 2 + 1] = L;
+  }
   if (grp == 0) {
     float tot = 0.f;
 #pragma unroll
@@ -367,10 +533,17 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(MergeArgs a
   }
 }
 
-hipError_t launch_decode_split(const DecodeArgs& a, int d, hipStream_t s) {
+template <int D>
+static void launch_split_d(const DecodeArgs& a, int mode, int grid, hipStream_t s) {
+  if (mode == 1) hipLaunchKernelGGL((decode_split_bf16_kernel<D, 1>), dim3(grid), dim3(kWave), 0, s, a);
+  else if (mode == 2) hipLaunchKernelGGL((decode_split_bf16_kernel<D, 2>), dim3(grid), dim3(kWave), 0, s, a);
+  else hipLaunchKernelGGL((decode_split_bf16_kernel<D, 0>), dim3(grid), dim3(kWave), 0, s, a);
+}
+
+hipError_t launch_decode_split(const DecodeArgs& a, int d, int mode, hipStream_t s) {
   const int grid = a.full.n_items + a.ring.n_items;
-  if (d == 64) hipLaunchKernelGGL((decode_split_bf16_kernel<64>), dim3(grid), dim3(kWave), 0, s, a);
-  else hipLaunchKernelGGL((decode_split_bf16_kernel<128>), dim3(grid), dim3(kWave), 0, s, a);
+  if (d == 64) launch_split_d<64>(a, mode, grid, s);
+  else launch_split_d<128>(a, mode, grid, s);
   return hipGetLastError();
 }
 

@@ -1,0 +1,265 @@
+"""H2Share on the GPU (through the C interface) against the float64 oracle.
+
+* Head mapping: similarities within 1e-4 (Gram matrices of bf16 weights with
+  fp32 accumulation; everything after in fp64), mapping exact (cases are built
+  with separated maxima).
+* Anchor decode: the attention output is bit-identical to aoh_decode (same
+  kernels, the scores are only kept); the selected positions are checked
+  against the oracle's group-mean probabilities: equal to the oracle's set
+  where its k-th and (k+1)-th scores are further apart than the tolerance,
+  else every selected score must reach the oracle's k-th score (and every
+  unselected one must not exceed it) within the tolerance.  Format: ascending,
+  distinct, < lens, min(lens, k) entries then -1.
+* Reuse decode: borrowed lists drawn by a seeded generator, attention output
+  against the oracle (bf16 bar); the anchor -> reuse chain end to end against
+  the oracle's own chain where the selections coincide.
+"""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import h2share as HS
+from oracle import attention as OA
+from paper_2608_06849_amd import (PagedCache, RingCache, aoh_decode, aoh_decode_anchor, aoh_decode_reuse,
+                                  aoh_decode_workspace_bytes, aoh_head_mapping, aoh_kv_append)
+from tests.helpers import assert_parity, bits, f64
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+BF = torch.bfloat16
+SEL_RTOL = 1e-3   # relative tolerance on selection scores (fp32 scores of bf16 products vs fp64)
+SEL_ATOL = 1e-9
+
+
+def _bf(x):
+    return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(BF)
+
+
+# ------------------------------------------------------------------------- head mapping
+
+def _check_mapping(wq_a, wk_a, wq_r, wk_r, d, mask_a, mask_r, what):
+    t = [_bf(w) for w in (wq_a, wk_a, wq_r, wk_r)]
+    hs, gsim, mp = aoh_head_mapping(*[x.to(DEV) for x in t], d, mask_a, mask_r)
+    torch.cuda.synchronize()
+    w64 = [x.double().numpy() for x in t]
+    want_h = HS.head_similarity(*w64, d)
+    want_g = HS.group_similarity(want_h, len(mask_a))
+    want_m = HS.mapping_to_rank(HS.group_mapping(want_g, mask_a, mask_r), mask_a)
+    err = np.abs(hs.cpu().numpy() - want_h).max()
+    assert err < 1e-4, f"{what}: head similarity error {err:.2e}"
+    assert np.abs(gsim.cpu().numpy() - want_g).max() < 1e-4, what
+    assert mp.cpu().numpy().tolist() == want_m.tolist(), what
+    print(f"{what}: max similarity error {err:.2e}, mapping {want_m.tolist()}")
+    return want_m
+
+
+def test_mapping_permuted_copies():
+    d, gs, hkv, dm = 128, 2, 4, 512
+    r = np.random.default_rng(0)
+    wq = r.standard_normal((gs * hkv * d, dm)) * 0.05
+    wk = r.standard_normal((hkv * d, dm)) * 0.05
+    perm = [3, 1, 0, 2]
+    wq_r, wk_r = np.empty_like(wq), np.empty_like(wk)
+    for g2, g in enumerate(perm):
+        wk_r[g2 * d:(g2 + 1) * d] = r.uniform(0.5, 2) * wk[g * d:(g + 1) * d]
+        wq_r[g2 * gs * d:(g2 + 1) * gs * d] = r.uniform(0.5, 2) * wq[g * gs * d:(g + 1) * gs * d]
+    m = _check_mapping(wq, wk, wq_r, wk_r, d, [0, 0, 0, 0], [0, 0, 0, 0], "permuted copies")
+    assert m.tolist() == perm
+    # only the anchor's retrieval groups (0 and 3) are candidates: reuse group 0
+    # copies anchor group 3 (rank 1), group 2 copies anchor group 0 (rank 0);
+    # group 3 copies a streaming anchor group, so its choice is the oracle's
+    m = _check_mapping(wq, wk, wq_r, wk_r, d, [0, 1, 1, 0], [0, 1, 0, 0], "permuted copies, mixed labels")
+    assert m.tolist()[:3] == [1, -1, 0]
+
+
+@pytest.mark.parametrize("hq,hkv,d,dm,seed", [(8, 2, 64, 192, 1), (4, 4, 128, 256, 2)])
+def test_mapping_random(hq, hkv, d, dm, seed):
+    r = np.random.default_rng(seed)
+    w = [r.standard_normal((n * d, dm)) for n in (hq, hkv, hq, hkv)]
+    _check_mapping(*w, d, [0] * hkv, [0] * hkv, f"random {hq, hkv, d, dm}")
+
+
+def test_mapping_qwen_shaped_layers():
+    # two consecutive layers of the Qwen2.5-7B-shaped classifier workload
+    a = synth.projection_weights("qwen25_classify", 4)
+    b = synth.projection_weights("qwen25_classify", 5)
+    _check_mapping(a[0], a[1], b[0], b[1], 128, [0, 1, 0, 1], [1, 0, 0, 1], "qwen25 layers 4 -> 5")
+
+
+# ------------------------------------------------------------------------- decode
+
+def _decode_setup(B, L, hq, hkv, d, mask, n_sink, window, seed, k_boost=None):
+    """Seeded K/V for L positions of B sequences in a paged cache (shuffled pages)
+    and a ring, appended from position 0."""
+    kk = synth.gaussian((B, L, hkv, d), seed, "h2-k")
+    vv = synth.gaussian((B, L, hkv, d), seed, "h2-v")
+    if k_boost is not None:
+        k_boost(kk)
+    k, v = _bf(kk), _bf(vv)
+    n_ret, n_str = mask.count(0), mask.count(1)
+    max_pages = (L + 15) // 16
+    perm = synth.page_permutation(B * max_pages, seed, "h2-pages")
+    bt = torch.from_numpy(perm.reshape(B, max_pages).astype(np.int32))
+    full = PagedCache.allocate(B * max_pages, n_ret, d, BF, bt) if n_ret else None
+    ring = RingCache.allocate(B, n_str, n_sink, window, d, BF) if n_str else None
+    return k, v, full, ring
+
+
+def _fill(k, v, mask, lens, full, ring, n_sink, window):
+    # append each sequence's first lens[b] tokens (the ring must end at lens[b])
+    for b, n in enumerate(lens):
+        f = PagedCache(full.k, full.v, full.block_table[b:b + 1]) if full else None
+        rg = RingCache(ring.k[b:b + 1], ring.v[b:b + 1], ring.capacity) if ring else None
+        aoh_kv_append(k[b:b + 1, :n].to(DEV), v[b:b + 1, :n].to(DEV), mask, torch.zeros(1, dtype=torch.int32, device=DEV),
+                      f, rg, n_sink, window)
+
+
+def _check_selection(got, q, k, lens, mask, top_k, what):
+    """got [B, n_ret, top_k] (numpy) against the oracle's scores."""
+    k64 = f64(k)
+    q64 = f64(q)
+    ret = [g for g in range(len(mask)) if not mask[g]]
+    exact = 0
+    for b in range(len(lens)):
+        n = int(lens[b])
+        for r, g in enumerate(ret):
+            sel = got[b, r]
+            m = min(n, top_k)
+            assert np.all(sel[m:] == -1), f"{what}: padding"
+            s = sel[:m]
+            assert np.all(np.diff(s) > 0) and s[0] >= 0 and s[-1] < n, f"{what}: order/range"
+            sc = HS.group_scores(q64, k64, lens, b, g, len(mask))
+            if n <= top_k:
+                continue
+            srt = np.sort(sc)[::-1]
+            kth, nxt = srt[top_k - 1], srt[top_k]
+            tol = SEL_RTOL * kth + SEL_ATOL
+            if kth - nxt > 2 * tol:
+                assert s.tolist() == HS.top_k_positions(sc, top_k).tolist(), f"{what}: b{b} group {g}"
+                exact += 1
+            else:
+                unsel = np.setdiff1d(np.arange(n), s)
+                assert sc[s].min() >= kth - tol and sc[unsel].max() <= kth + tol, f"{what}: b{b} group {g}"
+    return exact
+
+
+@pytest.mark.parametrize("B,L,lens,hq,hkv,d,mask,top_k,seed", [
+    (2, 700, [700, 413], 8, 2, 128, [0, 1], 64, 1),
+    (1, 300, [300], 8, 4, 128, [0, 0, 1, 0], 300, 2),      # top_k = lens: everything
+    (2, 500, [37, 500], 4, 2, 64, [0, 0], 100, 3),          # lens < top_k for one sequence
+    (1, 2048, [2048], 28, 4, 128, [0, 1, 0, 1], 256, 4),    # Qwen-shaped heads
+])
+def test_anchor_decode(B, L, lens, hq, hkv, d, mask, top_k, seed):
+    n_sink, window = 4, 64
+    k, v, full, ring = _decode_setup(B, L, hq, hkv, d, mask, n_sink, window, seed)
+    _fill(k, v, mask, lens, full, ring, n_sink, window)
+    q = _bf(synth.gaussian((B, hq, d), seed, "h2-q"))
+    lens_t = torch.tensor(lens, dtype=torch.int32, device=DEV)
+    out_a, idx = aoh_decode_anchor(q.to(DEV), full, ring, mask, lens_t, n_sink, window, top_k)
+    ws = torch.empty(aoh_decode_workspace_bytes(B, hq, d, full.block_table.shape[1], n_sink + window) // 4 + 4,
+                     dtype=torch.float32, device=DEV)
+    out_d = aoh_decode(q.to(DEV), full, ring, mask, lens_t, n_sink, window, workspace=ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits(out_a), bits(out_d)), "anchor output differs from aoh_decode"
+    n_exact = _check_selection(idx.cpu().numpy(), q, k, lens, mask, top_k, f"anchor {B, L, hq, hkv, d, top_k}")
+    print(f"anchor {B, L, hq, hkv, d, top_k}: selections exact for {n_exact} separable lists")
+
+
+def test_anchor_exact_ties_go_to_lower_positions():
+    # K rows at positions 40, 90, 140, 190, 240 are identical and dominant: five
+    # exactly tied scores for a top-3 selection -> positions 40, 90, 140
+    B, L, hq, hkv, d = 1, 256, 4, 1, 128
+    def boost(kk):
+        row = kk[0, 7, 0] * 6.0
+        for p in (40, 90, 140, 190, 240):
+            kk[0, p, 0] = row
+    k, v, full, ring = _decode_setup(B, L, hq, hkv, d, [0], 4, 16, 5, k_boost=boost)
+    _fill(k, v, [0], [L], full, None, 4, 16)
+    # queries aligned with the planted row so that it dominates
+    q = _bf(np.repeat(k[0, 40, 0].float().numpy()[None, None], hq, axis=1) * 0.5)
+    _, idx = aoh_decode_anchor(q.to(DEV), full, None, [0], torch.tensor([L], dtype=torch.int32, device=DEV), 4, 16, 3)
+    torch.cuda.synchronize()
+    assert idx.cpu().numpy()[0, 0].tolist() == [40, 90, 140]
+
+
+def _lists(B, n_lists, lens, top_k, seed):
+    """Seeded borrowed lists: per (b, list) min(lens, top_k) distinct sorted positions, then -1."""
+    out = np.full((B, n_lists, top_k), -1, dtype=np.int32)
+    for b in range(B):
+        for r in range(n_lists):
+            n = int(lens[b])
+            m = min(n, top_k)
+            pick = synth.rng(seed, "h2-lists", b, r).choice(n, m, replace=False)
+            out[b, r, :m] = np.sort(pick)
+    return out
+
+
+@pytest.mark.parametrize("B,L,lens,hq,hkv,d,mask,mapping,n_lists,top_k,seed", [
+    (2, 900, [900, 611], 8, 2, 128, [0, 1], [1, -1], 2, 128, 6),
+    (1, 400, [400], 8, 4, 128, [0, 0, 1, 0], [2, 0, -1, 2], 3, 77, 7),   # ragged list length
+    (2, 300, [300, 20], 4, 2, 64, [0, 0], [0, 0], 1, 64, 8),             # lens < top_k
+    (1, 3000, [3000], 28, 4, 128, [0, 1, 0, 1], [1, -1, 0, -1], 2, 1024, 9),
+])
+def test_reuse_decode(B, L, lens, hq, hkv, d, mask, mapping, n_lists, top_k, seed):
+    n_sink, window = 8, 96
+    k, v, full, ring = _decode_setup(B, L, hq, hkv, d, mask, n_sink, window, seed)
+    _fill(k, v, mask, lens, full, ring, n_sink, window)
+    q = _bf(synth.gaussian((B, hq, d), seed, "h2-q"))
+    sel = _lists(B, n_lists, lens, top_k, seed)
+    lens_t = torch.tensor(lens, dtype=torch.int32, device=DEV)
+    out = aoh_decode_reuse(q.to(DEV), full, ring, mask, lens_t, n_sink, window,
+                           torch.from_numpy(sel).to(DEV), mapping)
+    torch.cuda.synchronize()
+    want = HS.reuse_decode(f64(q), f64(k), f64(v), lens, mask, n_sink, window, sel, mapping)
+    mx, mean = assert_parity(out, want, BF, f"reuse {B, L, hq, hkv, d, top_k}")
+    print(f"reuse {B, L, hq, hkv, d, top_k}: max abs {mx:.2e} mean {mean:.2e}")
+
+
+def test_reuse_every_position_matches_oracle_full_decode():
+    B, L, hq, hkv, d = 2, 640, 8, 2, 128
+    mask = [0, 0]
+    lens = [640, 333]
+    k, v, full, _ = _decode_setup(B, L, hq, hkv, d, mask, 4, 32, 10)
+    _fill(k, v, mask, lens, full, None, 4, 32)
+    q = _bf(synth.gaussian((B, hq, d), 10, "h2-q"))
+    sel = np.full((B, 1, L), -1, dtype=np.int32)
+    for b in range(B):
+        sel[b, 0, :lens[b]] = np.arange(lens[b])
+    out = aoh_decode_reuse(q.to(DEV), full, None, mask, torch.tensor(lens, dtype=torch.int32, device=DEV), 4, 32,
+                           torch.from_numpy(sel).to(DEV), [0, 0])
+    torch.cuda.synchronize()
+    assert_parity(out, OA.decode(f64(q), f64(k), f64(v), lens, mask, 4, 32), BF, "reuse over every position")
+
+
+def test_anchor_then_reuse_chain():
+    # Two layers of one block on the same sequences: the anchor's planted needles
+    # (48 per sequence and retrieval group) make its top-48 set clear-cut; the
+    # reuse layer (own K/V) borrows it through the mapping.
+    B, L, hq, hkv, d, top_k = 2, 4096, 8, 2, 128, 48
+    mask = [0, 0]
+    lens = [4096, 2500]
+    qa = synth.gaussian((B, hq, d), 11, "h2-qa")
+
+    def needles(kk):
+        for b in range(B):
+            for g in range(hkv):
+                pos = synth.rng(11, "h2-needles", b, g).choice(lens[b], top_k, replace=False)
+                direction = qa[b, g * (hq // hkv)] / np.linalg.norm(qa[b, g * (hq // hkv)])
+                kk[b, pos, g] = 3.0 * direction * np.sqrt(d)
+
+    ka, va, fa, _ = _decode_setup(B, L, hq, hkv, d, mask, 4, 32, 11, k_boost=needles)
+    kr, vr, fr, _ = _decode_setup(B, L, hq, hkv, d, mask, 4, 32, 12)
+    _fill(ka, va, mask, lens, fa, None, 4, 32)
+    _fill(kr, vr, mask, lens, fr, None, 4, 32)
+    qr = _bf(synth.gaussian((B, hq, d), 12, "h2-qr"))
+    q_a = _bf(qa)
+    lens_t = torch.tensor(lens, dtype=torch.int32, device=DEV)
+    _, idx = aoh_decode_anchor(q_a.to(DEV), fa, None, mask, lens_t, 4, 32, top_k)
+    mapping = [1, 0]
+    out = aoh_decode_reuse(qr.to(DEV), fr, None, mask, lens_t, 4, 32, idx, mapping)
+    torch.cuda.synchronize()
+    want_idx = HS.anchor_select(f64(q_a), f64(ka), lens, mask, top_k)
+    assert np.array_equal(idx.cpu().numpy(), want_idx), "anchor selection differs from the oracle's"
+    want = HS.reuse_decode(f64(qr), f64(kr), f64(vr), lens, mask, 4, 32, want_idx, mapping)
+    assert_parity(out, want, BF, "anchor -> reuse chain")
