@@ -388,6 +388,8 @@ def decode_leg(args, torch, synth, PagedCache, RingCache, aoh_decode, aoh_decode
     }
     log(f"decode {ms:.4f} ms/step, {gbps:.0f} GB/s ({res['frac_of_hbm_peak']:.3f} of peak); "
         f"decode call alone {dec_ms:.4f} ms")
+    res["h2share"] = h2share_decode(torch, q_steps[-1], full, ring, mask, lens_tab[steps], n_sink, window, B, Hq, D,
+                                    max_pages, L0 + steps, dec_ms)
     if full_all is not None:
         ms_all = run([0] * Hkv, full_all, None)
         res["all_retrieval_ms_per_step"] = round(ms_all, 4)
@@ -395,6 +397,61 @@ def decode_leg(args, torch, synth, PagedCache, RingCache, aoh_decode, aoh_decode
         res["resident_kv_gb_all_retrieval"] = round((full_all.k.numel() + full_all.v.numel()) * 2 / 1e9, 4)
         log(f"decode all-retrieval {ms_all:.4f} ms/step")
     return res
+
+
+def h2share_decode(torch, q, full, ring, mask, lens, n_sink, window, B, Hq, D, max_pages, length, plain_ms,
+                   top_k=2048, block=4):
+    """H2Share decode on the same caches: an anchor step (decode + top-k
+    selection) and a reuse step (retrieval groups attend to the anchor's
+    top_k positions in their own cache; identity group mapping), each timed
+    alone; a block of `block` layers costs one anchor and block-1 reuse steps."""
+    from paper_2608_06849_amd import (aoh_decode_anchor, aoh_decode_anchor_workspace_bytes, aoh_decode_reuse,
+                                      aoh_decode_reuse_workspace_bytes)
+    n_ret, n_str = mask.count(0), mask.count(1)
+    out = torch.empty_like(q)
+    idx = torch.empty((B, n_ret, top_k), dtype=torch.int32, device="cuda")
+    ws_a = torch.empty(aoh_decode_anchor_workspace_bytes(B, Hq, D, max_pages, n_sink + window), dtype=torch.uint8,
+                       device="cuda")
+    ws_r = torch.empty(aoh_decode_reuse_workspace_bytes(B, Hq, D, top_k, n_sink + window), dtype=torch.uint8,
+                       device="cuda")
+    mapping = [0] * len(mask)
+    r = 0
+    for g in range(len(mask)):
+        if not mask[g]:
+            mapping[g] = r
+            r += 1
+
+    def timed(fn, n=20):
+        for _ in range(3):
+            fn()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        ev[0].record()
+        for _ in range(n):
+            fn()
+        ev[1].record()
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]) / n
+
+    anchor_ms = timed(lambda: aoh_decode_anchor(q, full, ring, mask, lens, n_sink, window, top_k, indices=idx,
+                                                out=out, workspace=ws_a))
+    reuse_ms = timed(lambda: aoh_decode_reuse(q, full, ring, mask, lens, n_sink, window, idx, mapping, out=out,
+                                              workspace=ws_r))
+    gs = Hq // len(mask)
+    reuse_bytes = B * (n_ret * top_k + n_str * min(length, n_sink + window)) * D * 2 * 2
+    per_layer = (anchor_ms + (block - 1) * reuse_ms) / block
+    log(f"H2Share: anchor {anchor_ms:.4f} ms, reuse {reuse_ms:.4f} ms (top-{top_k}); block of {block}: "
+        f"{per_layer:.4f} ms/layer vs {plain_ms:.4f} plain")
+    return {
+        "top_k": top_k, "block": block,
+        "anchor_ms": round(anchor_ms, 4), "reuse_ms": round(reuse_ms, 4), "plain_ms": round(plain_ms, 4),
+        "anchor_overhead": round(anchor_ms / plain_ms, 3),
+        "ms_per_layer_in_block": round(per_layer, 4),
+        "speedup_per_layer_vs_plain": round(plain_ms / per_layer, 3),
+        "reuse_useful_gb": round(reuse_bytes / 1e9, 5),
+        "reuse_useful_gbps": round(reuse_bytes / (reuse_ms * 1e-3) / 1e9, 1),
+        "group_size": gs,
+    }
 
 
 def stack_decode_leg(args, torch, synth, PagedCache, RingCache, aoh_decode, aoh_decode_workspace_bytes,

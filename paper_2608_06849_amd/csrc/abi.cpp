@@ -363,10 +363,23 @@ size_t aoh_decode_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t d_he
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Anchor extras: scores [B][Hq][16 * max_pages] and final (m, l) [B][Hq][2].
+// Anchor extras: scores [B][Hq][16 * max_pages], final (m, l) [B][Hq][2], and
+// the top-k partial histograms and counts per (sequence, KV head) list (sized
+// with Hq lists per sequence, a bound on the retrieval KV heads).
+static size_t anchor_scores_bytes(int64_t B, int64_t Hq, int64_t max_pages) {
+  return align256((size_t)(B * Hq * max_pages * kPageTokens) * sizeof(float));
+}
+static size_t anchor_ml_bytes(int64_t B, int64_t Hq) { return align256((size_t)(B * Hq * 2) * sizeof(float)); }
+static size_t anchor_part_bytes(int64_t B, int64_t Hq) {
+  return align256((size_t)(B * Hq * 3 * kTopkParts * 2048) * sizeof(uint32_t));
+}
+static size_t anchor_counts_bytes(int64_t B, int64_t Hq) {
+  return align256((size_t)(B * Hq * kTopkParts * 2) * sizeof(uint32_t));
+}
+static constexpr size_t kScoreDummyBytes = 64 * 8 * sizeof(float);
 static size_t anchor_extra(int64_t B, int64_t Hq, int64_t max_pages) {
-  return align256((size_t)(B * Hq * max_pages * kPageTokens) * sizeof(float)) +
-         align256((size_t)(B * Hq * 2) * sizeof(float));
+  return anchor_scores_bytes(B, Hq, max_pages) + anchor_ml_bytes(B, Hq) + anchor_part_bytes(B, Hq) +
+         anchor_counts_bytes(B, Hq) + kScoreDummyBytes;
 }
 
 // H2Share roles of a decode call (Sec. "AoH-Guided Sparse Attention"): plain,
@@ -483,10 +496,19 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
   a.part_acc = part_acc; a.part_ml = part_ml; a.max_splits = sp_bound.max_splits;
   float* scores = nullptr;
   float* ml = nullptr;
+  uint32_t* part = nullptr;
+  uint32_t* counts = nullptr;
   if (x.mode == kAnchor) {
     char* w = reinterpret_cast<char*>(workspace) + align256(base_need);
     scores = reinterpret_cast<float*>(w);
-    ml = reinterpret_cast<float*>(w + align256((size_t)(B * Hq * max_pages * kPageTokens) * sizeof(float)));
+    w += anchor_scores_bytes(B, Hq, max_pages);
+    ml = reinterpret_cast<float*>(w);
+    w += anchor_ml_bytes(B, Hq);
+    part = reinterpret_cast<uint32_t*>(w);
+    w += anchor_part_bytes(B, Hq);
+    counts = reinterpret_cast<uint32_t*>(w);
+    w += anchor_counts_bytes(B, Hq);
+    a.score_dummy = reinterpret_cast<float*>(w);
     a.scores = scores;
     a.score_len = max_pages * kPageTokens;
   }
@@ -523,6 +545,7 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
     t.B = (int)B; t.Hq = (int)Hq; t.gs = gs; t.n_kv = hs.n_ret;
     t.score_len = max_pages * kPageTokens;
     t.n_sel = x.top_k;
+    t.part = part; t.counts = counts;
     std::memcpy(t.kv_heads, hs.ret, hs.n_ret);
     if (B > 65535) return fail(AOH_ERR_UNSUPPORTED, "batch too large");
     e = launch_topk(t, s);

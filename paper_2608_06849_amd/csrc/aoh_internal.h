@@ -76,6 +76,7 @@ struct DecodeArgs {
   // Anchor layer (H2Share): scaled scores of the paged-cache heads,
   // [B][Hq][score_len] in log2 units, for positions < lens.
   float* scores;
+  float* score_dummy;           // 64 x 8 floats written by lanes without a query head
   int32_t score_len;
   // Reuse layer (H2Share): paged-cache items attend to borrowed positions
   // sel[b][sel_rank[j]][0..n_sel) (ascending, -1 = none) of KV head j of the
@@ -166,8 +167,11 @@ struct TopkArgs {
   int32_t B, Hq, gs, n_kv;
   int32_t score_len;            // positions per row (16 * pages per sequence)
   int32_t n_sel;
+  uint32_t* part;               // [B][n_kv][3][kTopkParts][2048] partial histograms
+  uint32_t* counts;             // [B][n_kv][kTopkParts][2]  (above, equal to the threshold)
   uint8_t kv_heads[kMaxKvHeads];
 };
+constexpr int kTopkParts = 8;   // workgroups per (sequence, KV head) list
 hipError_t launch_topk(const TopkArgs& a, hipStream_t s);
 
 // Cross-layer head similarity (H2Share): grams of both layers are in gram

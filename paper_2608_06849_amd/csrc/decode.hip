@@ -63,17 +63,26 @@ __device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const Cac
 
   const uint16_t* kc = reinterpret_cast<const uint16_t*>(cv.k);
   const uint16_t* vc = reinterpret_cast<const uint16_t*>(cv.v);
-  auto block_base = [&](int blk, int64_t& kb, int64_t& vb) {
-    int64_t unit;
+  // Cache unit of a block: ring block, or the page of the block table (an
+  // invalid entry reads page 0, never outside the cache).
+  auto unit_of = [&](int entry) -> int64_t {
+    if (RING) return ((int64_t)b * cv.n_kv + rank) * cv.ring_blocks + entry;
+    const int page = (entry < 0 || entry >= cv.num_pages) ? 0 : entry;
+    return (int64_t)page * cv.n_kv + rank;
+  };
+  // Block-table entries of the two blocks of chunk c (block ids for the ring);
+  // they are fetched one chunk ahead of their use, so waiting for them never
+  // waits for anything issued later (the score stores of the anchor layer).
+  auto fetch_entries = [&](int c, int (&e)[2]) {
+    const int c1 = min(c + 1, blk_end - 1);  // a chunk's second block may not exist
     if (RING) {
-      unit = ((int64_t)b * cv.n_kv + rank) * cv.ring_blocks + blk;
+      e[0] = c;
+      e[1] = c1;
     } else {
-      int page = cv.block_table[(int64_t)b * cv.max_pages + blk];
-      page = (page < 0 || page >= cv.num_pages) ? 0 : page;  // invalid entry: read page 0, never outside
-      unit = (int64_t)page * cv.n_kv + rank;
+      const int32_t* bt = cv.block_table + (int64_t)b * cv.max_pages;
+      e[0] = bt[c];
+      e[1] = bt[c1];  // two independent loads: nothing waits for the first
     }
-    kb = unit * (kPage * D);
-    vb = unit * (kPage * D);
   };
 
   // K row of MFMA row m = lane & 15 for token block X: chunk token
@@ -87,17 +96,9 @@ __device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const Cac
 
   u32x4 kreg[2][kKSteps];
   u32x4 vreg[kDimBlocks];
-  auto load_chunk = [&](int c) {
-    int64_t kbA, vbA, kbB, vbB;
-    block_base(c, kbA, vbA);
-    if (c + 1 < blk_end) {
-      block_base(c + 1, kbB, vbB);
-    } else {
-      kbB = kbA;
-      vbB = vbA;
-    }
-    const int64_t kb = k_half ? kbB : kbA;
-    const int64_t vb = v_half ? vbB : vbA;
+  auto load_chunk = [&](const int (&e)[2]) {
+    const int64_t kb = unit_of(e[k_half]) * (kPage * D);
+    const int64_t vb = unit_of(e[v_half]) * (kPage * D);
 #pragma unroll
     for (int X = 0; X < 2; ++X)
 #pragma unroll
@@ -114,7 +115,10 @@ __device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const Cac
   float m_run = -INFINITY;
   float l_run = 0.f;
 
-  load_chunk(blk0);
+  int ent[2];
+  fetch_entries(blk0, ent);
+  load_chunk(ent);
+  if (blk0 + 2 < blk_end) fetch_entries(blk0 + 2, ent);
   for (int c = blk0; c < blk_end; c += 2) {
     u32x4 kcur[2][kKSteps];
     u32x4 vcur[kDimBlocks];
@@ -124,7 +128,10 @@ __device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const Cac
       for (int s = 0; s < kKSteps; ++s) kcur[X][s] = kreg[X][s];
 #pragma unroll
     for (int nb = 0; nb < kDimBlocks; ++nb) vcur[nb] = vreg[nb];
-    if (c + 2 < blk_end) load_chunk(c + 2);
+    if (c + 2 < blk_end) {
+      load_chunk(ent);                                // chunk c + 2
+      if (c + 4 < blk_end) fetch_entries(c + 4, ent);  // entries of chunk c + 4
+    }
 
     // S^T for the two 16-token blocks.
     f32x4 sc[2];
@@ -148,17 +155,16 @@ __device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const Cac
         x[4 * X + i] = v;
         mx = fmaxf(mx, v);
       }
-    if (SCORES && head_ok) {
-      // anchor layer: keep the scaled scores for the top-k selection
-      float* sp = a.scores + ((int64_t)b * a.Hq + hq) * a.score_len + tok0;
-      if (!partial) {
-        *reinterpret_cast<f32x4*>(sp) = f32x4{x[0], x[1], x[2], x[3]};
-        *reinterpret_cast<f32x4*>(sp + 4) = f32x4{x[4], x[5], x[6], x[7]};
-      } else {
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-          if (tok0 + j < tok_end) sp[j] = x[j];
-      }
+    if (SCORES) {
+      // Anchor layer: keep the scaled scores for the top-k selection.  Every
+      // lane issues the same two stores in every chunk (a fixed count, so the
+      // compiler's wait for the prefetched chunk stays exact): lanes without a
+      // query head write to a dummy area, and masked positions (beyond the
+      // valid length, never read by the selection) get -inf.
+      float* sp = head_ok ? a.scores + ((int64_t)b * a.Hq + hq) * a.score_len + tok0
+                          : a.score_dummy + 8 * lane;
+      *reinterpret_cast<f32x4*>(sp) = f32x4{x[0], x[1], x[2], x[3]};
+      *reinterpret_cast<f32x4*>(sp + 4) = f32x4{x[4], x[5], x[6], x[7]};
     }
     mx = wave_xor_max(mx, 16);
     mx = wave_xor_max(mx, 32);

@@ -3,13 +3,15 @@
 // token indices from their attention scores; GQA appendix: a group's query
 // heads share one index set).
 //
-// One workgroup of 1024 threads per (sequence, retrieval KV head).  The score
+// Each (sequence, retrieval KV head) list is cut into kTopkParts segments, one
+// workgroup of 1024 threads each, over five launches that exchange partial
+// histograms and counts through the workspace (no atomics in memory).  The score
 // of position j is the sum over the group's query heads of their attention
 // probability exp2(s_hj - m_h) / l_h (the mean up to the constant 1/gs, so the
 // same ranking), from the scaled scores the split pass kept and the final
 // (m, l) of the merge.  Probabilities are non-negative, so their fp32 bit
 // patterns order like the values; the k-th largest bit pattern is found by a
-// three-digit (11 + 11 + 10 bits) radix select over histograms in LDS, and the
+// three-digit (11 + 11 + 10 bits) radix select over per-segment histograms, and the
 // positions are then compacted in ascending order: every key above the
 // threshold, and as many keys equal to it as still needed, lowest positions
 // first.  Sequences with at most k positions select all of them; unused
@@ -47,102 +49,259 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* wsum, 
   return before + x - v;
 }
 
-__global__ __launch_bounds__(kTopkThreads) void topk_kernel(TopkArgs a) {
-  __shared__ uint32_t hist[2048];
-  __shared__ uint32_t wsum[kTopkWaves];
-  __shared__ uint32_t s_bin, s_above;
-  __shared__ float s_m[kMaxKvHeads], s_il[kMaxKvHeads];
-  const int kvl = blockIdx.x, b = blockIdx.y;
-  const int g = a.kv_heads[kvl];
-  const int t = threadIdx.x;
-  const int n = max(0, min(a.lens[b], a.score_len));
-  const int k = a.n_sel;
-  int32_t* out = a.sel + ((int64_t)b * a.n_kv + kvl) * k;
-  if (n <= k) {
-    for (int j = t; j < k; j += kTopkThreads) out[j] = j < n ? j : -1;
-    return;
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
+  const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const uint32_t y = __shfl_up(x, o, kWave);
+    if (lane >= o) x += y;
   }
-  const int64_t row_stride = a.score_len;
-  float* row0 = a.scores + ((int64_t)b * a.Hq + (int64_t)g * a.gs) * row_stride;
-  uint32_t* keys = reinterpret_cast<uint32_t*>(row0);  // written over the first head's row
-  if (t < a.gs) {
+  return x;
+}
+
+constexpr int kHistCopies = 4;  // lanes spread their increments over 4 copies (hot bins)
+constexpr int kTile = 4 * kTopkThreads;  // positions per compaction tile
+
+struct ListView {
+  int n;                 // positions of the list (lens clamped to the score row)
+  int seg0, seg1;        // this workgroup's segment [seg0, seg1)
+  uint32_t* keys;        // key row (the group's first score row)
+  const uint32_t* part;  // partial histograms of the list [3][kTopkParts][2048]
+  uint32_t* my_part;     // this workgroup's [3][...] slot base
+  uint32_t* counts;      // [kTopkParts][2]
+  int32_t* out;
+};
+
+__device__ __forceinline__ ListView list_view(const TopkArgs& a) {
+  ListView v;
+  const int p = blockIdx.x, kvl = blockIdx.y, b = blockIdx.z;
+  const int g = a.kv_heads[kvl];
+  v.n = max(0, min(a.lens[b], a.score_len));
+  // segments are whole compaction tiles
+  const int per = (v.n + kTopkParts - 1) / kTopkParts;
+  const int seg = ((per + kTile - 1) / kTile) * kTile;
+  v.seg0 = min(v.n, p * seg);
+  v.seg1 = min(v.n, v.seg0 + seg);
+  v.keys = reinterpret_cast<uint32_t*>(a.scores + ((int64_t)b * a.Hq + (int64_t)g * a.gs) * a.score_len);
+  const int64_t list = (int64_t)b * a.n_kv + kvl;
+  v.part = a.part + list * 3 * kTopkParts * 2048;
+  v.my_part = a.part + list * 3 * kTopkParts * 2048 + (int64_t)p * 2048;
+  v.counts = a.counts + list * kTopkParts * 2;
+  v.out = a.sel + list * a.n_sel;
+  return v;
+}
+
+// The digit of the k-th largest key among those matching the earlier digits:
+// sum the partial histograms of `pass` over the parts, then scan from the top.
+__device__ __forceinline__ void find_digit(const uint32_t* part, int pass, int nb, uint32_t& kk, uint32_t& bin,
+                                           uint32_t* wsum, uint32_t* s_bin) {
+  const int t = threadIdx.x;
+  const int b_hi = nb - 1 - 2 * t, b_lo = nb - 2 - 2 * t;
+  uint32_t h_hi = 0, h_lo = 0;
+  for (int q = 0; q < kTopkParts; ++q) {
+    const uint32_t* h = part + ((int64_t)pass * kTopkParts + q) * 2048;
+    if (b_hi >= 0) h_hi += h[b_hi];
+    if (b_lo >= 0) h_lo += h[b_lo];
+  }
+  uint32_t total;
+  const uint32_t above = block_excl_scan(h_hi + h_lo, wsum, total);
+  if (above < kk && kk <= above + h_hi) {
+    s_bin[0] = (uint32_t)b_hi;
+    s_bin[1] = above;
+  } else if (above + h_hi < kk && kk <= above + h_hi + h_lo) {
+    s_bin[0] = (uint32_t)b_lo;
+    s_bin[1] = above + h_hi;
+  }
+  __syncthreads();
+  bin = s_bin[0];
+  kk -= s_bin[1];
+  __syncthreads();
+}
+
+constexpr int kShift[3] = {21, 10, 0};
+constexpr int kBins[3] = {2048, 2048, 1024};
+
+// Threshold key (the k-th largest) and the number of keys equal to it to take,
+// from the three histograms.
+__device__ __forceinline__ void threshold(const ListView& v, int k, uint32_t& thr, uint32_t& need_eq,
+                                          uint32_t* wsum, uint32_t* s_bin) {
+  uint32_t kk = (uint32_t)k, prefix = 0, bin;
+#pragma unroll
+  for (int pass = 0; pass < 3; ++pass) {
+    find_digit(v.part, pass, kBins[pass], kk, bin, wsum, s_bin);
+    prefix |= bin << kShift[pass];
+  }
+  thr = prefix;
+  need_eq = kk;
+}
+
+// Pass PASS: keys (PASS 0 only) and the histogram of digit PASS of this
+// workgroup's segment, among keys matching the digits already found.
+template <int PASS>
+__global__ __launch_bounds__(kTopkThreads) void topk_hist_kernel(TopkArgs a) {
+  __shared__ uint32_t hist[kHistCopies][2048];
+  __shared__ uint32_t wsum[kTopkWaves];
+  __shared__ uint32_t s_bin[2];
+  __shared__ float s_m[16], s_il[16];
+  const ListView v = list_view(a);
+  if (v.n <= a.n_sel) return;  // everything is selected: nothing to rank
+  const int t = threadIdx.x;
+  const int b = blockIdx.z, g = a.kv_heads[blockIdx.y];
+  uint32_t prefix = 0, pmask = 0;
+  if (PASS > 0) {
+    uint32_t kk = (uint32_t)a.n_sel, bin;
+#pragma unroll
+    for (int q = 0; q < PASS; ++q) {
+      find_digit(v.part, q, kBins[q], kk, bin, wsum, s_bin);
+      prefix |= bin << kShift[q];
+      pmask |= (uint32_t)(kBins[q] - 1) << kShift[q];
+    }
+  }
+  for (int i = t; i < kHistCopies * 2048; i += kTopkThreads) (&hist[0][0])[i] = 0;
+  if (PASS == 0 && t < a.gs) {
     const float* ml = a.ml + ((int64_t)b * a.Hq + g * a.gs + t) * 2;
     s_m[t] = ml[0];
     s_il[t] = 1.f / ml[1];
   }
   __syncthreads();
-  for (int j = t; j < n; j += kTopkThreads) {
-    float p = 0.f;
-    for (int h = 0; h < a.gs; ++h) p += fast_exp2(row0[h * row_stride + j] - s_m[h]) * s_il[h];
-    keys[j] = __builtin_bit_cast(uint32_t, p);
+  uint32_t* my_hist = hist[t & (kHistCopies - 1)];
+  const int64_t row = a.score_len;
+  for (int j = v.seg0 + t; j < v.seg1; j += kTopkThreads) {
+    uint32_t key;
+    if (PASS == 0) {
+      const float* s0 = reinterpret_cast<const float*>(v.keys);
+      float p = 0.f;
+      for (int h = 0; h < a.gs; ++h) p += fast_exp2(s0[h * row + j] - s_m[h]) * s_il[h];
+      key = __builtin_bit_cast(uint32_t, p);
+      v.keys[j] = key;
+    } else {
+      key = v.keys[j];
+    }
+    if ((key & pmask) == prefix) atomicAdd(&my_hist[(key >> kShift[PASS]) & (kBins[PASS] - 1)], 1u);
   }
   __syncthreads();
-
-  // radix select of the k-th largest key
-  uint32_t prefix = 0, pmask = 0;
-  uint32_t kk = (uint32_t)k;  // rank (from the top, 1-based) still to find among keys matching prefix
-#pragma unroll 1
-  for (int pass = 0; pass < 3; ++pass) {
-    const int shift = pass == 0 ? 21 : (pass == 1 ? 10 : 0);
-    const int nb = pass == 2 ? 1024 : 2048;
-    for (int i = t; i < 2048; i += kTopkThreads) hist[i] = 0;
-    __syncthreads();
-    for (int j = t; j < n; j += kTopkThreads) {
-      const uint32_t key = keys[j];
-      if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & (nb - 1)], 1u);
-    }
-    __syncthreads();
-    // thread t owns the bins of descending rank 2t, 2t+1
-    const int b_hi = nb - 1 - 2 * t, b_lo = nb - 2 - 2 * t;
-    const uint32_t h_hi = b_hi >= 0 ? hist[b_hi] : 0u;
-    const uint32_t h_lo = b_lo >= 0 ? hist[b_lo] : 0u;
-    uint32_t total;
-    const uint32_t above = block_excl_scan(h_hi + h_lo, wsum, total);
-    if (above < kk && kk <= above + h_hi) {
-      s_bin = (uint32_t)b_hi;
-      s_above = above;
-    } else if (above + h_hi < kk && kk <= above + h_hi + h_lo) {
-      s_bin = (uint32_t)b_lo;
-      s_above = above + h_hi;
-    }
-    __syncthreads();
-    prefix |= s_bin << shift;
-    pmask |= (uint32_t)(nb - 1) << shift;
-    kk -= s_above;
-    __syncthreads();  // s_bin / s_above are rewritten by the next pass
+  uint32_t* dst = v.my_part + (int64_t)PASS * kTopkParts * 2048;
+  for (int i = t; i < 2048; i += kTopkThreads) {
+    uint32_t c = 0;
+#pragma unroll
+    for (int q = 0; q < kHistCopies; ++q) c += hist[q][i];
+    dst[i] = c;
   }
-  const uint32_t thr = prefix;
-  const uint32_t need_eq = kk;  // keys equal to thr still to take
+}
 
-  // ascending compaction: each thread owns a contiguous segment of positions
-  const int seg = (n + kTopkThreads - 1) / kTopkThreads;
-  const int j0 = min(n, t * seg), j1 = min(n, j0 + seg);
+// Counts of keys above and equal to the threshold in this workgroup's segment.
+__global__ __launch_bounds__(kTopkThreads) void topk_count_kernel(TopkArgs a) {
+  __shared__ uint32_t wsum[kTopkWaves];
+  __shared__ uint32_t s_bin[2];
+  const ListView v = list_view(a);
+  if (v.n <= a.n_sel) return;
+  uint32_t thr, need_eq;
+  threshold(v, a.n_sel, thr, need_eq, wsum, s_bin);
   uint32_t gt = 0, eq = 0;
-  for (int j = j0; j < j1; ++j) {
-    const uint32_t key = keys[j];
+  for (int j = v.seg0 + (int)threadIdx.x; j < v.seg1; j += kTopkThreads) {
+    const uint32_t key = v.keys[j];
     gt += key > thr;
     eq += key == thr;
   }
   uint32_t tot_gt, tot_eq;
-  const uint32_t gt_before = block_excl_scan(gt, wsum, tot_gt);
-  const uint32_t eq_before = block_excl_scan(eq, wsum, tot_eq);
-  uint32_t pos = gt_before + min(eq_before, need_eq);
-  uint32_t eq_seen = eq_before;
-  for (int j = j0; j < j1; ++j) {
-    const uint32_t key = keys[j];
-    if (key > thr) {
-      out[pos++] = j;
-    } else if (key == thr) {
-      if (eq_seen < need_eq) out[pos++] = j;
-      ++eq_seen;
+  block_excl_scan(gt, wsum, tot_gt);
+  block_excl_scan(eq, wsum, tot_eq);
+  if (threadIdx.x == 0) {
+    v.counts[blockIdx.x * 2 + 0] = tot_gt;
+    v.counts[blockIdx.x * 2 + 1] = tot_eq;
+  }
+}
+
+// Ascending compaction of this workgroup's segment into the list: tiles of
+// 4 x 1024 consecutive positions (4 per thread, coalesced); tied keys are
+// ranked from the counts of the earlier segments and wave scans.
+__global__ __launch_bounds__(kTopkThreads) void topk_compact_kernel(TopkArgs a) {
+  __shared__ uint32_t wsum[kTopkWaves];
+  __shared__ uint32_t s_bin[2];
+  __shared__ uint32_t s_weq[kTopkWaves], s_wsel[kTopkWaves];
+  const ListView v = list_view(a);
+  const int t = threadIdx.x;
+  const int k = a.n_sel;
+  if (v.n <= k) {
+    if (blockIdx.x == 0)
+      for (int j = t; j < k; j += kTopkThreads) v.out[j] = j < v.n ? j : -1;
+    return;
+  }
+  uint32_t thr, need_eq;
+  threshold(v, k, thr, need_eq, wsum, s_bin);
+  uint32_t gt_before = 0, eq_before0 = 0;
+  for (int q = 0; q < (int)blockIdx.x; ++q) {
+    gt_before += v.counts[q * 2 + 0];
+    eq_before0 += v.counts[q * 2 + 1];
+  }
+  const int lane = t & (kWave - 1), wave = t / kWave;
+  uint32_t carry_eq = eq_before0;
+  uint32_t carry_sel = gt_before + min(eq_before0, need_eq);
+  const uint32_t* keys = v.keys;
+  for (int base = v.seg0; base < v.seg1; base += kTile) {
+    const int j0 = base + 4 * t;
+    uint32_t kv[4];
+    if (j0 + 4 <= v.seg1) {
+      const u32x4 w = *reinterpret_cast<const u32x4*>(keys + j0);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) kv[i] = w[i];
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) kv[i] = j0 + i < v.seg1 ? keys[j0 + i] : 0u;
     }
+    uint32_t n_eq = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) n_eq += (j0 + i < v.seg1 && kv[i] == thr);
+    const uint32_t eq_incl = wave_incl_scan(n_eq);
+    if (lane == kWave - 1) s_weq[wave] = eq_incl;
+    __syncthreads();
+    uint32_t eq_rank = carry_eq, eq_tile = 0;
+#pragma unroll
+    for (int w = 0; w < kTopkWaves; ++w) {
+      if (w < wave) eq_rank += s_weq[w];
+      eq_tile += s_weq[w];
+    }
+    eq_rank += eq_incl - n_eq;
+    bool sel[4];
+    uint32_t n_sel = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const bool valid = j0 + i < v.seg1;
+      const bool gt = valid && kv[i] > thr;
+      const bool eqk = valid && kv[i] == thr;
+      sel[i] = gt || (eqk && eq_rank < need_eq);
+      eq_rank += eqk;
+      n_sel += sel[i];
+    }
+    const uint32_t sel_incl = wave_incl_scan(n_sel);
+    if (lane == kWave - 1) s_wsel[wave] = sel_incl;
+    __syncthreads();
+    uint32_t pos = carry_sel, sel_tile = 0;
+#pragma unroll
+    for (int w = 0; w < kTopkWaves; ++w) {
+      if (w < wave) pos += s_wsel[w];
+      sel_tile += s_wsel[w];
+    }
+    pos += sel_incl - n_sel;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (sel[i]) v.out[pos++] = j0 + i;
+    carry_sel += sel_tile;
+    carry_eq += eq_tile;
+    __syncthreads();  // s_weq / s_wsel are rewritten by the next tile
   }
 }
 
 }  // namespace
 
 hipError_t launch_topk(const TopkArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(topk_kernel, dim3(a.n_kv, a.B), dim3(kTopkThreads), 0, s, a);
+  const dim3 grid(kTopkParts, a.n_kv, a.B);
+  hipLaunchKernelGGL(topk_hist_kernel<0>, grid, dim3(kTopkThreads), 0, s, a);
+  hipLaunchKernelGGL(topk_hist_kernel<1>, grid, dim3(kTopkThreads), 0, s, a);
+  hipLaunchKernelGGL(topk_hist_kernel<2>, grid, dim3(kTopkThreads), 0, s, a);
+  hipLaunchKernelGGL(topk_count_kernel, grid, dim3(kTopkThreads), 0, s, a);
+  hipLaunchKernelGGL(topk_compact_kernel, grid, dim3(kTopkThreads), 0, s, a);
   return hipGetLastError();
 }
 
