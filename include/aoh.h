@@ -167,6 +167,27 @@ aoh_status aoh_prefill_append(const aoh_tensor* q, const aoh_tensor* k, const ao
                               aoh_tensor* out, void* stream);
 
 /*
+ * Prefill of a batch of prompts of different lengths packed along the token
+ * axis (no padding): sequence b is rows cu_seqlens[b] .. cu_seqlens[b+1]-1 of
+ *   q: [total][Hq][D]   k, v: [total][Hkv][D]   out: [total][Hq][D]
+ * and attends only within itself (positions restart at 0).  Each sequence's
+ * rows are computed exactly as by aoh_prefill (chunk = 0) or
+ * aoh_prefill_chunked (chunk >= 1) on that sequence alone.
+ *   cu_seqlens: DEVICE int32 [batch + 1], non-decreasing, cu_seqlens[0] = 0,
+ *     cu_seqlens[batch] <= total (entries are clamped into [0, total]).
+ *   max_seqlen: HOST bound on every sequence length; it sizes the grid (rows
+ *     past it are not computed), so the call reads nothing back from the device.
+ * With kv_full or kv_ring given, the prompts' K/V are also written to the
+ * caches as aoh_prefill_append does (sequence b into block-table row b / ring
+ * row b, positions 0..len_b-1; bf16 only).  Errors as aoh_prefill.
+ */
+aoh_status aoh_prefill_varlen(const aoh_tensor* q, const aoh_tensor* k, const aoh_tensor* v,
+                              const int32_t* cu_seqlens, int32_t batch, int32_t max_seqlen,
+                              const uint8_t* head_is_streaming, int32_t n_sink, int32_t window, int32_t chunk,
+                              const aoh_paged_cache* kv_full, const aoh_ring_cache* kv_ring, aoh_tensor* out,
+                              void* stream);
+
+/*
  * Append n_new tokens per sequence to the caches (Sec. 5: retrieval heads
  * retain every token; streaming heads evict all but the sink and recent
  * tokens).  Token t of k_new/v_new has position start_pos[b] + t.

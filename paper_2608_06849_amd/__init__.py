@@ -7,4 +7,4 @@ from .aoh import (AohError, PagedCache, RingCache, aoh_classify, aoh_classify_wo
                   aoh_decode, aoh_decode_anchor, aoh_decode_anchor_workspace_bytes, aoh_decode_reuse,
                   aoh_decode_reuse_workspace_bytes, aoh_decode_workspace_bytes, aoh_head_mapping,
                   aoh_head_mapping_workspace_bytes, aoh_kv_append, aoh_last_error, aoh_prefill,
-                  aoh_prefill_append, aoh_prefill_chunked, aoh_retrieval_group_count, aoh_version, lib)
+                  aoh_prefill_append, aoh_prefill_chunked, aoh_prefill_varlen, aoh_retrieval_group_count, aoh_version, lib)

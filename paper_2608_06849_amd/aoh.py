@@ -48,7 +48,7 @@ class AohRingCache(ctypes.Structure):
 
 _lib = None
 
-EXPORTS = ("aoh_prefill", "aoh_prefill_chunked", "aoh_prefill_append", "aoh_kv_append", "aoh_decode_workspace_bytes", "aoh_decode",
+EXPORTS = ("aoh_prefill", "aoh_prefill_chunked", "aoh_prefill_append", "aoh_prefill_varlen", "aoh_kv_append", "aoh_decode_workspace_bytes", "aoh_decode",
            "aoh_classify_workspace_bytes", "aoh_classify", "aoh_retrieval_group_count",
            "aoh_head_mapping_workspace_bytes", "aoh_head_mapping", "aoh_decode_anchor_workspace_bytes",
            "aoh_decode_anchor", "aoh_decode_reuse_workspace_bytes", "aoh_decode_reuse",
@@ -74,6 +74,11 @@ def lib():
                                          ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, P(AohPagedCache),
                                          P(AohRingCache), P(AohTensor), ctypes.c_void_p]
         L.aoh_prefill_append.restype = ctypes.c_int
+        L.aoh_prefill_varlen.argtypes = [P(AohTensor), P(AohTensor), P(AohTensor), ctypes.c_void_p, ctypes.c_int32,
+                                         ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                         ctypes.c_int32, P(AohPagedCache), P(AohRingCache), P(AohTensor),
+                                         ctypes.c_void_p]
+        L.aoh_prefill_varlen.restype = ctypes.c_int
         L.aoh_kv_append.argtypes = [P(AohTensor), P(AohTensor), ctypes.c_void_p, ctypes.c_void_p,
                                     P(AohPagedCache), P(AohRingCache), ctypes.c_int32, ctypes.c_int32,
                                     ctypes.c_void_p]
@@ -246,6 +251,22 @@ def aoh_prefill_append(q, k, v, head_is_streaming, n_sink, window, kv_full, kv_r
     m = _Mask(head_is_streaming)
     _check(lib().aoh_prefill_append(ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), m.ptr, n_sink, window,
                                     chunk, ctypes.byref(fd) if fd else None, ctypes.byref(rd) if rd else None,
+                                    ctypes.byref(od), _stream(stream)))
+    return out
+
+
+def aoh_prefill_varlen(q, k, v, cu_seqlens, max_seqlen, head_is_streaming, n_sink, window, chunk=0, kv_full=None,
+                       kv_ring=None, out=None, stream=None):
+    """Packed variable-length prefill: q [total, Hq, D], k/v [total, Hkv, D], cu_seqlens device int32 [B + 1]."""
+    if out is None:
+        out = torch.empty_like(q)
+    qd, kd, vd, od = tensor_desc(q), tensor_desc(k), tensor_desc(v), tensor_desc(out)
+    fd = kv_full.desc() if kv_full is not None else None
+    rd = kv_ring.desc() if kv_ring is not None else None
+    m = _Mask(head_is_streaming)
+    _check(lib().aoh_prefill_varlen(ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd), _ptr(cu_seqlens),
+                                    cu_seqlens.numel() - 1, max_seqlen, m.ptr, n_sink, window, chunk,
+                                    ctypes.byref(fd) if fd else None, ctypes.byref(rd) if rd else None,
                                     ctypes.byref(od), _stream(stream)))
     return out
 

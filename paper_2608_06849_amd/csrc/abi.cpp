@@ -158,24 +158,48 @@ static aoh_status check_ring(const aoh_ring_cache* c, int n_str, int n_sink, int
 
 // Prefill; with append set, also writes the prompt's K/V (positions 0..T-1 of
 // every sequence) into kv_full / kv_ring.
+// Varlen (packed) form of a prefill call: cu_seqlens != nullptr.
+struct Varlen {
+  const int32_t* cu_seqlens = nullptr;  // DEVICE [batch + 1]
+  int32_t batch = 0, max_seqlen = 0;
+};
+
 static aoh_status prefill_impl(const aoh_tensor* q, const aoh_tensor* k, const aoh_tensor* v,
                                const uint8_t* head_is_streaming, int32_t n_sink, int32_t window,
                                int32_t chunk, bool append, const aoh_paged_cache* kv_full,
-                               const aoh_ring_cache* kv_ring, aoh_tensor* out, void* stream) {
+                               const aoh_ring_cache* kv_ring, aoh_tensor* out, void* stream,
+                               const Varlen& vl = Varlen()) {
   aoh_status st;
-  if ((st = check_tensor(q, "q", 4, AOH_BF16, AOH_F32))) return st;
+  const bool packed = vl.cu_seqlens != nullptr;
+  const int nd = packed ? 3 : 4;  // packed tensors are [total][H][D]
+  if ((st = check_tensor(q, "q", nd, AOH_BF16, AOH_F32))) return st;
   const int dt = q->dtype;
-  if ((st = check_tensor(k, "k", 4, dt, dt))) return st;
-  if ((st = check_tensor(v, "v", 4, dt, dt))) return st;
-  if ((st = check_tensor(out, "out", 4, dt, AOH_F32))) return st;
-  const int64_t B = q->shape[0], T = q->shape[1], Hq = q->shape[2], D = q->shape[3];
-  const int64_t Hkv = k->shape[2];
-  for (const aoh_tensor* t : {k, v})
-    if (t->shape[0] != B || t->shape[1] != T || t->shape[2] != Hkv || t->shape[3] != D)
-      return fail(AOH_ERR_INVALID_ARG, "k/v must be [B=%lld, T=%lld, Hkv, D=%lld] with equal shapes",
-                  (long long)B, (long long)T, (long long)D);
-  if (out->shape[0] != B || out->shape[1] != T || out->shape[2] != Hq || out->shape[3] != D)
-    return fail(AOH_ERR_INVALID_ARG, "out must have the shape of q");
+  if ((st = check_tensor(k, "k", nd, dt, dt))) return st;
+  if ((st = check_tensor(v, "v", nd, dt, dt))) return st;
+  if ((st = check_tensor(out, "out", nd, dt, AOH_F32))) return st;
+  // as [B][T][H][D]; packed: B = batch, T = max_seqlen, rows = total tokens
+  const int64_t n_rows = packed ? q->shape[0] : q->shape[1];
+  const int64_t B = packed ? vl.batch : q->shape[0], T = packed ? vl.max_seqlen : q->shape[1];
+  const int64_t Hq = q->shape[nd - 2], D = q->shape[nd - 1];
+  const int64_t Hkv = k->shape[nd - 2];
+  if (packed) {
+    if (B < 1) return fail(AOH_ERR_INVALID_ARG, "batch=%lld must be >= 1", (long long)B);
+    if (T < 1) return fail(AOH_ERR_INVALID_ARG, "max_seqlen=%lld must be >= 1", (long long)T);
+    if (n_rows > (1ll << 31) - 1) return fail(AOH_ERR_UNSUPPORTED, "too many packed tokens");
+    for (const aoh_tensor* t : {k, v})
+      if (t->shape[0] != n_rows || t->shape[1] != Hkv || t->shape[2] != D)
+        return fail(AOH_ERR_INVALID_ARG, "k/v must be [total=%lld, Hkv, D=%lld] with equal shapes",
+                    (long long)n_rows, (long long)D);
+    if (out->shape[0] != n_rows || out->shape[1] != Hq || out->shape[2] != D)
+      return fail(AOH_ERR_INVALID_ARG, "out must have the shape of q");
+  } else {
+    for (const aoh_tensor* t : {k, v})
+      if (t->shape[0] != B || t->shape[1] != T || t->shape[2] != Hkv || t->shape[3] != D)
+        return fail(AOH_ERR_INVALID_ARG, "k/v must be [B=%lld, T=%lld, Hkv, D=%lld] with equal shapes",
+                    (long long)B, (long long)T, (long long)D);
+    if (out->shape[0] != B || out->shape[1] != T || out->shape[2] != Hq || out->shape[3] != D)
+      return fail(AOH_ERR_INVALID_ARG, "out must have the shape of q");
+  }
   if (D != 64 && D != 128) return fail(AOH_ERR_UNSUPPORTED, "D=%lld; supported: 64, 128", (long long)D);
   if (Hq % Hkv) return fail(AOH_ERR_UNSUPPORTED, "Hq=%lld is not a multiple of Hkv=%lld", (long long)Hq, (long long)Hkv);
   if (T > (1ll << 30)) return fail(AOH_ERR_UNSUPPORTED, "T=%lld too large", (long long)T);
@@ -195,10 +219,19 @@ static aoh_status prefill_impl(const aoh_tensor* q, const aoh_tensor* k, const a
   PrefillArgs a;
   std::memset(&a, 0, sizeof(a));
   a.q = q->data; a.k = k->data; a.v = v->data; a.out = out->data;
-  a.q_sb = q->stride[0]; a.q_st = q->stride[1]; a.q_sh = q->stride[2];
-  a.k_sb = k->stride[0]; a.k_st = k->stride[1]; a.k_sh = k->stride[2];
-  a.v_sb = v->stride[0]; a.v_st = v->stride[1]; a.v_sh = v->stride[2];
-  a.o_sb = out->stride[0]; a.o_st = out->stride[1]; a.o_sh = out->stride[2];
+  if (packed) {
+    a.q_st = q->stride[0]; a.q_sh = q->stride[1];
+    a.k_st = k->stride[0]; a.k_sh = k->stride[1];
+    a.v_st = v->stride[0]; a.v_sh = v->stride[1];
+    a.o_st = out->stride[0]; a.o_sh = out->stride[1];
+    a.cu_seqlens = vl.cu_seqlens;
+    a.total = (int)n_rows;
+  } else {
+    a.q_sb = q->stride[0]; a.q_st = q->stride[1]; a.q_sh = q->stride[2];
+    a.k_sb = k->stride[0]; a.k_st = k->stride[1]; a.k_sh = k->stride[2];
+    a.v_sb = v->stride[0]; a.v_st = v->stride[1]; a.v_sh = v->stride[2];
+    a.o_sb = out->stride[0]; a.o_st = out->stride[1]; a.o_sh = out->stride[2];
+  }
   a.B = (int)B; a.T = (int)T; a.gs = gs;
   a.n_sink = n_sink; a.window = window; a.chunk = chunk;
   a.n_qblocks = (int)n_qblocks;
@@ -233,6 +266,8 @@ static aoh_status prefill_impl(const aoh_tensor* q, const aoh_tensor* k, const a
     hipError_t e = launch_prefill(a, dt, out_f32, (int)D, true, s);
     if (e != hipSuccess) return fail(AOH_ERR_HIP, "prefill streaming launch: %s", hipGetErrorString(e));
   }
+  if (append && !fused && packed)
+    return fail(AOH_ERR_UNSUPPORTED, "packed prefill with cache append needs bf16");
   if (append && !fused) {
     AppendArgs ap;
     std::memset(&ap, 0, sizeof(ap));
@@ -270,6 +305,19 @@ aoh_status aoh_prefill_chunked(const aoh_tensor* q, const aoh_tensor* k, const a
                                int32_t chunk, aoh_tensor* out, void* stream) {
   if (chunk < 1) return fail(AOH_ERR_INVALID_ARG, "chunk=%d must be >= 1", chunk);
   return prefill_impl(q, k, v, head_is_streaming, n_sink, window, chunk, false, nullptr, nullptr, out, stream);
+}
+
+aoh_status aoh_prefill_varlen(const aoh_tensor* q, const aoh_tensor* k, const aoh_tensor* v,
+                              const int32_t* cu_seqlens, int32_t batch, int32_t max_seqlen,
+                              const uint8_t* head_is_streaming, int32_t n_sink, int32_t window, int32_t chunk,
+                              const aoh_paged_cache* kv_full, const aoh_ring_cache* kv_ring, aoh_tensor* out,
+                              void* stream) {
+  if (chunk < 0) return fail(AOH_ERR_INVALID_ARG, "chunk=%d must be >= 0", chunk);
+  if (!cu_seqlens) return fail(AOH_ERR_INVALID_ARG, "cu_seqlens: null pointer");
+  Varlen vl;
+  vl.cu_seqlens = cu_seqlens; vl.batch = batch; vl.max_seqlen = max_seqlen;
+  const bool append = kv_full != nullptr || kv_ring != nullptr;
+  return prefill_impl(q, k, v, head_is_streaming, n_sink, window, chunk, append, kv_full, kv_ring, out, stream, vl);
 }
 
 aoh_status aoh_prefill_append(const aoh_tensor* q, const aoh_tensor* k, const aoh_tensor* v,

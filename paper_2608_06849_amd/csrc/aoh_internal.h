@@ -22,7 +22,12 @@ struct PrefillArgs {
   int64_t k_sb, k_st, k_sh;
   int64_t v_sb, v_st, v_sh;
   int64_t o_sb, o_st, o_sh;
-  int32_t B, T, gs;      // gs = query heads per KV head
+  int32_t B, T, gs;      // gs = query heads per KV head; T = the longest sequence (varlen)
+  // Packed variable-length batch: sequence b is rows cu_seqlens[b] ..
+  // cu_seqlens[b+1] - 1 of the tensors (token stride *_st; *_sb unused);
+  // nullptr for the dense [B][T] layout.  total = rows of the tensors.
+  const int32_t* cu_seqlens;
+  int32_t total;
   int32_t n_kv;          // KV heads in this launch
   int32_t n_sink, window;
   int32_t chunk;         // streaming mask: 0 = per-token band, K >= 1 = chunk eviction

@@ -119,8 +119,16 @@ __global__ __launch_bounds__(kWaves * kWave, kRB == 1 ? 2 : 1) void prefill_bf16
   const int lane = tid & 63;
   const int l32 = lane & 31;
   const int h2 = lane >> 5;
-  const int T = a.T;
+  int T = a.T;
+  int64_t tok0 = 0;  // varlen: first row of this sequence in the packed tensors
+  if (a.cu_seqlens) {
+    const int s0 = min(max(a.cu_seqlens[b], 0), a.total);
+    const int s1 = min(max(a.cu_seqlens[b + 1], s0), a.total);
+    T = min(s1 - s0, a.T);
+    tok0 = s0;
+  }
   const int i0 = qb * kPrefillRows;
+  if (i0 >= T) return;  // query block past this sequence's end (whole workgroup)
   const int r0 = i0 + wave * kRowsPerWave;      // first row of this wave
   int my_row[kRB];                              // row of this lane in each 32-row block
   int my_lo[kRB];                               // its first visible non-sink key (streaming)
@@ -130,9 +138,13 @@ __global__ __launch_bounds__(kWaves * kWave, kRB == 1 ? 2 : 1) void prefill_bf16
     my_lo[rb] = lo_of(my_row[rb], a.chunk, a.window);
   }
 
-  const uint16_t* qp = reinterpret_cast<const uint16_t*>(a.q) + (int64_t)b * a.q_sb + (int64_t)h * a.q_sh;
-  const uint16_t* kp = reinterpret_cast<const uint16_t*>(a.k) + (int64_t)b * a.k_sb + (int64_t)g * a.k_sh;
-  const uint16_t* vp = reinterpret_cast<const uint16_t*>(a.v) + (int64_t)b * a.v_sb + (int64_t)g * a.v_sh;
+  const int64_t qoff = a.cu_seqlens ? tok0 * a.q_st : (int64_t)b * a.q_sb;
+  const int64_t koff = a.cu_seqlens ? tok0 * a.k_st : (int64_t)b * a.k_sb;
+  const int64_t voff = a.cu_seqlens ? tok0 * a.v_st : (int64_t)b * a.v_sb;
+  const int64_t ooff = a.cu_seqlens ? tok0 * a.o_st : (int64_t)b * a.o_sb;
+  const uint16_t* qp = reinterpret_cast<const uint16_t*>(a.q) + qoff + (int64_t)h * a.q_sh;
+  const uint16_t* kp = reinterpret_cast<const uint16_t*>(a.k) + koff + (int64_t)g * a.k_sh;
+  const uint16_t* vp = reinterpret_cast<const uint16_t*>(a.v) + voff + (int64_t)g * a.v_sh;
 
   // Q^T operands: lane holds row my_row[rb], dims 8*h2 + 16*s .. +8.
   bf16x8 qreg[kRB][kKSteps];
@@ -469,7 +481,7 @@ __global__ __launch_bounds__(kWaves * kWave, kRB == 1 ? 2 : 1) void prefill_bf16
     const float inv = 1.f / l_tot;
     if (my_row[rb] >= T) continue;
     if (OUT_F32) {
-      float* op = reinterpret_cast<float*>(a.out) + (int64_t)b * a.o_sb + (int64_t)my_row[rb] * a.o_st +
+      float* op = reinterpret_cast<float*>(a.out) + ooff + (int64_t)my_row[rb] * a.o_st +
                   (int64_t)h * a.o_sh;
 #pragma unroll
       for (int mb = 0; mb < kMBlocks; ++mb)
@@ -481,7 +493,7 @@ __global__ __launch_bounds__(kWaves * kWave, kRB == 1 ? 2 : 1) void prefill_bf16
           *reinterpret_cast<f32x4*>(op + 32 * mb + 8 * q4 + 4 * h2) = w;
         }
     } else {
-      uint16_t* op = reinterpret_cast<uint16_t*>(a.out) + (int64_t)b * a.o_sb + (int64_t)my_row[rb] * a.o_st +
+      uint16_t* op = reinterpret_cast<uint16_t*>(a.out) + ooff + (int64_t)my_row[rb] * a.o_st +
                      (int64_t)h * a.o_sh;
 #pragma unroll
       for (int mb = 0; mb < kMBlocks; ++mb)
@@ -514,11 +526,23 @@ __global__ __launch_bounds__(kPrefillRowsF32) void prefill_f32_kernel(PrefillArg
   const int g = a.kv_heads[qh_local / a.gs];
   const int h = g * a.gs + (qh_local % a.gs);
   const int i = qb * kPrefillRowsF32 + threadIdx.x;
-  if (i >= a.T) return;
-  const float* qp = reinterpret_cast<const float*>(a.q) + (int64_t)b * a.q_sb + (int64_t)i * a.q_st +
+  int T = a.T;
+  int64_t tok0 = 0;
+  if (a.cu_seqlens) {
+    const int s0 = min(max(a.cu_seqlens[b], 0), a.total);
+    const int s1 = min(max(a.cu_seqlens[b + 1], s0), a.total);
+    T = min(s1 - s0, a.T);
+    tok0 = s0;
+  }
+  if (i >= T) return;
+  const int64_t qoff = a.cu_seqlens ? tok0 * a.q_st : (int64_t)b * a.q_sb;
+  const int64_t koff = a.cu_seqlens ? tok0 * a.k_st : (int64_t)b * a.k_sb;
+  const int64_t voff = a.cu_seqlens ? tok0 * a.v_st : (int64_t)b * a.v_sb;
+  const int64_t ooff = a.cu_seqlens ? tok0 * a.o_st : (int64_t)b * a.o_sb;
+  const float* qp = reinterpret_cast<const float*>(a.q) + qoff + (int64_t)i * a.q_st +
                     (int64_t)h * a.q_sh;
-  const float* kp = reinterpret_cast<const float*>(a.k) + (int64_t)b * a.k_sb + (int64_t)g * a.k_sh;
-  const float* vp = reinterpret_cast<const float*>(a.v) + (int64_t)b * a.v_sb + (int64_t)g * a.v_sh;
+  const float* kp = reinterpret_cast<const float*>(a.k) + koff + (int64_t)g * a.k_sh;
+  const float* vp = reinterpret_cast<const float*>(a.v) + voff + (int64_t)g * a.v_sh;
   float q[D], o[D];
 #pragma unroll
   for (int d = 0; d < D; ++d) {
@@ -548,7 +572,7 @@ __global__ __launch_bounds__(kPrefillRowsF32) void prefill_f32_kernel(PrefillArg
   };
   for (int j = 0; j < sink_end; ++j) visit(j);
   for (int j = lo; j <= i; ++j) visit(j);
-  float* op = reinterpret_cast<float*>(a.out) + (int64_t)b * a.o_sb + (int64_t)i * a.o_st + (int64_t)h * a.o_sh;
+  float* op = reinterpret_cast<float*>(a.out) + ooff + (int64_t)i * a.o_st + (int64_t)h * a.o_sh;
   const float inv = 1.f / l;
 #pragma unroll
   for (int d = 0; d < D; ++d) op[d] = o[d] * inv;
