@@ -72,6 +72,7 @@ def parse():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-stack-decode", action="store_true")
     ap.add_argument("--no-classify", action="store_true")
+    ap.add_argument("--no-varlen", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (for scaling HBM counters)")
     return ap.parse_args()
@@ -252,6 +253,9 @@ def main():
     cls = None
     if not args.no_classify:
         cls = classify_leg(args, torch, synth)
+    vlen = None
+    if not args.no_varlen:
+        vlen = varlen_leg(args, torch, synth)
 
     # ------------------------------------------------------------------ CPU baseline (oracle)
     cpu = None
@@ -298,6 +302,7 @@ def main():
         "decode": dec,
         "stack_decode": stack,
         "classify": cls,
+        "varlen_prefill": vlen,
         "cpu_baseline": cpu,
         "paper_context": "paper (hardware unstated, end-to-end model latency, bf16, batch 1): prefill/decode "
                          "latency reduction up to 41.4%/66.0% and 50.0% KV saving at 256K, 50% sparsity",
@@ -527,6 +532,61 @@ def stack_decode_leg(args, torch, synth, PagedCache, RingCache, aoh_decode, aoh_
     }
     log(f"stack decode: eager {eager_ms:.3f} ms/step, graph {graph_ms:.3f} ms/step, "
         f"{res['kv_gbps_graph']:.0f} GB/s with the graph")
+    return res
+
+
+def varlen_leg(args, torch, synth):
+    """The variable-length workload (16 sequences of U[4096, 65536] tokens, 32 q /
+    8 KV heads, d_head 128, bf16, n_sink 64) as one packed prefill per setting
+    (streaming fraction x window), against one prefill call per sequence."""
+    from paper_2608_06849_amd import aoh_prefill, aoh_prefill_varlen
+    c = synth.CONFIGS["varlen_sweep"]
+    lens = synth.lengths_uniform(c["n_seq"], c["len_lo"], c["len_hi"], c["seed"])
+    bf = torch.bfloat16
+    t0 = time.time()
+    parts = [synth.sweep_sequence(b, int(lens[b])) for b in range(len(lens))]
+    q = torch.cat([torch.from_numpy(p["q"][0]).to(bf) for p in parts]).to("cuda")
+    k = torch.cat([torch.from_numpy(p["k"][0]).to(bf) for p in parts]).to("cuda")
+    v = torch.cat([torch.from_numpy(p["v"][0]).to(bf) for p in parts]).to("cuda")
+    del parts
+    cu = torch.tensor(np.concatenate([[0], np.cumsum(lens)]), dtype=torch.int32, device="cuda")
+    out = torch.empty_like(q)
+    offs = np.concatenate([[0], np.cumsum(lens)])
+    hq, hkv, d, n_sink = c["hq"], c["hkv"], c["d"], c["n_sink"]
+    gs = hq // hkv
+    torch.cuda.synchronize()
+    log(f"varlen workload ready in {time.time() - t0:.1f}s ({int(lens.sum())} tokens)")
+
+    def timed(fn, n=3):
+        fn()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        ev[0].record()
+        for _ in range(n):
+            fn()
+        ev[1].record()
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]) / n
+
+    res = {"workload": f"{len(lens)} sequences of U[4096, 65536] tokens ({int(lens.sum())} total), 32 q / 8 KV heads, "
+                       "d_head 128, bf16, n_sink 64; one packed prefill call", "settings": []}
+    for sp in c["sparsity_pct"]:
+        n_str = synth.n_streaming_for(hkv, sp)
+        for window in c["windows"]:
+            mask = synth.choose_streaming(hkv, n_str, c["seed"], "streaming", sp, window).tolist()
+            fl = sum(useful_prefill_flops(int(n), d, gs * (hkv - n_str), gs * n_str, n_sink, window) for n in lens)
+            ms = timed(lambda: aoh_prefill_varlen(q, k, v, cu, int(lens.max()), mask, n_sink, window, out=out))
+            entry = {"streaming_pct": sp, "window": window, "ms": round(ms, 3),
+                     "useful_tflop": round(fl / 1e12, 3), "tflops": round(fl / (ms * 1e-3) / 1e12, 1)}
+            if sp == 50 and window == 4096:
+                def per_seq():
+                    for b in range(len(lens)):
+                        sl = slice(int(offs[b]), int(offs[b + 1]))
+                        aoh_prefill(q[sl][None], k[sl][None], v[sl][None], mask, n_sink, window, out=out[sl][None])
+                entry["per_sequence_calls_ms"] = round(timed(per_seq), 3)
+            res["settings"].append(entry)
+            log(f"varlen {sp}% w{window}: {ms:.2f} ms, {entry['tflops']} TFLOP/s")
+    del q, k, v, out
     return res
 
 

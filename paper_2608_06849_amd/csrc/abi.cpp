@@ -158,6 +158,8 @@ static aoh_status check_ring(const aoh_ring_cache* c, int n_str, int n_sink, int
 
 // Prefill; with append set, also writes the prompt's K/V (positions 0..T-1 of
 // every sequence) into kv_full / kv_ring.
+constexpr int64_t kSeqMajorMaxBatch = 64;
+
 // Varlen (packed) form of a prefill call: cu_seqlens != nullptr.
 struct Varlen {
   const int32_t* cu_seqlens = nullptr;  // DEVICE [batch + 1]
@@ -226,6 +228,9 @@ static aoh_status prefill_impl(const aoh_tensor* q, const aoh_tensor* k, const a
     a.o_st = out->stride[0]; a.o_sh = out->stride[1];
     a.cu_seqlens = vl.cu_seqlens;
     a.total = (int)n_rows;
+    // sequence-major order for the bf16 kernel when the per-workgroup walk
+    // over the sequences stays short
+    a.seq_major = (dt == AOH_BF16 && B <= kSeqMajorMaxBatch) ? 1 : 0;
   } else {
     a.q_sb = q->stride[0]; a.q_st = q->stride[1]; a.q_sh = q->stride[2];
     a.k_sb = k->stride[0]; a.k_st = k->stride[1]; a.k_sh = k->stride[2];

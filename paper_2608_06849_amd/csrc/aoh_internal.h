@@ -28,6 +28,7 @@ struct PrefillArgs {
   // nullptr for the dense [B][T] layout.  total = rows of the tensors.
   const int32_t* cu_seqlens;
   int32_t total;
+  int32_t seq_major;     // varlen: visit sequences in order (heaviest block first in each)
   int32_t n_kv;          // KV heads in this launch
   int32_t n_sink, window;
   int32_t chunk;         // streaming mask: 0 = per-token band, K >= 1 = chunk eviction

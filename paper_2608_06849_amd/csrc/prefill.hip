@@ -107,10 +107,29 @@ __global__ __launch_bounds__(kWaves * kWave, kRB == 1 ? 2 : 1) void prefill_bf16
   const int per_block = n_qh * a.B;
   const int wg = blockIdx.x;
   // Heaviest query blocks first (longest-processing-time order) for causal work.
-  const int qb = a.n_qblocks - 1 - wg / per_block;
+  int qb = a.n_qblocks - 1 - wg / per_block;
   const int rem = wg % per_block;
-  const int qh_local = rem % n_qh;
-  const int b = rem / n_qh;
+  int qh_local = rem % n_qh;
+  int b = rem / n_qh;
+  if (a.seq_major) {
+    // Packed batch, sequence-major: the workgroups in flight share one or two
+    // sequences' K/V (cache reuse); heaviest block first within a sequence.
+    int unit = wg / n_qh;
+    qh_local = wg % n_qh;
+    b = -1;
+    for (int s2 = 0; s2 < a.B; ++s2) {
+      const int s0 = min(max(a.cu_seqlens[s2], 0), a.total);
+      const int s1 = min(max(a.cu_seqlens[s2 + 1], s0), a.total);
+      const int nb = (min(s1 - s0, a.T) + kPrefillRows - 1) / kPrefillRows;
+      if (unit < nb) {
+        b = s2;
+        qb = nb - 1 - unit;
+        break;
+      }
+      unit -= nb;
+    }
+    if (b < 0) return;  // past the last sequence's blocks
+  }
   const int g = a.kv_heads[qh_local / a.gs];
   const int h = g * a.gs + (qh_local % a.gs);
 
