@@ -94,11 +94,11 @@ def copy_calibration():
 # 1 GiB copy (bench.py --copy-calibration), and the hash of the kernel sources
 # they were taken on: a source change makes the figure stale and it is dropped.
 TRAFFIC = {
-    "source_hash": "6ff0fd057756bc7d",
+    "source_hash": "81cb6a92dcdd2413",
     "fetch_factor": 524301.2 / 1048576.0,   # FETCH_SIZE of a 1 GiB copy / 1 GiB
     "write_factor": 1048576.0 / 1048576.0,  # WRITE_SIZE of a 1 GiB copy / 1 GiB
-    "prefill_retrieval": {"fetch_kib": 1033996.8, "write_kib": 114701.0},
-    "decode_split": {"fetch_kib": 1061481.4, "write_kib": 4829.6},
+    "prefill_retrieval": {"fetch_kib": 966819.8, "write_kib": 114691.2},
+    "decode_split": {"fetch_kib": 1074770.4, "write_kib": 4829.9},
 }
 
 
