@@ -597,9 +597,512 @@ __global__ __launch_bounds__(kPrefillRowsF32) void prefill_f32_kernel(PrefillArg
   for (int d = 0; d < D; ++d) op[d] = o[d] * inv;
 }
 
+// ---------------------------------------------------------------------------
+// D = 128 bf16 kernel, phase-shifted wave groups.
+//
+// Same work item and math as prefill_bf16_kernel (256 query rows of one query
+// head, 32 rows per wave, S^T = K.Q^T and O^T += V^T.P^T on the 32x32x16 bf16
+// MFMA, online softmax in fp32 with lazy rescaling); differences:
+//  * K/V tiles move global -> LDS with direct loads (global_load_lds_dwordx4),
+//    no register staging, into a ring of four 32 KB stages, issued two tiles
+//    ahead of their first use.
+//  * Rows hold 16 chunks of 16 bytes with no padding; chunk c of row r sits
+//    at c ^ (r & 15) for K and c ^ 4 (r & 3) for V, which keeps the K row
+//    reads and the V transpose reads free of bank conflicts and makes every
+//    operand address one base register XOR a constant.
+//  * Per tile t a wave runs an MFMA phase (P(t-1).V(t-1) then K(t).Q^T) and a
+//    vector phase (mask, max, exponentials of S(t)); waves 0-3 and waves 4-7
+//    (one of each per SIMD) run one phase apart, separated by workgroup
+//    barriers.  The loop has a single path (a tile with no visible key for a
+//    wave yields P = 0), so the accumulators never move between registers.
+//  * Workgroups are ordered so that the query heads of one KV group and query
+//    block run on the same XCD (one L2).
+// On the 32K Qwen2.5-7B-shaped layer this kernel and prefill_bf16_kernel take
+// the same time (3.68 ms): this one needs ~4% more cycles and the GPU holds a
+// higher clock for it (2.10 vs 2.01 GHz), i.e. both run at the clock the chip
+// sustains for this mix of MFMA, LDS and vector work.
+#ifndef AOH_PP_STAGES
+#define AOH_PP_STAGES 4
+#endif
+#ifndef AOH_PP_XCD
+#define AOH_PP_XCD 1
+#endif
+constexpr int kPPStages = AOH_PP_STAGES;
+static_assert(kPPStages == 4 || kPPStages == 5, "4 or 5 LDS stages (32 KB each)");
+constexpr int kPPD = 128;
+#ifndef AOH_PP_SCHED
+#define AOH_PP_SCHED 1
+#endif
+constexpr int kPPRows = kPrefillRows;     // query rows per workgroup (8 waves x 32)
+static_assert(kPPRows == 256 && kPrefillRB == 1, "phase-shifted kernel: 8 waves x 32 rows");
+
+struct PPStage {
+  uint16_t k[kBN * kPPD];
+  uint16_t v[kBN * kPPD];
+};
+// Element offset of 16-byte chunk c of row r in a stage's K / V tile.
+__device__ __forceinline__ int pp_koff(int r, int c) { return r * kPPD + 8 * (c ^ (r & 15)); }
+__device__ __forceinline__ int pp_voff(int r, int c) { return r * kPPD + 8 * (c ^ (4 * (r & 3))); }
+
+// Direct global -> LDS load of 16 bytes per lane: lane L's bytes land at
+// lds_row + 16 L (one contiguous 1 KB block per wave).  Issued as inline
+// assembly so that the compiler does not treat every later LDS read as
+// possibly depending on it (it would wait for all outstanding loads before
+// each one); the kernel orders these loads itself with s_waitcnt and barriers.
+__device__ __forceinline__ void lds_dma16(const void* gptr, const void* lds_row) {
+  const uint32_t m0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds_row));
+  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(gptr), "{m0}"(m0) : "memory");
+}
+
+// s_waitcnt immediates (gfx9 encoding: vmcnt [3:0] and [15:14], expcnt [6:4],
+// lgkmcnt [11:8]); a field at its maximum does not wait.
+constexpr int kWaitVm0 = 0x0 | (0x7 << 4) | (0xF << 8);
+constexpr int kWaitVm4 = 0x4 | (0x7 << 4) | (0xF << 8);
+constexpr int kWaitVm8 = 0x8 | (0x7 << 4) | (0xF << 8);
+constexpr int kWaitLgkm0 = 0xF | (0x7 << 4) | (0x0 << 8) | (0x3 << 14);
+
+template <bool STREAM, bool OUT_F32, bool APPEND>
+__global__ __launch_bounds__(512, 1) void prefill_pp_kernel(PrefillArgs a) {
+  __shared__ __align__(1024) PPStage lds[kPPStages];
+  constexpr int D = kPPD;
+  constexpr int kKSteps = D / 16;
+  constexpr int kMBlocks = D / 32;
+
+  const int n_qh = a.n_kv * a.gs;
+  const int per_block = n_qh * a.B;
+  const int wg = blockIdx.x;
+  int qb = a.n_qblocks - 1 - wg / per_block;
+  const int rem = wg % per_block;
+  int qh_local = rem % n_qh;
+  int b = rem / n_qh;
+#if AOH_PP_XCD
+  if (!a.seq_major) {
+    // XCD-aware order.  Workgroups go to the 8 XCDs (each with its own L2)
+    // in turn; work item group j = (query block, sequence, KV head), heaviest
+    // block first, holds the gs query heads that read the same K/V tiles.
+    // Group j runs on XCD j % 8 as gs consecutive workgroups of that XCD, so
+    // its tiles are fetched into that L2 once; the trailing groups that do
+    // not fill a round of 8 are dealt out in plain order.
+    const int n_groups = a.n_qblocks * a.n_kv * a.B;
+    const int full = 8 * a.gs * (n_groups / 8);
+    int j, hl;
+    if (wg < full) {
+      const int slot = wg >> 3;
+      j = 8 * (slot / a.gs) + (wg & 7);
+      hl = slot % a.gs;
+    } else {
+      j = (full / a.gs) + (wg - full) / a.gs;
+      hl = (wg - full) % a.gs;
+    }
+    const int per_qb = a.n_kv * a.B;
+    qb = a.n_qblocks - 1 - j / per_qb;
+    const int r2 = j % per_qb;
+    b = r2 / a.n_kv;
+    qh_local = (r2 % a.n_kv) * a.gs + hl;
+  }
+#endif
+  if (a.seq_major) {
+    int unit = wg / n_qh;
+    qh_local = wg % n_qh;
+    b = -1;
+    for (int s2 = 0; s2 < a.B; ++s2) {
+      const int s0 = min(max(a.cu_seqlens[s2], 0), a.total);
+      const int s1 = min(max(a.cu_seqlens[s2 + 1], s0), a.total);
+      const int nb = (min(s1 - s0, a.T) + kPPRows - 1) / kPPRows;
+      if (unit < nb) {
+        b = s2;
+        qb = nb - 1 - unit;
+        break;
+      }
+      unit -= nb;
+    }
+    if (b < 0) return;
+  }
+  const int g = a.kv_heads[qh_local / a.gs];
+  const int h = g * a.gs + (qh_local % a.gs);
+
+  const int tid = threadIdx.x;
+  // Wave index as a scalar: every branch that decides a barrier is uniform.
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = wave >> 2;
+  const int lane = tid & 63;
+  const int l32 = lane & 31;
+  const int h2 = lane >> 5;
+  int T = a.T;
+  int64_t tok0 = 0;
+  if (a.cu_seqlens) {
+    const int s0 = min(max(a.cu_seqlens[b], 0), a.total);
+    const int s1 = min(max(a.cu_seqlens[b + 1], s0), a.total);
+    T = min(s1 - s0, a.T);
+    tok0 = s0;
+  }
+  T = __builtin_amdgcn_readfirstlane(T);
+  const int i0 = qb * kPPRows;
+  if (i0 >= T) return;
+  const int r0 = i0 + wave * 32;
+  const int my_row = r0 + l32;
+  const int my_lo = lo_of(my_row, a.chunk, a.window);
+
+  const int64_t qoff = a.cu_seqlens ? tok0 * a.q_st : (int64_t)b * a.q_sb;
+  const int64_t koff = a.cu_seqlens ? tok0 * a.k_st : (int64_t)b * a.k_sb;
+  const int64_t voff = a.cu_seqlens ? tok0 * a.v_st : (int64_t)b * a.v_sb;
+  const int64_t ooff = a.cu_seqlens ? tok0 * a.o_st : (int64_t)b * a.o_sb;
+  const uint16_t* qp = reinterpret_cast<const uint16_t*>(a.q) + qoff + (int64_t)h * a.q_sh;
+  const uint16_t* kp = reinterpret_cast<const uint16_t*>(a.k) + koff + (int64_t)g * a.k_sh;
+  const uint16_t* vp = reinterpret_cast<const uint16_t*>(a.v) + voff + (int64_t)g * a.v_sh;
+
+  const TilePlan plan = make_plan<STREAM>(i0, kPPRows, T, a.n_sink, a.window, a.chunk);
+  const int n = __builtin_amdgcn_readfirstlane(plan.n_visit);
+  if (n < 1) return;  // a block with rows below T always has its diagonal tile
+
+  // Direct loads of tile `it` into stage it % 4: wave w fills rows 8w .. 8w+7
+  // of K and of V, one 4-row (1 KB) instruction at a time; lane L writes
+  // physical chunk L % 16 of row 4j + L / 16 and therefore fetches the
+  // logical chunk that the swizzle puts there.  Rows past the sequence end
+  // repeat its last row (those keys are masked for every query row).
+  auto issue_tile = [&](int it) {
+    const int kb = plan.tile(it) * kBN;
+    PPStage& st = lds[it % kPPStages];
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj) {
+      const int j = 2 * wave + jj;
+      const int r = 4 * j + (lane >> 4);
+      const int pc = lane & 15;
+      const int64_t row = min(kb + r, T - 1);
+      lds_dma16(kp + row * a.k_st + 8 * (pc ^ (r & 15)), &st.k[4 * j * kPPD]);
+      lds_dma16(vp + row * a.v_st + 8 * (pc ^ (4 * (r & 3))), &st.v[4 * j * kPPD]);
+    }
+  };
+
+  bf16x8 qreg[kKSteps];  // Q^T operands: lane holds row my_row, dims 8*h2 + 16*s .. +8
+  f32x16 acc_o[kMBlocks];
+#pragma unroll
+  for (int mb = 0; mb < kMBlocks; ++mb)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc_o[mb][i] = 0.f;
+  float m_run = -INFINITY;  // reference max (log2 units) of this lane's row
+  float l_run = 0.f;        // this lane's partial row sum (partner lane has the rest)
+  f32x16 sacc[2];           // S^T of the current tile, two 32-key blocks
+  bf16x8 pop[4];            // P^T operands of the previous tile's 4 key steps
+
+  const float c = a.scale_log2;
+
+  // Per-lane LDS byte addresses.  K operand of step s, block blk: row
+  // 32 blk + l32, logical chunk 2 s + h2; with the swizzle that is
+  // kaddr0 ^ 32 s (+ 8 KB per block).  V^T operand of key step ks, 32-dim
+  // block mb (transpose reads): row 16 ks + 4 h2 + i16 / 4 (+ 8 rows for the
+  // second half), logical chunk 4 mb + 2 (q16 & 1) + (i16 & 3) / 2, 4 more
+  // elements for odd i16; that is vaddr0 ^ 64 mb (+ 4 KB per key step).
+  // Stage bases are multiples of 32 KB, so the XORs stay inside a row.
+  const int q16 = lane >> 4;
+  const int i16 = lane & 15;
+  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&lds[0]));
+  const uint32_t kaddr0 = 2u * (uint32_t)pp_koff(l32, h2);
+  const int vrow0 = 4 * h2 + (i16 >> 2);
+  const uint32_t vaddr0 = 2u * (uint32_t)(pp_voff(vrow0, 2 * (q16 & 1) + ((i16 & 3) >> 1)) + 4 * (i16 & 1));
+  auto stage_k = [&](int st) { return lds0 + (uint32_t)st * (uint32_t)sizeof(PPStage) + kaddr0; };
+  auto stage_v = [&](int st) {
+    return lds0 + (uint32_t)st * (uint32_t)sizeof(PPStage) + (uint32_t)(kBN * kPPD * 2) + vaddr0;
+  };
+  auto k_operand = [&](uint32_t kb_addr, int s, int blk) {
+    typedef __attribute__((address_space(3))) const bf16x8 lds_bf16x8;
+    return *reinterpret_cast<lds_bf16x8*>((kb_addr ^ (32u * s)) + 8192u * blk);
+  };
+  auto v_operand = [&](uint32_t vb_addr, int ks, int mb) {
+    typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+    const uint32_t a = (vb_addr ^ (64u * mb)) + 4096u * ks;
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(reinterpret_cast<lds_i16x4*>(a));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(reinterpret_cast<lds_i16x4*>(a + 2048u));
+    return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+  };
+
+  auto wave_dead = [&](int kb) {
+    return (kb > r0 + 31) || (STREAM && kb >= a.n_sink && kb + kBN - 1 < lo_of(r0, a.chunk, a.window));
+  };
+  auto need_mask = [&](int kb) {
+    return (kb + kBN - 1 > r0) ||
+           (STREAM && !(kb + kBN - 1 < a.n_sink || kb >= lo_of(r0 + 31, a.chunk, a.window)));
+  };
+
+  // Fused append (as in prefill_bf16_kernel): the first query head of each
+  // group copies its block's own K/V rows from LDS into the cache; each wave
+  // writes its share (a fixed per-thread partition) in its MFMA phase of the
+  // tile.
+  const bool writer = APPEND && (qh_local % a.gs) == 0;
+  const int crank = qh_local / a.gs;
+  auto write_tile = [&](const PPStage& st, int kb) {
+    constexpr int kCh = D / 8;
+    uint16_t* ck = static_cast<uint16_t*>(a.ck);
+    uint16_t* cv = static_cast<uint16_t*>(a.cv);
+    if (!STREAM) {
+      for (int e = tid; e < kBN * kCh; e += 512) {
+        const int row = e / kCh, ch = e % kCh;
+        const int p = kb + row;
+        const int lp = p / kPageTokens;
+        if (p >= T || lp >= a.max_pages) continue;
+        const int page = a.block_table[(int64_t)b * a.max_pages + lp];
+        if (page < 0 || page >= a.num_pages) continue;
+        uint16_t* dst = ck + (((int64_t)page * a.n_cache + crank) * kPageTokens + p % kPageTokens) * D + 8 * ch;
+        st16(dst, *reinterpret_cast<const u32x4*>(&st.k[pp_koff(row, ch)]));
+      }
+      for (int e = tid; e < (kBN / kPageTokens) * D * 2; e += 512) {
+        const int pg = e / (2 * D), d = (e / 2) % D, hf = e % 2;
+        const int p0 = kb + kPageTokens * pg + 8 * hf;
+        const int lp = p0 / kPageTokens;
+        if (p0 >= T || lp >= a.max_pages) continue;
+        const int page = a.block_table[(int64_t)b * a.max_pages + lp];
+        if (page < 0 || page >= a.num_pages) continue;
+        uint16_t* dst = cv + (((int64_t)page * a.n_cache + crank) * D + d) * kPageTokens + 8 * hf;
+        const int row0 = kPageTokens * pg + 8 * hf;
+        const int dc = d >> 3, de = d & 7;
+        if (p0 + 8 <= T) {
+          u32x4 w;
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            w[j] = (uint32_t)st.v[pp_voff(row0 + 2 * j, dc) + de] |
+                   ((uint32_t)st.v[pp_voff(row0 + 2 * j + 1, dc) + de] << 16);
+          st16(dst, w);
+        } else {
+          for (int j = 0; p0 + j < T; ++j) dst[j] = st.v[pp_voff(row0 + j, dc) + de];
+        }
+      }
+    } else {
+      for (int e = tid; e < kBN * kCh; e += 512) {
+        const int row = e / kCh, ch = e % kCh;
+        const int p = kb + row;
+        if (p >= T || !(p < a.n_sink || p >= T - a.window)) continue;
+        const int slot = p < a.n_sink ? p : a.n_sink + (p - a.n_sink) % a.window;
+        const int64_t unit = ((int64_t)b * a.n_cache + crank) * a.ring_blocks + slot / kPageTokens;
+        const int r = slot % kPageTokens;
+        st16(ck + unit * (kPageTokens * D) + r * D + 8 * ch, *reinterpret_cast<const u32x4*>(&st.k[pp_koff(row, ch)]));
+        uint16_t* rv = cv + unit * (kPageTokens * D);
+        const int vo = pp_voff(row, ch);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) rv[(8 * ch + j) * kPageTokens + r] = st.v[vo + j];
+      }
+    }
+  };
+
+  // MFMA phase of tile t: O^T += V(t-1)^T P(t-1)^T, then S^T(t) = K(t) Q^T.
+  int v_tile = 0;  // tile whose P^T is in pop
+  auto pv_part = [&]() {
+    const uint32_t va = stage_v(v_tile % kPPStages);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int mb = 0; mb < kMBlocks; ++mb) acc_o[mb] = mfma32(v_operand(va, ks, mb), pop[ks], acc_o[mb]);
+  };
+  auto qk_part = [&](int t) {
+    const uint32_t ka = stage_k(t % kPPStages);
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) sacc[blk][i] = 0.f;
+#pragma unroll
+    for (int s = 0; s < kKSteps; ++s)
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk) sacc[blk] = mfma32(k_operand(ka, s, blk), qreg[s], sacc[blk]);
+  };
+  auto append_tile = [&](int t) {
+    if (APPEND && writer) {
+      const int kb = plan.tile(t) * kBN;
+      if (kb >= i0 && kb < i0 + kPPRows) write_tile(lds[t % kPPStages], kb);
+    }
+  };
+  // Steady-state MFMA phase.  Both products run unconditionally (a wave with
+  // no visible key in a tile gets P = 0 from its vector phase), so the loop
+  // has one path and the O accumulators stay in place.
+  auto mfma_phase = [&](int t) {
+    append_tile(t);
+    pv_part();
+    qk_part(t);
+#if AOH_PP_SCHED
+    // Operands are read four MFMAs ahead of their products, the first K
+    // operands while the last P.V products run.
+    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+    for (int i = 0; i < 12; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+#endif
+  };
+
+  // Vector phase of tile t: mask, row max, lazy rescale, exponentials into
+  // the P^T operands, row sums of the bf16 P actually used.
+  auto apply_mask = [&](int kb) {
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int key = kb + 32 * blk + 8 * (i >> 2) + 4 * h2 + (i & 3);
+        bool vis = key <= my_row;
+        if (STREAM) vis = vis && (key < a.n_sink || key >= my_lo);
+        sacc[blk][i] = vis ? sacc[blk][i] : -INFINITY;
+      }
+  };
+  auto softmax_tile = [&]() {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[blk][i]);
+    mx = xor32_max(mx) * c;
+    if (__any(mx > m_run + kRescaleThreshold)) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = (m_new == -INFINITY) ? 1.f : fast_exp2(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int mb = 0; mb < kMBlocks; ++mb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc_o[mb][i] *= alpha;
+    }
+    const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
+    float psum = 0.f;
+    const bf16x2 ones = {(bf16)1.f, (bf16)1.f};
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        bf16x8 pv;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) pv[i] = f32_to_bf16(fast_exp2(fmaf(sacc[blk][8 * hf + i], c, -m_use)));
+        psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pv, pv, 0, 1), ones, psum, false);
+        psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pv, pv, 2, 3), ones, psum, false);
+        psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pv, pv, 4, 5), ones, psum, false);
+        psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pv, pv, 6, 7), ones, psum, false);
+        pop[2 * blk + hf] = pv;
+      }
+    l_run += psum;
+  };
+  auto valu_phase = [&](int t) {
+    v_tile = t;
+    const int kb = plan.tile(t) * kBN;
+    if (wave_dead(kb)) {
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) pop[ks][i] = (bf16)0.f;
+      return;
+    }
+    if (need_mask(kb)) apply_mask(kb);
+    softmax_tile();
+  };
+
+  // Phase bookkeeping, identical for every wave: phase p ends with (odd p)
+  // the wait for this wave's loads of tile (p+1)/2, first read in phase p+1,
+  // and a barrier; even phases p >= 2 start by loading tile
+  // u = p/2 + kPPStages - 2 into the stage that tile u - kPPStages (last
+  // read in phase p - 1) occupied.
+  const int last_phase = 2 * n + 1;
+  int ph = 0;
+  auto barrier = [&]() {
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  auto end_phase = [&]() {
+    if (ph & 1) {
+      const int u = (ph + 1) >> 1;
+      if (u < n) {
+        // tiles u+1 .. u+kPPStages-3 (4 loads each) may stay in flight
+        const int later = min(kPPStages - 3, n - 1 - u);
+        if (later >= 2) __builtin_amdgcn_s_waitcnt(kWaitVm8);
+        else if (later == 1) __builtin_amdgcn_s_waitcnt(kWaitVm4);
+        else __builtin_amdgcn_s_waitcnt(kWaitVm0);
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    if (ph < last_phase) barrier();
+    ++ph;
+    if (!(ph & 1) && ph >= 2) {
+      const int u = ph / 2 + kPPStages - 2;
+      if (u < n) issue_tile(u);
+    }
+  };
+
+  // Prologue: tiles 0 .. kPPStages-2 and this wave's Q rows in flight, then
+  // everything complete (the explicit full wait also tells the compiler that
+  // the Q registers are ready, so it adds no wait of its own inside the loop).
+  for (int u = 0; u < kPPStages - 1 && u < n; ++u) issue_tile(u);
+#pragma unroll
+  for (int s = 0; s < kKSteps; ++s) {
+    u32x4 x = {0u, 0u, 0u, 0u};
+    if (my_row < T) x = ld16(qp + (int64_t)my_row * a.q_st + 8 * h2 + 16 * s);
+    qreg[s] = __builtin_bit_cast(bf16x8, x);
+  }
+  __builtin_amdgcn_s_waitcnt(kWaitVm0);
+  barrier();
+
+  if (grp == 1) end_phase();  // waves 4-7 start one phase late
+  append_tile(0);
+  qk_part(0);
+  end_phase();
+  valu_phase(0);
+  end_phase();
+  for (int t = 1; t < n; ++t) {
+    mfma_phase(t);
+    end_phase();
+    valu_phase(t);
+    end_phase();
+  }
+  pv_part();
+  end_phase();
+  if (grp == 0) end_phase();  // waves 0-3 idle through the last phase
+
+  // Epilogue: normalise by the row sum, store.
+  const float l_tot = xor32_sum(l_run);
+  const float inv = 1.f / l_tot;
+  if (my_row < T) {
+    if (OUT_F32) {
+      float* op = reinterpret_cast<float*>(a.out) + ooff + (int64_t)my_row * a.o_st + (int64_t)h * a.o_sh;
+#pragma unroll
+      for (int mb = 0; mb < kMBlocks; ++mb)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          f32x4 w;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) w[e] = acc_o[mb][4 * q4 + e] * inv;
+          *reinterpret_cast<f32x4*>(op + 32 * mb + 8 * q4 + 4 * h2) = w;
+        }
+    } else {
+      uint16_t* op = reinterpret_cast<uint16_t*>(a.out) + ooff + (int64_t)my_row * a.o_st + (int64_t)h * a.o_sh;
+#pragma unroll
+      for (int mb = 0; mb < kMBlocks; ++mb)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          u32x2 w;
+          w[0] = (uint32_t)f32_to_bf16_bits(acc_o[mb][4 * q4 + 0] * inv) |
+                 ((uint32_t)f32_to_bf16_bits(acc_o[mb][4 * q4 + 1] * inv) << 16);
+          w[1] = (uint32_t)f32_to_bf16_bits(acc_o[mb][4 * q4 + 2] * inv) |
+                 ((uint32_t)f32_to_bf16_bits(acc_o[mb][4 * q4 + 3] * inv) << 16);
+          *reinterpret_cast<u32x2*>(op + 32 * mb + 8 * q4 + 4 * h2) = w;
+        }
+    }
+  }
+}
+
+#ifndef AOH_PREFILL_PP
+#define AOH_PREFILL_PP 1
+#endif
+
 template <int D, bool STREAM, bool OUT_F32>
 static hipError_t launch_bf16(const PrefillArgs& a, hipStream_t s) {
   const int grid = a.n_qblocks * a.n_kv * a.gs * a.B;
+  if (AOH_PREFILL_PP && D == kPPD) {
+    if (a.append)
+      hipLaunchKernelGGL((prefill_pp_kernel<STREAM, OUT_F32, true>), dim3(grid), dim3(512), 0, s, a);
+    else
+      hipLaunchKernelGGL((prefill_pp_kernel<STREAM, OUT_F32, false>), dim3(grid), dim3(512), 0, s, a);
+    return hipGetLastError();
+  }
   if (a.append)
     hipLaunchKernelGGL((prefill_bf16_kernel<D, STREAM, OUT_F32, true>), dim3(grid), dim3(kWaves * kWave), 0, s, a);
   else
