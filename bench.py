@@ -65,7 +65,7 @@ def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--decode-steps", type=int, default=64)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-all-retrieval", action="store_true")
@@ -94,13 +94,12 @@ def copy_calibration():
 # 1 GiB copy (bench.py --copy-calibration), and the hash of the kernel sources
 # they were taken on: a source change makes the figure stale and it is dropped.
 TRAFFIC = {
-    "source_hash": "81cb6a92dcdd2413",
-    "fetch_factor": 524301.2 / 1048576.0,   # FETCH_SIZE of a 1 GiB copy / 1 GiB
+    "source_hash": "04e9ba4852cf9caf",
+    "fetch_factor": 524302.5 / 1048576.0,   # FETCH_SIZE of a 1 GiB copy / 1 GiB
     "write_factor": 1048576.0 / 1048576.0,  # WRITE_SIZE of a 1 GiB copy / 1 GiB
-    "prefill_retrieval": {"fetch_kib": 966819.8, "write_kib": 114691.2},
-    "decode_split": {"fetch_kib": 1074770.4, "write_kib": 4829.9},
+    "prefill_retrieval": {"fetch_kib": 323998.1, "write_kib": 114691.3},
+    "decode_split": {"fetch_kib": 1074684.2, "write_kib": 4829.7},
 }
-
 
 def kernel_source_hash():
     import hashlib
@@ -289,7 +288,7 @@ def main():
             "frac_of_bf16_peak": round(flops_step / (prefill_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         },
         "roofline": {
-            "kernel": f"prefill_bf16_kernel<128,retrieval> ({gs * n_ret} q heads x {T} rows)",
+            "kernel": f"prefill_pp_kernel<retrieval> ({gs * n_ret} q heads x {T} rows, d_head 128)",
             "bound": "mfma", "achieved": round(ret_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
             "frac": round(ret_tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic_for("prefill_retrieval"),
             "algorithmic_per_launch": f"{flops_ret:.4e} FLOP", "avg_launch_ms": round(ret_ms, 4),
