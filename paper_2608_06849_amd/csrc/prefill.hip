@@ -661,20 +661,20 @@ constexpr int kWaitVm4 = 0x4 | (0x7 << 4) | (0xF << 8);
 constexpr int kWaitVm8 = 0x8 | (0x7 << 4) | (0xF << 8);
 constexpr int kWaitLgkm0 = 0xF | (0x7 << 4) | (0x0 << 8) | (0x3 << 14);
 
-template <bool STREAM, bool OUT_F32, bool APPEND>
-__global__ __launch_bounds__(512, 1) void prefill_pp_kernel(PrefillArgs a) {
-  __shared__ __align__(1024) PPStage lds[kPPStages];
-  constexpr int D = kPPD;
-  constexpr int kKSteps = D / 16;
-  constexpr int kMBlocks = D / 32;
 
+// Work item of a workgroup of the d_head-128 kernels: query block qb (rows
+// qb * rows ..), local query head qh_local of the launch's KV-head list and
+// sequence b.  Dense batches use the XCD-aware order below; packed batches
+// with sequence-major order walk cu_seqlens.  Returns false when the
+// workgroup has no work (past the last sequence's blocks).
+__device__ __forceinline__ bool pp_work_item(const PrefillArgs& a, int rows, int& qb, int& qh_local, int& b) {
   const int n_qh = a.n_kv * a.gs;
   const int per_block = n_qh * a.B;
   const int wg = blockIdx.x;
-  int qb = a.n_qblocks - 1 - wg / per_block;
+  qb = a.n_qblocks - 1 - wg / per_block;
   const int rem = wg % per_block;
-  int qh_local = rem % n_qh;
-  int b = rem / n_qh;
+  qh_local = rem % n_qh;
+  b = rem / n_qh;
 #if AOH_PP_XCD
   if (!a.seq_major) {
     // XCD-aware order.  Workgroups go to the 8 XCDs (each with its own L2)
@@ -708,7 +708,7 @@ __global__ __launch_bounds__(512, 1) void prefill_pp_kernel(PrefillArgs a) {
     for (int s2 = 0; s2 < a.B; ++s2) {
       const int s0 = min(max(a.cu_seqlens[s2], 0), a.total);
       const int s1 = min(max(a.cu_seqlens[s2 + 1], s0), a.total);
-      const int nb = (min(s1 - s0, a.T) + kPPRows - 1) / kPPRows;
+      const int nb = (min(s1 - s0, a.T) + rows - 1) / rows;
       if (unit < nb) {
         b = s2;
         qb = nb - 1 - unit;
@@ -716,8 +716,81 @@ __global__ __launch_bounds__(512, 1) void prefill_pp_kernel(PrefillArgs a) {
       }
       unit -= nb;
     }
-    if (b < 0) return;
+    if (b < 0) return false;
   }
+  return true;
+}
+
+// Fused append of one resident tile (keys kb .. kb+63) into the cache of the
+// launch: the paged cache (K token-major, V dimension-major per page; pages
+// outside the block table are skipped) or the ring (a position is kept only
+// if no later prompt position maps to its slot).  Threads tid, tid + nthr, ..
+// take the 16-byte chunks of the tile; crank = the KV head's rank in the cache.
+template <bool STREAM>
+__device__ __forceinline__ void pp_write_tile(const PrefillArgs& a, const PPStage& st, int kb, int b, int crank,
+                                              int T, int tid, int nthr) {
+  constexpr int D = kPPD;
+  constexpr int kCh = D / 8;
+  uint16_t* ck = static_cast<uint16_t*>(a.ck);
+  uint16_t* cv = static_cast<uint16_t*>(a.cv);
+  if (!STREAM) {
+    for (int e = tid; e < kBN * kCh; e += nthr) {
+      const int row = e / kCh, ch = e % kCh;
+      const int p = kb + row;
+      const int lp = p / kPageTokens;
+      if (p >= T || lp >= a.max_pages) continue;
+      const int page = a.block_table[(int64_t)b * a.max_pages + lp];
+      if (page < 0 || page >= a.num_pages) continue;
+      uint16_t* dst = ck + (((int64_t)page * a.n_cache + crank) * kPageTokens + p % kPageTokens) * D + 8 * ch;
+      st16(dst, *reinterpret_cast<const u32x4*>(&st.k[pp_koff(row, ch)]));
+    }
+    for (int e = tid; e < (kBN / kPageTokens) * D * 2; e += nthr) {
+      const int pg = e / (2 * D), d = (e / 2) % D, hf = e % 2;
+      const int p0 = kb + kPageTokens * pg + 8 * hf;
+      const int lp = p0 / kPageTokens;
+      if (p0 >= T || lp >= a.max_pages) continue;
+      const int page = a.block_table[(int64_t)b * a.max_pages + lp];
+      if (page < 0 || page >= a.num_pages) continue;
+      uint16_t* dst = cv + (((int64_t)page * a.n_cache + crank) * D + d) * kPageTokens + 8 * hf;
+      const int row0 = kPageTokens * pg + 8 * hf;
+      const int dc = d >> 3, de = d & 7;
+      if (p0 + 8 <= T) {
+        u32x4 w;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          w[j] = (uint32_t)st.v[pp_voff(row0 + 2 * j, dc) + de] |
+                 ((uint32_t)st.v[pp_voff(row0 + 2 * j + 1, dc) + de] << 16);
+        st16(dst, w);
+      } else {
+        for (int j = 0; p0 + j < T; ++j) dst[j] = st.v[pp_voff(row0 + j, dc) + de];
+      }
+    }
+  } else {
+    for (int e = tid; e < kBN * kCh; e += nthr) {
+      const int row = e / kCh, ch = e % kCh;
+      const int p = kb + row;
+      if (p >= T || !(p < a.n_sink || p >= T - a.window)) continue;
+      const int slot = p < a.n_sink ? p : a.n_sink + (p - a.n_sink) % a.window;
+      const int64_t unit = ((int64_t)b * a.n_cache + crank) * a.ring_blocks + slot / kPageTokens;
+      const int r = slot % kPageTokens;
+      st16(ck + unit * (kPageTokens * D) + r * D + 8 * ch, *reinterpret_cast<const u32x4*>(&st.k[pp_koff(row, ch)]));
+      uint16_t* rv = cv + unit * (kPageTokens * D);
+      const int vo = pp_voff(row, ch);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) rv[(8 * ch + j) * kPageTokens + r] = st.v[vo + j];
+    }
+  }
+}
+
+template <bool STREAM, bool OUT_F32, bool APPEND>
+__global__ __launch_bounds__(512, 1) void prefill_pp_kernel(PrefillArgs a) {
+  __shared__ __align__(1024) PPStage lds[kPPStages];
+  constexpr int D = kPPD;
+  constexpr int kKSteps = D / 16;
+  constexpr int kMBlocks = D / 32;
+
+  int qb, qh_local, b;
+  if (!pp_work_item(a, kPPRows, qb, qh_local, b)) return;
   const int g = a.kv_heads[qh_local / a.gs];
   const int h = g * a.gs + (qh_local % a.gs);
 
@@ -830,58 +903,7 @@ __global__ __launch_bounds__(512, 1) void prefill_pp_kernel(PrefillArgs a) {
   // tile.
   const bool writer = APPEND && (qh_local % a.gs) == 0;
   const int crank = qh_local / a.gs;
-  auto write_tile = [&](const PPStage& st, int kb) {
-    constexpr int kCh = D / 8;
-    uint16_t* ck = static_cast<uint16_t*>(a.ck);
-    uint16_t* cv = static_cast<uint16_t*>(a.cv);
-    if (!STREAM) {
-      for (int e = tid; e < kBN * kCh; e += 512) {
-        const int row = e / kCh, ch = e % kCh;
-        const int p = kb + row;
-        const int lp = p / kPageTokens;
-        if (p >= T || lp >= a.max_pages) continue;
-        const int page = a.block_table[(int64_t)b * a.max_pages + lp];
-        if (page < 0 || page >= a.num_pages) continue;
-        uint16_t* dst = ck + (((int64_t)page * a.n_cache + crank) * kPageTokens + p % kPageTokens) * D + 8 * ch;
-        st16(dst, *reinterpret_cast<const u32x4*>(&st.k[pp_koff(row, ch)]));
-      }
-      for (int e = tid; e < (kBN / kPageTokens) * D * 2; e += 512) {
-        const int pg = e / (2 * D), d = (e / 2) % D, hf = e % 2;
-        const int p0 = kb + kPageTokens * pg + 8 * hf;
-        const int lp = p0 / kPageTokens;
-        if (p0 >= T || lp >= a.max_pages) continue;
-        const int page = a.block_table[(int64_t)b * a.max_pages + lp];
-        if (page < 0 || page >= a.num_pages) continue;
-        uint16_t* dst = cv + (((int64_t)page * a.n_cache + crank) * D + d) * kPageTokens + 8 * hf;
-        const int row0 = kPageTokens * pg + 8 * hf;
-        const int dc = d >> 3, de = d & 7;
-        if (p0 + 8 <= T) {
-          u32x4 w;
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            w[j] = (uint32_t)st.v[pp_voff(row0 + 2 * j, dc) + de] |
-                   ((uint32_t)st.v[pp_voff(row0 + 2 * j + 1, dc) + de] << 16);
-          st16(dst, w);
-        } else {
-          for (int j = 0; p0 + j < T; ++j) dst[j] = st.v[pp_voff(row0 + j, dc) + de];
-        }
-      }
-    } else {
-      for (int e = tid; e < kBN * kCh; e += 512) {
-        const int row = e / kCh, ch = e % kCh;
-        const int p = kb + row;
-        if (p >= T || !(p < a.n_sink || p >= T - a.window)) continue;
-        const int slot = p < a.n_sink ? p : a.n_sink + (p - a.n_sink) % a.window;
-        const int64_t unit = ((int64_t)b * a.n_cache + crank) * a.ring_blocks + slot / kPageTokens;
-        const int r = slot % kPageTokens;
-        st16(ck + unit * (kPageTokens * D) + r * D + 8 * ch, *reinterpret_cast<const u32x4*>(&st.k[pp_koff(row, ch)]));
-        uint16_t* rv = cv + unit * (kPageTokens * D);
-        const int vo = pp_voff(row, ch);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) rv[(8 * ch + j) * kPageTokens + r] = st.v[vo + j];
-      }
-    }
-  };
+  auto write_tile = [&](const PPStage& st, int kb) { pp_write_tile<STREAM>(a, st, kb, b, crank, T, tid, 512); };
 
   // MFMA phase of tile t: O^T += V(t-1)^T P(t-1)^T, then S^T(t) = K(t) Q^T.
   int v_tile = 0;  // tile whose P^T is in pop
