@@ -833,17 +833,42 @@ __global__ __launch_bounds__(512, 1) void prefill_pp_kernel(PrefillArgs a) {
   // physical chunk L % 16 of row 4j + L / 16 and therefore fetches the
   // logical chunk that the swizzle puts there.  Rows past the sequence end
   // repeat its last row (those keys are masked for every query row).
+  // Per-lane element offsets of the two 4-row blocks this wave loads, relative
+  // to the tile's first key (full tiles), and the rows themselves (the ragged
+  // last tile clamps them).
+  int64_t dma_k[2], dma_v[2];
+  int dma_r[2];
+#pragma unroll
+  for (int jj = 0; jj < 2; ++jj) {
+    const int j = 2 * wave + jj;
+    const int r = 4 * j + (lane >> 4);
+    const int pc = lane & 15;
+    dma_r[jj] = r;
+    dma_k[jj] = (int64_t)r * a.k_st + 8 * (pc ^ (r & 15));
+    dma_v[jj] = (int64_t)r * a.v_st + 8 * (pc ^ (4 * (r & 3)));
+  }
   auto issue_tile = [&](int it) {
     const int kb = plan.tile(it) * kBN;
     PPStage& st = lds[it % kPPStages];
+    if (kb + kBN <= T) {
+      const uint16_t* kt = kp + (int64_t)kb * a.k_st;
+      const uint16_t* vt = vp + (int64_t)kb * a.v_st;
 #pragma unroll
-    for (int jj = 0; jj < 2; ++jj) {
-      const int j = 2 * wave + jj;
-      const int r = 4 * j + (lane >> 4);
-      const int pc = lane & 15;
-      const int64_t row = min(kb + r, T - 1);
-      lds_dma16(kp + row * a.k_st + 8 * (pc ^ (r & 15)), &st.k[4 * j * kPPD]);
-      lds_dma16(vp + row * a.v_st + 8 * (pc ^ (4 * (r & 3))), &st.v[4 * j * kPPD]);
+      for (int jj = 0; jj < 2; ++jj) {
+        const int j = 2 * wave + jj;
+        lds_dma16(kt + dma_k[jj], &st.k[4 * j * kPPD]);
+        lds_dma16(vt + dma_v[jj], &st.v[4 * j * kPPD]);
+      }
+    } else {
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        const int j = 2 * wave + jj;
+        const int r = dma_r[jj];
+        const int pc = lane & 15;
+        const int64_t row = min(kb + r, T - 1);
+        lds_dma16(kp + row * a.k_st + 8 * (pc ^ (r & 15)), &st.k[4 * j * kPPD]);
+        lds_dma16(vp + row * a.v_st + 8 * (pc ^ (4 * (r & 3))), &st.v[4 * j * kPPD]);
+      }
     }
   };
 
