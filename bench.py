@@ -94,12 +94,13 @@ def copy_calibration():
 # 1 GiB copy (bench.py --copy-calibration), and the hash of the kernel sources
 # they were taken on: a source change makes the figure stale and it is dropped.
 TRAFFIC = {
-    "source_hash": "04e9ba4852cf9caf",
-    "fetch_factor": 524302.5 / 1048576.0,   # FETCH_SIZE of a 1 GiB copy / 1 GiB
+    "source_hash": "15f9fd9a708aacb1",
+    "fetch_factor": 524301.1 / 1048576.0,   # FETCH_SIZE of a 1 GiB copy / 1 GiB
     "write_factor": 1048576.0 / 1048576.0,  # WRITE_SIZE of a 1 GiB copy / 1 GiB
-    "prefill_retrieval": {"fetch_kib": 323998.1, "write_kib": 114691.3},
-    "decode_split": {"fetch_kib": 1074684.2, "write_kib": 4829.7},
+    "prefill_retrieval": {"fetch_kib": 324443.2, "write_kib": 114688.0},
+    "decode_split": {"fetch_kib": 1074669.6, "write_kib": 4830.0},
 }
+
 
 def kernel_source_hash():
     import hashlib
