@@ -94,7 +94,7 @@ def copy_calibration():
 # 1 GiB copy (bench.py --copy-calibration), and the hash of the kernel sources
 # they were taken on: a source change makes the figure stale and it is dropped.
 TRAFFIC = {
-    "source_hash": "15f9fd9a708aacb1",
+    "source_hash": "dc08a6bb7f091bc7",
     "fetch_factor": 524301.1 / 1048576.0,   # FETCH_SIZE of a 1 GiB copy / 1 GiB
     "write_factor": 1048576.0 / 1048576.0,  # WRITE_SIZE of a 1 GiB copy / 1 GiB
     "prefill_retrieval": {"fetch_kib": 324443.2, "write_kib": 114688.0},
@@ -102,13 +102,24 @@ TRAFFIC = {
 }
 
 
-def kernel_source_hash():
+def kernel_source_hash(read=None):
+    """Hash of the kernel sources the traffic figures were measured on: their
+    code lines, with // comments and blank lines dropped (comments do not
+    change the kernels)."""
     import hashlib
+    import re
     root = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2608_06849_amd", "csrc")
     h = hashlib.sha256()
     for name in ("prefill.hip", "decode.hip", "aoh_device.h", "aoh_internal.h"):
-        with open(os.path.join(root, name), "rb") as f:
-            h.update(f.read())
+        if read is None:
+            with open(os.path.join(root, name), "rb") as f:
+                text = f.read().decode()
+        else:
+            text = read(name)
+        for line in text.splitlines():
+            code = re.sub(r"//.*$", "", line).rstrip()
+            if code.strip():
+                h.update(code.encode() + b"\n")
     return h.hexdigest()[:16]
 
 

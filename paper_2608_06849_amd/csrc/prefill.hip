@@ -8,9 +8,9 @@
 // with chunks of K tokens (the cache before a chunk keeps the sink and the
 // window most recent tokens; the chunk sees those and itself).
 //
-// bf16 kernel (the hot one).  One workgroup = 4 waves = 128 query rows of one
-// query head; each wave owns 32 rows.  Key/value tiles of 64 keys are staged
-// in LDS and shared by the 4 waves.  Per tile and wave:
+// bf16 kernels.  One workgroup = 8 waves = 256 query rows of one query head;
+// each wave owns 32 rows.  Key/value tiles of 64 keys are staged in LDS and
+// shared by the 8 waves.  Per tile and wave:
 //   S^T[64 keys x 32 rows] = K_tile . Q^T        (v_mfma_f32_32x32x16_bf16)
 //   online softmax in fp32, one query row per lane column, so the row max is a
 //   lane-local reduction plus one exchange with the partner lane (lane ^ 32)
@@ -21,6 +21,11 @@
 // Streaming heads iterate only over the sink tiles and the diagonal band of
 // tiles; other tiles are never loaded.  Tiles that are fully visible skip the
 // per-element mask.
+//   prefill_pp_kernel (d_head 128): direct global->LDS tile loads into a
+//     4-stage ring, swizzled LDS rows, two phase-shifted wave groups,
+//     XCD-aware workgroup order (see its own comment).
+//   prefill_bf16_kernel (d_head 64): register-staged, double-buffered, padded
+//     LDS tiles.
 //
 // fp32 kernel: a plain per-row kernel (one thread per query row) kept exact
 // for fp32 inputs; it has no performance role.
