@@ -234,6 +234,29 @@ aoh_status aoh_decode(const aoh_tensor* q, const aoh_paged_cache* kv_full,
                       void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Fused decode step (Sec. 5 decode stage, Eq. 8, with the cache policy of the
+ * same section): the result and the final caches equal those of
+ * aoh_kv_append of the step's token at start_pos = lens[b] - 1 followed by
+ * aoh_decode with the same lens, bit for bit.
+ *   k_new, v_new: [B][Hkv][D], dtype of q, the key / value of the token at
+ *   position lens[b] - 1; the other arguments as for aoh_decode (lens counts
+ *   the new token; the workspace is sized by aoh_decode_workspace_bytes).
+ * bf16: one launch fewer than the two calls; the decode wave that reads the
+ * token's page (ring block) writes the token there first.  This needs the
+ * page of position lens[b] - 1 to be referenced by no other block-table entry
+ * read in the call (pages are not shared across sequences at the write
+ * position), which paged serving guarantees by copy-on-write.  fp32: the two
+ * operations run as separate launches.
+ * Errors: as aoh_decode, plus AOH_ERR_INVALID_ARG for a null or misshapen
+ * k_new / v_new.
+ */
+aoh_status aoh_decode_step(const aoh_tensor* q, const aoh_tensor* k_new, const aoh_tensor* v_new,
+                           const aoh_paged_cache* kv_full, const aoh_ring_cache* kv_ring,
+                           const uint8_t* head_is_streaming, const int32_t* lens, int32_t n_sink,
+                           int32_t window, aoh_tensor* out, void* workspace, size_t workspace_bytes,
+                           void* stream);
+
+/*
  * ---------------------------------------------------------------- H2Share
  * AoH-guided cross-layer sparse attention (paper section "AoH-Guided Sparse
  * Attention: H2Share" and its Inference Phase; GQA appendix, group-level head

@@ -48,7 +48,7 @@ class AohRingCache(ctypes.Structure):
 
 _lib = None
 
-EXPORTS = ("aoh_prefill", "aoh_prefill_chunked", "aoh_prefill_append", "aoh_prefill_varlen", "aoh_kv_append", "aoh_decode_workspace_bytes", "aoh_decode",
+EXPORTS = ("aoh_prefill", "aoh_prefill_chunked", "aoh_prefill_append", "aoh_prefill_varlen", "aoh_kv_append", "aoh_decode_workspace_bytes", "aoh_decode", "aoh_decode_step",
            "aoh_classify_workspace_bytes", "aoh_classify", "aoh_retrieval_group_count",
            "aoh_head_mapping_workspace_bytes", "aoh_head_mapping", "aoh_decode_anchor_workspace_bytes",
            "aoh_decode_anchor", "aoh_decode_reuse_workspace_bytes", "aoh_decode_reuse",
@@ -89,6 +89,10 @@ def lib():
                                  ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, P(AohTensor),
                                  ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
         L.aoh_decode.restype = ctypes.c_int
+        L.aoh_decode_step.argtypes = [P(AohTensor), P(AohTensor), P(AohTensor), P(AohPagedCache), P(AohRingCache),
+                                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                      P(AohTensor), ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+        L.aoh_decode_step.restype = ctypes.c_int
         L.aoh_classify_workspace_bytes.argtypes = [ctypes.c_int32] * 4
         L.aoh_classify_workspace_bytes.restype = ctypes.c_size_t
         L.aoh_classify.argtypes = [P(AohTensor), P(AohTensor), ctypes.c_int32, ctypes.c_int32,
@@ -303,6 +307,25 @@ def aoh_decode(q, kv_full, kv_ring, head_is_streaming, lens, n_sink, window, out
                             ctypes.byref(rd) if rd else None, m.ptr,
                             _ptr(lens), n_sink, window, ctypes.byref(od), ctypes.c_void_p(ws_ptr),
                             ws_bytes, _stream(stream)))
+    return out
+
+
+def aoh_decode_step(q, k_new, v_new, kv_full, kv_ring, head_is_streaming, lens, n_sink, window, out=None,
+                    workspace=None, stream=None):
+    """Append the token at position lens[b]-1 (k_new, v_new [B,Hkv,D]) and decode
+    with it in one call: the same result and caches as aoh_kv_append + aoh_decode."""
+    if out is None:
+        out = torch.empty_like(q)
+    qd, kd, vd, od = tensor_desc(q), tensor_desc(k_new), tensor_desc(v_new), tensor_desc(out)
+    fd = kv_full.desc() if kv_full is not None else None
+    rd = kv_ring.desc() if kv_ring is not None else None
+    ws_ptr, ws_bytes = (workspace.data_ptr(), workspace.numel() * workspace.element_size()) \
+        if workspace is not None else (0, 0)
+    m = _Mask(head_is_streaming)
+    _check(lib().aoh_decode_step(ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd),
+                                 ctypes.byref(fd) if fd else None, ctypes.byref(rd) if rd else None, m.ptr,
+                                 _ptr(lens), n_sink, window, ctypes.byref(od), ctypes.c_void_p(ws_ptr),
+                                 ws_bytes, _stream(stream)))
     return out
 
 

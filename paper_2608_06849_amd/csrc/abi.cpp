@@ -447,6 +447,8 @@ struct DecodeExtra {
   const int32_t* sel_in = nullptr;  // reuse input [B][n_lists][top_k]
   int32_t n_lists = 0;
   const int32_t* mapping = nullptr;  // reuse: HOST [Hkv], list rank per retrieval group
+  const aoh_tensor* k_new = nullptr;  // fused step: token at lens - 1, [B][Hkv][D]
+  const aoh_tensor* v_new = nullptr;
 };
 
 static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_full, const aoh_ring_cache* kv_ring,
@@ -476,6 +478,15 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
   if ((st = check_ring(kv_ring, hs.n_str, n_sink, window))) return st;
   const int gs = (int)(Hq / Hkv);
   if (dt == AOH_BF16 && gs > 16) return fail(AOH_ERR_UNSUPPORTED, "Hq/Hkv=%d > 16", gs);
+  const bool step = x.k_new != nullptr;
+  if (step) {
+    if ((st = check_tensor(x.k_new, "k_new", 3, dt, dt))) return st;
+    if ((st = check_tensor(x.v_new, "v_new", 3, dt, dt))) return st;
+    for (const aoh_tensor* t : {x.k_new, x.v_new})
+      if (t->shape[0] != B || t->shape[1] != Hkv || t->shape[2] != D)
+        return fail(AOH_ERR_INVALID_ARG, "k_new / v_new must be [B=%lld][Hkv=%lld][D=%lld]", (long long)B,
+                    (long long)Hkv, (long long)D);
+  }
   if (x.mode != kPlain) {
     if (dt != AOH_BF16) return fail(AOH_ERR_UNSUPPORTED, "anchor/reuse decode needs bf16");
     if (x.top_k < 1 || x.top_k > (1 << 30)) return fail(AOH_ERR_INVALID_ARG, "top_k=%d must be >= 1", x.top_k);
@@ -531,6 +542,38 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
   }
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
 
+  if (step) {
+    a.k_new = x.k_new->data; a.v_new = x.v_new->data;
+    a.kn_sb = x.k_new->stride[0]; a.kn_sh = x.k_new->stride[1];
+    a.vn_sb = x.v_new->stride[0]; a.vn_sh = x.v_new->stride[1];
+    a.n_sink = n_sink; a.window = window;
+  }
+  if (step && dt == AOH_F32) {
+    // fp32 step: a separate append at position lens - 1 before the decode.
+    AppendArgs ap;
+    std::memset(&ap, 0, sizeof(ap));
+    ap.k_new = x.k_new->data; ap.v_new = x.v_new->data;
+    ap.k_sb = x.k_new->stride[0]; ap.k_st = 0; ap.k_sh = x.k_new->stride[1];
+    ap.v_sb = x.v_new->stride[0]; ap.v_st = 0; ap.v_sh = x.v_new->stride[1];
+    ap.start_pos = lens; ap.start_bias = -1;
+    ap.B = (int)B; ap.n_new = 1; ap.Hkv = (int)Hkv;
+    if (hs.n_ret) {
+      ap.pk = kv_full->k; ap.pv = kv_full->v; ap.block_table = kv_full->block_table;
+      ap.max_pages = kv_full->max_pages_per_seq; ap.num_pages = (int)kv_full->num_pages; ap.n_ret = hs.n_ret;
+    }
+    if (hs.n_str) {
+      ap.rk = kv_ring->k; ap.rv = kv_ring->v; ap.n_str = hs.n_str;
+      ap.ring_blocks = (int)ceil_div(kv_ring->capacity, kPageTokens);
+    }
+    ap.n_sink = n_sink; ap.window = window;
+    ap.n_chunks = 2;
+    ap.streaming_mask = hs.streaming_mask;
+    std::memcpy(ap.rank, hs.rank, sizeof(ap.rank));
+    if (B > 65535) return fail(AOH_ERR_UNSUPPORTED, "batch too large");
+    hipError_t e = launch_append(ap, dt, (int)D, s);
+    if (e != hipSuccess) return fail(AOH_ERR_HIP, "append launch: %s", hipGetErrorString(e));
+  }
+
   if (dt == AOH_F32) {
     // fp32: direct per-head kernel, no workspace.
     hipError_t e = launch_decode_f32(a, (int)D, out->data, out->stride[0], out->stride[1], s);
@@ -571,7 +614,7 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
   }
   if ((int64_t)a.full.n_items + a.ring.n_items >= (1ll << 31)) return fail(AOH_ERR_UNSUPPORTED, "grid too large");
   {
-    hipError_t e = launch_decode_split(a, (int)D, x.mode, s);
+    hipError_t e = launch_decode_split(a, (int)D, step ? 3 : x.mode, s);
     if (e != hipSuccess) return fail(AOH_ERR_HIP, "decode split launch: %s", hipGetErrorString(e));
   }
   MergeArgs m;
@@ -613,6 +656,19 @@ aoh_status aoh_decode(const aoh_tensor* q, const aoh_paged_cache* kv_full,
                       void* workspace, size_t workspace_bytes_given, void* stream) {
   return decode_impl(q, kv_full, kv_ring, head_is_streaming, lens, n_sink, window, out, workspace,
                      workspace_bytes_given, stream, DecodeExtra());
+}
+
+aoh_status aoh_decode_step(const aoh_tensor* q, const aoh_tensor* k_new, const aoh_tensor* v_new,
+                           const aoh_paged_cache* kv_full, const aoh_ring_cache* kv_ring,
+                           const uint8_t* head_is_streaming, const int32_t* lens, int32_t n_sink,
+                           int32_t window, aoh_tensor* out, void* workspace, size_t workspace_bytes_given,
+                           void* stream) {
+  if (!k_new) return fail(AOH_ERR_INVALID_ARG, "k_new: null descriptor");
+  if (!v_new) return fail(AOH_ERR_INVALID_ARG, "v_new: null descriptor");
+  DecodeExtra x;
+  x.k_new = k_new; x.v_new = v_new;
+  return decode_impl(q, kv_full, kv_ring, head_is_streaming, lens, n_sink, window, out, workspace,
+                     workspace_bytes_given, stream, x);
 }
 
 size_t aoh_decode_anchor_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t d_head,

@@ -90,6 +90,12 @@ struct DecodeArgs {
   const int32_t* sel;
   int32_t n_sel, n_lists;
   uint8_t sel_rank[kMaxKvHeads];
+  // Fused decode step: the key / value of the token at position lens - 1,
+  // [B][Hkv][D], written into its cache slot by the one wave that reads it.
+  const void* k_new;
+  const void* v_new;
+  int64_t kn_sb, kn_sh, vn_sb, vn_sh;
+  int32_t n_sink, window;
 };
 
 struct MergeArgs {
@@ -116,6 +122,7 @@ struct AppendArgs {
   int64_t k_sb, k_st, k_sh;
   int64_t v_sb, v_st, v_sh;
   const int32_t* start_pos;     // device [B]; nullptr: every sequence starts at 0
+  int32_t start_bias;           // added to start_pos[b] (-n_new: start_pos holds the end)
   int32_t B, n_new, Hkv;
   // paged cache
   void* pk;

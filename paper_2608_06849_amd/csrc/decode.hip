@@ -24,7 +24,7 @@
 
 namespace aoh {
 
-template <int D, bool RING, bool SCORES = false>
+template <int D, bool RING, bool SCORES = false, bool APPEND = false>
 __device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const CacheView& cv, int item) {
   constexpr int kKSteps = D / 32;   // 32-dim k-steps for Q K^T
   constexpr int kDimBlocks = D / 16;
@@ -114,6 +114,41 @@ __device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const Cac
   for (int nb = 0; nb < kDimBlocks; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY;
   float l_run = 0.f;
+
+  if (APPEND) {
+    // Fused step: position lens - 1 receives the new key / value (ring: its
+    // slot, sink positions kept, others modulo the window).  Its block lies in
+    // exactly one split, and only the wave of that split reads the unit (page
+    // or ring block) of this (sequence, KV head), so that wave stores the
+    // token, waits for the stores, then streams its range as usual.  A block
+    // beyond the table or an invalid page entry gets no write, as in a
+    // separate append.
+    const int p = len - 1;
+    if (p >= 0) {
+      const int slot = RING ? (p < a.n_sink ? p : a.n_sink + (p - a.n_sink) % a.window) : p;
+      const int blk = slot / kPage, row = slot % kPage;
+      if (blk >= blk0 && blk < blk_end) {
+        int64_t unit = -1;
+        if (RING) {
+          unit = ((int64_t)b * cv.n_kv + rank) * cv.ring_blocks + blk;
+        } else {
+          const int page = cv.block_table[(int64_t)b * cv.max_pages + blk];
+          if (page >= 0 && page < cv.num_pages) unit = (int64_t)page * cv.n_kv + rank;
+        }
+        if (unit >= 0) {
+          const uint16_t* kn = reinterpret_cast<const uint16_t*>(a.k_new) + (int64_t)b * a.kn_sb + (int64_t)g * a.kn_sh;
+          const uint16_t* vn = reinterpret_cast<const uint16_t*>(a.v_new) + (int64_t)b * a.vn_sb + (int64_t)g * a.vn_sh;
+          uint16_t* kdst = const_cast<uint16_t*>(kc) + unit * (kPage * D) + (int64_t)row * D;
+          uint16_t* vdst = const_cast<uint16_t*>(vc) + unit * (kPage * D) + row;
+          if (lane < D / 8) st16(kdst + 8 * lane, ld16(kn + 8 * lane));
+#pragma unroll
+          for (int i = 0; i < D / kWave; ++i) vdst[(int64_t)(lane + kWave * i) * kPage] = vn[lane + kWave * i];
+          // The stores must reach the cache before this wave's loads of it.
+          asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        }
+      }
+    }
+  }
 
   int ent[2];
   fetch_entries(blk0, ent);
@@ -363,15 +398,16 @@ __device__ __forceinline__ void decode_sparse_body(const DecodeArgs& a, const Ca
 
 // One launch for both cache types: paged-cache items first, ring items last.
 // MODE 0: plain decode; 1: anchor layer (paged items also keep their scores);
-// 2: reuse layer (paged items attend to borrowed positions only).
+// 2: reuse layer (paged items attend to borrowed positions only); 3: plain
+// decode that first stores the new token at position lens - 1 (fused step).
 template <int D, int MODE>
 __global__ __launch_bounds__(kWave) void decode_split_bf16_kernel(DecodeArgs a) {
   const int wg = blockIdx.x;
   if (wg < a.full.n_items) {
     if (MODE == 2) decode_sparse_body<D>(a, a.full, wg);
-    else decode_split_body<D, false, MODE == 1>(a, a.full, wg);
+    else decode_split_body<D, false, MODE == 1, MODE == 3>(a, a.full, wg);
   } else {
-    decode_split_body<D, true>(a, a.ring, wg - a.full.n_items);
+    decode_split_body<D, true, false, MODE == 3>(a, a.ring, wg - a.full.n_items);
   }
 }
 
@@ -543,6 +579,7 @@ template <int D>
 static void launch_split_d(const DecodeArgs& a, int mode, int grid, hipStream_t s) {
   if (mode == 1) hipLaunchKernelGGL((decode_split_bf16_kernel<D, 1>), dim3(grid), dim3(kWave), 0, s, a);
   else if (mode == 2) hipLaunchKernelGGL((decode_split_bf16_kernel<D, 2>), dim3(grid), dim3(kWave), 0, s, a);
+  else if (mode == 3) hipLaunchKernelGGL((decode_split_bf16_kernel<D, 3>), dim3(grid), dim3(kWave), 0, s, a);
   else hipLaunchKernelGGL((decode_split_bf16_kernel<D, 0>), dim3(grid), dim3(kWave), 0, s, a);
 }
 

@@ -25,7 +25,7 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
 
   const int g = blockIdx.y;
   const int b = blockIdx.z;
-  const int start = a.start_pos ? a.start_pos[b] : 0;
+  const int start = (a.start_pos ? a.start_pos[b] : 0) + a.start_bias;
   if (start < 0) return;  // invalid start position: write nothing
   const int end = start + a.n_new;
   const int lp = start / kPage + (int)blockIdx.x;

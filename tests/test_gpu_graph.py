@@ -11,7 +11,7 @@ import pytest
 import torch
 
 import synth
-from paper_2608_06849_amd import (PagedCache, RingCache, aoh_decode, aoh_decode_workspace_bytes,
+from paper_2608_06849_amd import (PagedCache, RingCache, aoh_decode, aoh_decode_step, aoh_decode_workspace_bytes,
                                   aoh_kv_append)
 from tests.helpers import bits
 
@@ -35,7 +35,8 @@ def _stack(n_layers, B, Hq, Hkv, D, L0, n_sink, window, seed):
     return layers, max_pages
 
 
-def test_graph_replay_matches_eager():
+@pytest.mark.parametrize("fused", [False, True])
+def test_graph_replay_matches_eager(fused):
     n_layers, B, Hq, Hkv, D, L0, n_sink, window, seed = 4, 2, 8, 4, 128, 3000, 16, 256, 11
     layers, max_pages = _stack(n_layers, B, Hq, Hkv, D, L0, n_sink, window, seed)
     ws = torch.empty(aoh_decode_workspace_bytes(B, Hq, D, max_pages, n_sink + window) // 4 + 4,
@@ -46,12 +47,17 @@ def test_graph_replay_matches_eager():
     lens_after = lens_before + 1
     outs = torch.empty((n_layers, B, Hq, D), dtype=BF, device=DEV)
 
-    def step():
+    def step(fused=False):
         for l, (mask, full, ring) in enumerate(layers):
-            aoh_kv_append(kn[l, 0], kn[l, 1], mask, lens_before, full, ring, n_sink, window)
-            aoh_decode(q[l], full, ring, mask, lens_after, n_sink, window, out=outs[l], workspace=ws)
+            if fused:
+                aoh_decode_step(q[l], kn[l, 0, :, 0], kn[l, 1, :, 0], full, ring, mask, lens_after, n_sink, window,
+                                out=outs[l], workspace=ws)
+            else:
+                aoh_kv_append(kn[l, 0], kn[l, 1], mask, lens_before, full, ring, n_sink, window)
+                aoh_decode(q[l], full, ring, mask, lens_after, n_sink, window, out=outs[l], workspace=ws)
 
-    # eager reference (appending the same token again is idempotent)
+    # eager reference: the two-call step (appending the same token again is
+    # idempotent); the captured step is the two-call or the fused one
     step()
     torch.cuda.synchronize()
     want = bits(outs)
@@ -60,12 +66,12 @@ def test_graph_replay_matches_eager():
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(s):
-        step()  # warm-up on the capture stream
+        step(fused)  # warm-up on the capture stream
     torch.cuda.current_stream().wait_stream(s)
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
-        step()
+        step(fused)
     for rep in range(4):
         outs.fill_(float("nan"))            # eager work between replays
         junk = torch.randn(1 << 20, device=DEV).sum()
