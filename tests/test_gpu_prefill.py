@@ -101,6 +101,35 @@ def test_zero_keys_average_visible_values():
         assert err < 1e-4, (n_sink, window, err)
 
 
+@pytest.mark.parametrize("T,n_sink,window", [(2048, 4, 600), (1500, 64, 1000), (777, 0, 300)])
+def test_score_spikes_far_from_the_diagonal(T, n_sink, window):
+    # Every query shares a direction u; a few keys far before the diagonal
+    # (and the first sink key) carry a large multiple of u, so their scores
+    # sit ~40 log2 units above the rest.  The running max a query block has
+    # when it reaches them (from its diagonal tiles) is far too low: the
+    # kernel must raise it and rescale what it has accumulated.  Retrieval
+    # and streaming heads, d_head 128, bf16 (Sec. 5 attention, oracle in fp64).
+    B, Hq, Hkv, D = 1, 4, 2, 128
+    rng_q = synth.gaussian((B, T, Hq, D), 31, "spike-q")
+    rng_k = synth.gaussian((B, T, Hkv, D), 31, "spike-k", scale=0.5)
+    rng_v = synth.gaussian((B, T, Hkv, D), 31, "spike-v")
+    u = np.zeros(D, dtype=np.float32)
+    u[::2] = 1.0 / np.sqrt(D / 2)
+    qn = rng_q + 10.0 * u
+    kn = rng_k.copy()
+    for p_ in (0, 5, 300, T // 2, T - 700):
+        if 0 <= p_ < T:
+            kn[:, p_] += 31.0 * u
+    q = to_dtype(qn, torch.bfloat16).to(DEV)
+    k = to_dtype(kn, torch.bfloat16).to(DEV)
+    v = to_dtype(rng_v, torch.bfloat16).to(DEV)
+    mask = [0, 1]
+    out = aoh_prefill(q, k, v, mask, n_sink, window, out=torch.empty((B, T, Hq, D), dtype=torch.float32, device=DEV))
+    torch.cuda.synchronize()
+    want = OA.prefill(f64(q), f64(k), f64(v), mask, n_sink, window)
+    assert_parity(out, want, torch.bfloat16, f"score spikes T={T}")
+
+
 def test_deterministic():
     q, k, v = _inputs(1, 777, 8, 2, 128, torch.bfloat16, seed=9)
     a = aoh_prefill(q, k, v, [0, 1], 4, 50)
