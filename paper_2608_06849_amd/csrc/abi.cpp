@@ -528,7 +528,8 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
     c.max_pages = kv_full->max_pages_per_seq; c.num_pages = (int)kv_full->num_pages;
     c.n_kv = hs.n_ret;
     c.split_blocks = sp.split_blocks_full; c.n_splits = sp.n_splits_full;
-    c.n_items = (int)(B * hs.n_ret * sp.n_splits_full);
+    c.n_groups = (int)ceil_div(sp.n_splits_full, kSplitWaves);
+    c.n_items = (int)(B * hs.n_ret * c.n_groups);
     std::memcpy(c.kv_heads, hs.ret, hs.n_ret);
   }
   if (hs.n_str) {
@@ -537,7 +538,8 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
     c.ring_blocks = sp.ring_blocks;
     c.n_kv = hs.n_str;
     c.split_blocks = sp.split_blocks_ring; c.n_splits = sp.n_splits_ring;
-    c.n_items = (int)(B * hs.n_str * sp.n_splits_ring);
+    c.n_groups = (int)ceil_div(sp.n_splits_ring, kSplitWaves);
+    c.n_items = (int)(B * hs.n_str * c.n_groups);
     std::memcpy(c.kv_heads, hs.str, hs.n_str);
   }
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
@@ -622,10 +624,11 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
   m.part_acc = part_acc; m.part_ml = part_ml; m.lens = lens;
   m.out = out->data; m.o_sb = out->stride[0]; m.o_sh = out->stride[1];
   m.B = (int)B; m.Hq = (int)Hq; m.gs = gs; m.max_splits = sp_bound.max_splits;
-  m.split_tokens_full = sp.split_blocks_full * kPageTokens;
-  m.split_tokens_ring = sp.split_blocks_ring * kPageTokens;
-  m.n_splits_full = sp.n_splits_full;
-  m.n_splits_ring = sp.n_splits_ring;
+  // One partial per split workgroup (kSplitWaves consecutive splits).
+  m.split_tokens_full = kSplitWaves * sp.split_blocks_full * kPageTokens;
+  m.split_tokens_ring = kSplitWaves * sp.split_blocks_ring * kPageTokens;
+  m.n_splits_full = a.full.n_groups;
+  m.n_splits_ring = a.ring.n_groups;
   // reuse: a retrieval head's "length" is its number of borrowed entries
   m.max_len = x.mode == kReuse ? x.top_k : max_pages * kPageTokens;
   m.ring_cap = ring_cap;

@@ -60,7 +60,8 @@ struct CacheView {
   int32_t n_kv;                 // KV heads of this type (= heads stored in the cache)
   int32_t split_blocks;         // 16-token blocks per split
   int32_t n_splits;             // splits per (batch, KV head)
-  int32_t n_items;              // B * n_kv * n_splits
+  int32_t n_groups;             // workgroups per (batch, KV head): ceil(n_splits / kSplitWaves)
+  int32_t n_items;              // workgroups of the launch: B * n_kv * n_groups
   uint8_t kv_heads[kMaxKvHeads];  // KV head ids; rank in the cache = index here
 };
 
@@ -106,10 +107,10 @@ struct MergeArgs {
   int64_t o_sb, o_sh;
   int32_t B, Hq, gs;
   int32_t max_splits;
-  int32_t split_tokens_full;    // tokens per split, paged cache
-  int32_t split_tokens_ring;    // tokens per split, ring
-  int32_t n_splits_full;        // splits written per (b, head), paged cache
-  int32_t n_splits_ring;        // splits written per (b, head), ring
+  int32_t split_tokens_full;    // tokens per partial (split workgroup), paged cache
+  int32_t split_tokens_ring;    // tokens per partial (split workgroup), ring
+  int32_t n_splits_full;        // partials written per (b, head), paged cache
+  int32_t n_splits_ring;        // partials written per (b, head), ring
   int32_t max_len;              // 16 * pages per sequence: lens are clamped to it
   int32_t ring_cap;
   uint64_t streaming_mask;      // bit g set = KV head g streaming
@@ -207,6 +208,9 @@ hipError_t launch_similarity(const SimilarityArgs& a, int d, hipStream_t s);
 
 // Largest number of splits per (sequence, head) the merge pass accepts.
 constexpr int kMaxSplits = 1024;
+// Decode split pass: waves per workgroup, one split each; the workgroup merges
+// its waves' partial results in LDS and writes one partial per group.
+constexpr int kSplitWaves = 4;
 
 // Query rows per bf16 prefill workgroup, and 32-row MFMA blocks per wave
 // (the workgroup has kPrefillRows / (32 * kPrefillRB) waves).

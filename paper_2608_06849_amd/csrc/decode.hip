@@ -4,7 +4,8 @@
 //   pass 1 (decode_split): one wave per (sequence, KV head, split of the
 //     cache).  The wave reads the split's K/V once for the whole GQA group and
 //     keeps fp32 partial results (running max m, sum l, unnormalised acc[D])
-//     for every query head of the group.
+//     for every query head of the group.  Four consecutive splits share a
+//     workgroup, which merges their partials in LDS and writes one.
 //   pass 2 (decode_merge): per (sequence, query head), log-sum-exp merge of
 //     the partials of the splits that hold tokens, normalise, store in the
 //     caller's head order.
@@ -24,17 +25,17 @@
 
 namespace aoh {
 
+// One split of the cache of (sequence b, KV head kvl) for one wave; its
+// partial results (unnormalised acc, running max m in log2 units, sum l) are
+// left in acc / m_out / l_out (unchanged when the split holds no token).
 template <int D, bool RING, bool SCORES = false, bool APPEND = false>
-__device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const CacheView& cv, int item) {
+__device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const CacheView& cv, int b, int kvl,
+                                                  int split, f32x4 (&acc)[D / 16], float& m_out, float& l_out) {
   constexpr int kKSteps = D / 32;   // 32-dim k-steps for Q K^T
   constexpr int kDimBlocks = D / 16;
-  const int split = item % cv.n_splits;
-  const int rest = item / cv.n_splits;
-  const int kvl = rest % cv.n_kv;
-  const int b = rest / cv.n_kv;
   const int g = cv.kv_heads[kvl];
   const int rank = kvl;
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & (kWave - 1);
   const int col = lane & 15;   // query head within the group (MFMA column)
   const int G = lane >> 4;     // lane group
 
@@ -109,9 +110,6 @@ __device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const Cac
       vreg[nb] = ld16_stream(vc + vb + (int64_t)(16 * nb + (lane & 15)) * kPage + v_off);
   };
 
-  f32x4 acc[kDimBlocks];
-#pragma unroll
-  for (int nb = 0; nb < kDimBlocks; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY;
   float l_run = 0.f;
 
@@ -238,17 +236,8 @@ __device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const Cac
   // Partial results of this split: m (log2 units), l, acc[D] for each head.
   float l_tot = wave_xor_sum(l_run, 16);
   l_tot = wave_xor_sum(l_tot, 32);
-  if (head_ok) {
-    const int64_t slot = ((int64_t)b * a.Hq + hq) * a.max_splits + split;
-    float* pa = a.part_acc + slot * D;
-#pragma unroll
-    for (int nb = 0; nb < kDimBlocks; ++nb)
-      *reinterpret_cast<f32x4*>(pa + 16 * nb + 4 * G) = acc[nb];
-    if (G == 0) {
-      a.part_ml[slot * 2 + 0] = m_run;
-      a.part_ml[slot * 2 + 1] = l_tot;
-    }
-  }
+  m_out = m_run;
+  l_out = l_tot;
 }
 
 
@@ -260,15 +249,12 @@ __device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const Cac
 // general on 8 different pages).  List entries < 0 or beyond the sequence
 // are masked out.
 template <int D>
-__device__ __forceinline__ void decode_sparse_body(const DecodeArgs& a, const CacheView& cv, int item) {
+__device__ __forceinline__ void decode_sparse_body(const DecodeArgs& a, const CacheView& cv, int b, int kvl,
+                                                   int split, f32x4 (&acc)[D / 16], float& m_out, float& l_out) {
   constexpr int kKSteps = D / 32;
   constexpr int kDimBlocks = D / 16;
-  const int split = item % cv.n_splits;
-  const int rest = item / cv.n_splits;
-  const int kvl = rest % cv.n_kv;
-  const int b = rest / cv.n_kv;
   const int g = cv.kv_heads[kvl];
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & (kWave - 1);
   const int col = lane & 15;
   const int G = lane >> 4;
   const int len = a.lens[b];
@@ -303,9 +289,6 @@ __device__ __forceinline__ void decode_sparse_body(const DecodeArgs& a, const Ca
   const int m = lane & 15;
   const int slot_k0 = 8 * (m >> 2) + (m & 3);  // chunk slot of MFMA row m, token block 0 (+4 for block 1)
 
-  f32x4 acc[kDimBlocks];
-#pragma unroll
-  for (int nb = 0; nb < kDimBlocks; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY;
   float l_run = 0.f;
 
@@ -383,31 +366,88 @@ __device__ __forceinline__ void decode_sparse_body(const DecodeArgs& a, const Ca
 
   float l_tot = wave_xor_sum(l_run, 16);
   l_tot = wave_xor_sum(l_tot, 32);
-  if (head_ok) {
-    const int64_t slot = ((int64_t)b * a.Hq + hq) * a.max_splits + split;
-    float* pa = a.part_acc + slot * D;
-#pragma unroll
-    for (int nb = 0; nb < kDimBlocks; ++nb)
-      *reinterpret_cast<f32x4*>(pa + 16 * nb + 4 * G) = acc[nb];
-    if (G == 0) {
-      a.part_ml[slot * 2 + 0] = m_run;
-      a.part_ml[slot * 2 + 1] = l_tot;
-    }
-  }
+  m_out = m_run;
+  l_out = l_tot;
 }
 
 // One launch for both cache types: paged-cache items first, ring items last.
 // MODE 0: plain decode; 1: anchor layer (paged items also keep their scores);
 // 2: reuse layer (paged items attend to borrowed positions only); 3: plain
 // decode that first stores the new token at position lens - 1 (fused step).
+// A workgroup holds kSplitWaves consecutive splits of one (sequence, KV
+// head), one per wave; the waves' partials are merged in LDS (log-sum-exp
+// weights, as in the merge pass) and the group writes one partial, so the
+// merge pass reads kSplitWaves times fewer.  Each wave then combines a share
+// of the dimension blocks.
 template <int D, int MODE>
-__global__ __launch_bounds__(kWave) void decode_split_bf16_kernel(DecodeArgs a) {
-  const int wg = blockIdx.x;
-  if (wg < a.full.n_items) {
-    if (MODE == 2) decode_sparse_body<D>(a, a.full, wg);
-    else decode_split_body<D, false, MODE == 1, MODE == 3>(a, a.full, wg);
-  } else {
-    decode_split_body<D, true, false, MODE == 3>(a, a.ring, wg - a.full.n_items);
+__global__ __launch_bounds__(kSplitWaves * kWave, 2) void decode_split_bf16_kernel(DecodeArgs a) {
+  constexpr int kDimBlocks = D / 16;
+  static_assert(kDimBlocks % kSplitWaves == 0, "dimension blocks split evenly over the waves");
+  __shared__ f32x4 s_acc[kSplitWaves][kDimBlocks][kWave];
+  __shared__ float s_m[kSplitWaves][kWave];
+  __shared__ float s_l[kSplitWaves][kWave];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & (kWave - 1);
+  int wg = blockIdx.x;
+  const bool ring = wg >= a.full.n_items;
+  if (ring) wg -= a.full.n_items;
+  const CacheView& cv = ring ? a.ring : a.full;
+  const int sg = wg % cv.n_groups;
+  const int rest = wg / cv.n_groups;
+  const int kvl = rest % cv.n_kv;
+  const int b = rest / cv.n_kv;
+  const int split = sg * kSplitWaves + wave;
+
+  f32x4 acc[kDimBlocks];
+#pragma unroll
+  for (int nb = 0; nb < kDimBlocks; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m = -INFINITY, l = 0.f;
+  if (split < cv.n_splits) {
+    if (ring) decode_split_body<D, true, false, MODE == 3>(a, a.ring, b, kvl, split, acc, m, l);
+    else if (MODE == 2) decode_sparse_body<D>(a, a.full, b, kvl, split, acc, m, l);
+    else decode_split_body<D, false, MODE == 1, MODE == 3>(a, a.full, b, kvl, split, acc, m, l);
+  }
+#pragma unroll
+  for (int nb = 0; nb < kDimBlocks; ++nb) s_acc[wave][nb][lane] = acc[nb];
+  s_m[wave][lane] = m;
+  s_l[wave][lane] = l;
+  __syncthreads();
+
+  // Lane (col, G) holds query head col of the group; the four lane groups of
+  // a column carry the same m and l.  A wave without tokens has m = -inf and
+  // weight 0; a group without tokens (never read by the merge) writes m = -inf.
+  float M = -INFINITY;
+#pragma unroll
+  for (int w = 0; w < kSplitWaves; ++w) M = fmaxf(M, s_m[w][lane]);
+  float wt[kSplitWaves];
+  float L = 0.f;
+#pragma unroll
+  for (int w = 0; w < kSplitWaves; ++w) {
+    const float mw = s_m[w][lane];
+    wt[w] = (mw == -INFINITY) ? 0.f : fast_exp2(mw - M);
+    L += wt[w] * s_l[w][lane];
+  }
+  const int col = lane & 15, G = lane >> 4;
+  if (col < a.gs) {
+    const int hq = cv.kv_heads[kvl] * a.gs + col;
+    const int64_t slot = ((int64_t)b * a.Hq + hq) * a.max_splits + sg;
+    float* pa = a.part_acc + slot * D;
+#pragma unroll
+    for (int k = 0; k < kDimBlocks / kSplitWaves; ++k) {
+      const int nb = wave * (kDimBlocks / kSplitWaves) + k;
+      f32x4 o = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int w = 0; w < kSplitWaves; ++w) {
+        const f32x4 x = s_acc[w][nb][lane];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[i] += wt[w] * x[i];
+      }
+      *reinterpret_cast<f32x4*>(pa + 16 * nb + 4 * G) = o;
+    }
+    if (wave == 0 && G == 0) {
+      a.part_ml[slot * 2 + 0] = M;
+      a.part_ml[slot * 2 + 1] = L;
+    }
   }
 }
 
@@ -577,10 +617,11 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(MergeArgs a
 
 template <int D>
 static void launch_split_d(const DecodeArgs& a, int mode, int grid, hipStream_t s) {
-  if (mode == 1) hipLaunchKernelGGL((decode_split_bf16_kernel<D, 1>), dim3(grid), dim3(kWave), 0, s, a);
-  else if (mode == 2) hipLaunchKernelGGL((decode_split_bf16_kernel<D, 2>), dim3(grid), dim3(kWave), 0, s, a);
-  else if (mode == 3) hipLaunchKernelGGL((decode_split_bf16_kernel<D, 3>), dim3(grid), dim3(kWave), 0, s, a);
-  else hipLaunchKernelGGL((decode_split_bf16_kernel<D, 0>), dim3(grid), dim3(kWave), 0, s, a);
+  const dim3 blk(kSplitWaves * kWave);
+  if (mode == 1) hipLaunchKernelGGL((decode_split_bf16_kernel<D, 1>), dim3(grid), blk, 0, s, a);
+  else if (mode == 2) hipLaunchKernelGGL((decode_split_bf16_kernel<D, 2>), dim3(grid), blk, 0, s, a);
+  else if (mode == 3) hipLaunchKernelGGL((decode_split_bf16_kernel<D, 3>), dim3(grid), blk, 0, s, a);
+  else hipLaunchKernelGGL((decode_split_bf16_kernel<D, 0>), dim3(grid), blk, 0, s, a);
 }
 
 hipError_t launch_decode_split(const DecodeArgs& a, int d, int mode, hipStream_t s) {
