@@ -94,11 +94,11 @@ def copy_calibration():
 # 1 GiB copy (bench.py --copy-calibration), and the hash of the kernel sources
 # they were taken on: a source change makes the figure stale and it is dropped.
 TRAFFIC = {
-    "source_hash": "dc08a6bb7f091bc7",
-    "fetch_factor": 524301.1 / 1048576.0,   # FETCH_SIZE of a 1 GiB copy / 1 GiB
+    "source_hash": "740746be3111d241",
+    "fetch_factor": 524302.3 / 1048576.0,   # FETCH_SIZE of a 1 GiB copy / 1 GiB
     "write_factor": 1048576.0 / 1048576.0,  # WRITE_SIZE of a 1 GiB copy / 1 GiB
-    "prefill_retrieval": {"fetch_kib": 324443.2, "write_kib": 114688.0},
-    "decode_split": {"fetch_kib": 1074669.6, "write_kib": 4830.0},
+    "prefill_retrieval": {"fetch_kib": 325373.4, "write_kib": 114688.0},
+    "decode_split": {"fetch_kib": 1077962.3, "write_kib": 1224.1},
 }
 
 
@@ -260,6 +260,7 @@ def main():
     if not args.no_stack_decode:
         stack = stack_decode_leg(args, torch, synth, PagedCache, RingCache, aoh_decode, aoh_decode_workspace_bytes,
                                  aoh_kv_append, decode_bytes)
+        stack["prefill"] = stack_prefill_leg(torch, synth, PagedCache, RingCache)
 
     cls = None
     if not args.no_classify:
@@ -565,6 +566,64 @@ def stack_decode_leg(args, torch, synth, PagedCache, RingCache, aoh_decode, aoh_
     }
     log(f"stack decode: eager {eager_ms:.3f} ms/step, graph {graph_ms:.3f} ms/step ({graph_two_ms:.3f} as two calls), "
         f"{res['kv_gbps_graph']:.0f} GB/s with the graph")
+    return res
+
+
+def stack_prefill_leg(torch, synth, PagedCache, RingCache):
+    """One layer of the 28-layer stack's 262144-token prefill (28 query / 4 KV
+    heads, d_head 128, bf16, the layer-0 choice of 2 streaming KV heads, n_sink
+    64, window 2048), filling the paged cache and the ring as in serving, timed
+    over three calls; the same kernels with every head retrieval for
+    comparison.  Inputs come from torch's seeded device generator (the cost
+    does not depend on the values); the 28-layer figure is 28 x this layer."""
+    from paper_2608_06849_amd import aoh_prefill_append
+    c = synth.CONFIGS["qwen25_stack_256k"]
+    L, T, Hq, Hkv, D, n_sink, window = c["layers"], c["seq"], c["hq"], c["hkv"], c["d"], c["n_sink"], c["window"]
+    dev, bf = "cuda", torch.bfloat16
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(c["seed"] + 1)
+    mask = synth.choose_streaming(Hkv, c["n_streaming"], c["seed"], "streaming", 0).tolist()
+    q = torch.randn((1, T, Hq, D), device=dev, generator=gen).to(bf)
+    k = (0.5 * torch.randn((1, T, Hkv, D), device=dev, generator=gen)).to(bf)
+    v = torch.randn((1, T, Hkv, D), device=dev, generator=gen).to(bf)
+    out = torch.empty_like(q)
+    max_pages = (T + 15) // 16
+    bt = torch.arange(max_pages, dtype=torch.int32)[None]
+    gs = Hq // Hkv
+
+    def timed(m, n=3):
+        full = PagedCache.allocate(max_pages, m.count(0), D, bf, bt)
+        ring = RingCache.allocate(1, m.count(1), n_sink, window, D, bf) if m.count(1) else None
+        aoh_prefill_append(q, k, v, m, n_sink, window, full, ring, out=out)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        ev[0].record()
+        for _ in range(n):
+            aoh_prefill_append(q, k, v, m, n_sink, window, full, ring, out=out)
+        ev[1].record()
+        torch.cuda.synchronize()
+        del full, ring
+        return ev[0].elapsed_time(ev[1]) / n
+
+    ms = timed(mask)
+    ms_all = timed([0] * Hkv)
+    fl = useful_prefill_flops(T, D, gs * mask.count(0), gs * mask.count(1), n_sink, window)
+    fl_all = useful_prefill_flops(T, D, gs * Hkv, 0, n_sink, window)
+    res = {
+        "workload": "one layer of the 28-layer Qwen2.5-7B-shaped stack: 262144-token prefill filling the caches, "
+                    f"28 q / 4 KV heads (streaming KV heads {[g for g in range(Hkv) if mask[g]]}), d_head 128, bf16, "
+                    "n_sink 64, window 2048",
+        "layer_ms": round(ms, 2),
+        "useful_tflop": round(fl / 1e12, 2),
+        "tflops": round(fl / (ms * 1e-3) / 1e12, 1),
+        "frac_of_bf16_peak": round(fl / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "all_retrieval_layer_ms": round(ms_all, 2),
+        "all_retrieval_tflops": round(fl_all / (ms_all * 1e-3) / 1e12, 1),
+        "speedup_vs_all_retrieval": round(ms_all / ms, 3),
+        "stack_prefill_s_extrapolated": round(L * ms / 1e3, 3),
+    }
+    log(f"stack prefill: {ms:.1f} ms per 262144-token layer ({res['tflops']:.0f} TFLOP/s useful), "
+        f"all-retrieval {ms_all:.1f} ms; 28 layers ~{L * ms / 1e3:.2f} s (extrapolated)")
     return res
 
 
