@@ -157,6 +157,39 @@ def test_decode_workspace_size_and_checks():
     assert st == A.AOH_ERR_UNSUPPORTED and "16" in A.aoh_last_error()
 
 
+def test_decode_step_validation():
+    # the fused step validates its new-token tensors on top of the decode checks
+    L = A.lib()
+    q, out = _t((2, 8, 128)), _t((2, 8, 128))
+    full = A.AohPagedCache(k=FAKE, v=FAKE, block_table=FAKE, num_pages=8, max_pages_per_seq=4, n_heads=1)
+    ring = A.AohRingCache(k=FAKE, v=FAKE, n_heads=1, capacity=4 + 32)
+    mask = ctypes.create_string_buffer(b"\x00\x01", 2)
+    need = A.aoh_decode_workspace_bytes(2, 8, 128, 4, 36)
+
+    def step(kn, vn, ws=need):
+        st = L.aoh_decode_step(ctypes.byref(q), ctypes.byref(kn) if kn is not None else None,
+                               ctypes.byref(vn) if vn is not None else None, ctypes.byref(full), ctypes.byref(ring),
+                               ctypes.cast(mask, ctypes.c_void_p), ctypes.c_void_p(FAKE), 4, 32, ctypes.byref(out),
+                               ctypes.c_void_p(FAKE), ws, None)
+        return st, A.aoh_last_error()
+
+    good = _t((2, 2, 128))
+    st, err = step(None, good)
+    assert st == A.AOH_ERR_INVALID_ARG and "k_new" in err
+    st, err = step(good, None)
+    assert st == A.AOH_ERR_INVALID_ARG and "v_new" in err
+    st, err = step(_t((2, 1, 2, 128)), _t((2, 1, 2, 128)))        # [B, 1, Hkv, D]: one dimension too many
+    assert st == A.AOH_ERR_INVALID_ARG and "dimensions" in err
+    st, err = step(_t((2, 3, 128)), _t((2, 3, 128)))              # Hkv 3, the caches hold 2 KV heads
+    assert st == A.AOH_ERR_INVALID_ARG and "k_new / v_new" in err
+    st, err = step(_t((2, 2, 128), A.AOH_F32), _t((2, 2, 128), A.AOH_F32))  # dtype of q required
+    assert st == A.AOH_ERR_UNSUPPORTED and "k_new" in err
+    st, err = step(good, _t((2, 2, 128), stride=[256, 128, 2]))   # last dimension not contiguous
+    assert st == A.AOH_ERR_INVALID_ARG and "contiguous" in err
+    st, err = step(good, good, need - 4)                          # workspace as for aoh_decode
+    assert st == A.AOH_ERR_WORKSPACE, err
+
+
 def test_append_validation():
     L = A.lib()
     k, v = _t((2, 5, 2, 128)), _t((2, 5, 2, 128))
