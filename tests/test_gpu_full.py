@@ -15,7 +15,7 @@ import torch
 import synth
 from oracle import attention as OA
 from oracle import cache_model as CM
-from paper_2608_06849_amd import (PagedCache, RingCache, aoh_decode, aoh_decode_workspace_bytes,
+from paper_2608_06849_amd import (PagedCache, RingCache, aoh_decode_step, aoh_decode_workspace_bytes,
                                   aoh_kv_append, aoh_prefill)
 from tests.helpers import assert_parity, bits, f64
 
@@ -67,9 +67,10 @@ def test_llama_decode_b8_128k():
                      dtype=torch.float32, device=DEV)
     outs = {}
     for s in range(steps):
-        lens = torch.full((B,), L0 + s, dtype=torch.int32, device=DEV)
-        aoh_kv_append(kv_steps[s, 0].to(DEV), kv_steps[s, 1].to(DEV), mask, lens, full, ring, n_sink, window)
-        out = aoh_decode(q_steps[s].to(DEV), full, ring, mask, lens + 1, n_sink, window, workspace=ws)
+        # one fused step (store the token at L0 + s, decode), as the benchmark runs it
+        lens = torch.full((B,), L0 + s + 1, dtype=torch.int32, device=DEV)
+        out = aoh_decode_step(q_steps[s].to(DEV), kv_steps[s, 0, :, 0].to(DEV), kv_steps[s, 1, :, 0].to(DEV), full,
+                              ring, mask, lens, n_sink, window, workspace=ws)
         if s in (0, steps - 1):
             outs[s] = out.cpu()
     torch.cuda.synchronize()
