@@ -94,11 +94,11 @@ def copy_calibration():
 # 1 GiB copy (bench.py --copy-calibration), and the hash of the kernel sources
 # they were taken on: a source change makes the figure stale and it is dropped.
 TRAFFIC = {
-    "source_hash": "740746be3111d241",
-    "fetch_factor": 524302.3 / 1048576.0,   # FETCH_SIZE of a 1 GiB copy / 1 GiB
+    "source_hash": "9108489038aaa09d",
+    "fetch_factor": 524301.2 / 1048576.0,   # FETCH_SIZE of a 1 GiB copy / 1 GiB
     "write_factor": 1048576.0 / 1048576.0,  # WRITE_SIZE of a 1 GiB copy / 1 GiB
-    "prefill_retrieval": {"fetch_kib": 325373.4, "write_kib": 114688.0},
-    "decode_split": {"fetch_kib": 1077962.3, "write_kib": 1224.1},
+    "prefill_retrieval": {"fetch_kib": 325257.7, "write_kib": 114688.0},
+    "decode_split": {"fetch_kib": 1078223.1, "write_kib": 1224.1},
 }
 
 
@@ -291,7 +291,7 @@ def main():
         "config": {
             "workload": "Qwen2.5-7B-shaped attention layer: prefill 32768 tokens, 28 q heads / 4 KV heads "
                         "(KV heads 1,3 streaming), d_head 128, n_sink 64, window 1024; step = schedule + "
-                        "prefill writing the caches (2 launches) + 1 decode step",
+                        "prefill writing the caches (one launch for both head types) + 1 decode step",
             "global_batch": 1, "seq_len": T, "parallelism": "none (1 GPU)",
         },
         "prefill": {

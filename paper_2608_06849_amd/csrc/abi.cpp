@@ -246,30 +246,43 @@ static aoh_status prefill_impl(const aoh_tensor* q, const aoh_tensor* k, const a
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   // The bf16 kernel writes the caches itself; the fp32 path appends after.
   const bool fused = append && dt == AOH_BF16;
-  // Retrieval launch first: its causal work dominates (O(T^2) vs O(T(n_sink+window))).
+  // Per-type arguments: the retrieval heads (and the paged cache), the
+  // streaming heads (and the ring).
+  PrefillArgs ar = a, as = a;
   if (hs.n_ret) {
-    a.n_kv = hs.n_ret;
-    std::memcpy(a.kv_heads, hs.ret, hs.n_ret);
+    ar.n_kv = hs.n_ret;
+    std::memcpy(ar.kv_heads, hs.ret, hs.n_ret);
     if (fused) {
-      a.append = 1;
-      a.ck = kv_full->k; a.cv = kv_full->v; a.block_table = kv_full->block_table;
-      a.max_pages = kv_full->max_pages_per_seq; a.num_pages = (int)kv_full->num_pages;
-      a.n_cache = hs.n_ret; a.ring_blocks = 0;
+      ar.append = 1;
+      ar.ck = kv_full->k; ar.cv = kv_full->v; ar.block_table = kv_full->block_table;
+      ar.max_pages = kv_full->max_pages_per_seq; ar.num_pages = (int)kv_full->num_pages;
+      ar.n_cache = hs.n_ret; ar.ring_blocks = 0;
     }
-    hipError_t e = launch_prefill(a, dt, out_f32, (int)D, false, s);
-    if (e != hipSuccess) return fail(AOH_ERR_HIP, "prefill retrieval launch: %s", hipGetErrorString(e));
   }
   if (hs.n_str) {
-    a.n_kv = hs.n_str;
-    std::memcpy(a.kv_heads, hs.str, hs.n_str);
+    as.n_kv = hs.n_str;
+    std::memcpy(as.kv_heads, hs.str, hs.n_str);
     if (fused) {
-      a.append = 1;
-      a.ck = kv_ring->k; a.cv = kv_ring->v; a.block_table = nullptr;
-      a.max_pages = 0; a.num_pages = 0;
-      a.n_cache = hs.n_str; a.ring_blocks = (int)ceil_div(kv_ring->capacity, kPageTokens);
+      as.append = 1;
+      as.ck = kv_ring->k; as.cv = kv_ring->v; as.block_table = nullptr;
+      as.max_pages = 0; as.num_pages = 0;
+      as.n_cache = hs.n_str; as.ring_blocks = (int)ceil_div(kv_ring->capacity, kPageTokens);
     }
-    hipError_t e = launch_prefill(a, dt, out_f32, (int)D, true, s);
-    if (e != hipSuccess) return fail(AOH_ERR_HIP, "prefill streaming launch: %s", hipGetErrorString(e));
+  }
+  if (hs.n_ret && hs.n_str && prefill_mixed_preferred(ar, dt, (int)D)) {
+    // One launch, retrieval items first: their causal work dominates
+    // (O(T^2) vs O(T(n_sink+window))); the streaming items fill the tail.
+    hipError_t e = launch_prefill_mixed(ar, as, out_f32, s);
+    if (e != hipSuccess) return fail(AOH_ERR_HIP, "prefill launch: %s", hipGetErrorString(e));
+  } else {
+    if (hs.n_ret) {
+      hipError_t e = launch_prefill(ar, dt, out_f32, (int)D, false, s);
+      if (e != hipSuccess) return fail(AOH_ERR_HIP, "prefill retrieval launch: %s", hipGetErrorString(e));
+    }
+    if (hs.n_str) {
+      hipError_t e = launch_prefill(as, dt, out_f32, (int)D, true, s);
+      if (e != hipSuccess) return fail(AOH_ERR_HIP, "prefill streaming launch: %s", hipGetErrorString(e));
+    }
   }
   if (append && !fused && packed)
     return fail(AOH_ERR_UNSUPPORTED, "packed prefill with cache append needs bf16");

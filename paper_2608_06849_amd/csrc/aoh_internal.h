@@ -163,6 +163,10 @@ struct ClassifyArgs {
 // Launchers (return the launch status; no synchronisation).
 hipError_t launch_prefill(const PrefillArgs& a, int dtype, int out_f32, int d, bool streaming,
                           hipStream_t s);
+// One launch for a layer with both head types (bf16, d_head 128, short
+// retrieval launches; see prefill.hip).
+bool prefill_mixed_preferred(const PrefillArgs& ar, int dtype, int d);
+hipError_t launch_prefill_mixed(const PrefillArgs& ar, const PrefillArgs& as, int out_f32, hipStream_t s);
 // mode: 0 plain, 1 anchor (also writes scores), 2 reuse (sparse paged items)
 hipError_t launch_decode_split(const DecodeArgs& a, int d, int mode, hipStream_t s);
 hipError_t launch_decode_merge(const MergeArgs& a, int dtype, int out_f32, int d, hipStream_t s);

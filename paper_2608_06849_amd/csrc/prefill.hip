@@ -23,7 +23,9 @@
 // per-element mask.
 //   prefill_pp_kernel (d_head 128): direct global->LDS tile loads into a
 //     4-stage ring, swizzled LDS rows, two phase-shifted wave groups,
-//     XCD-aware workgroup order (see its own comment).
+//     XCD-aware workgroup order (see its own comment).  A layer with both
+//     head types runs as one launch (prefill_pp_mixed_kernel): retrieval
+//     items first, streaming items after them.
 //   prefill_bf16_kernel (d_head 64): register-staged, double-buffered, padded
 //     LDS tiles.
 //
@@ -672,10 +674,10 @@ constexpr int kWaitLgkm0 = 0xF | (0x7 << 4) | (0x0 << 8) | (0x3 << 14);
 // sequence b.  Dense batches use the XCD-aware order below; packed batches
 // with sequence-major order walk cu_seqlens.  Returns false when the
 // workgroup has no work (past the last sequence's blocks).
-__device__ __forceinline__ bool pp_work_item(const PrefillArgs& a, int rows, int& qb, int& qh_local, int& b) {
+__device__ __forceinline__ bool pp_work_item(const PrefillArgs& a, int rows, int wg, int& qb, int& qh_local,
+                                             int& b) {
   const int n_qh = a.n_kv * a.gs;
   const int per_block = n_qh * a.B;
-  const int wg = blockIdx.x;
   qb = a.n_qblocks - 1 - wg / per_block;
   const int rem = wg % per_block;
   qh_local = rem % n_qh;
@@ -787,15 +789,16 @@ __device__ __forceinline__ void pp_write_tile(const PrefillArgs& a, const PPStag
   }
 }
 
+// One work item (workgroup index wg of its launch's item space) of the
+// d_head-128 kernel; lds = the kPPStages-stage ring of the workgroup.
 template <bool STREAM, bool OUT_F32, bool APPEND>
-__global__ __launch_bounds__(512, 1) void prefill_pp_kernel(PrefillArgs a) {
-  __shared__ __align__(1024) PPStage lds[kPPStages];
+__device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PPStage* lds) {
   constexpr int D = kPPD;
   constexpr int kKSteps = D / 16;
   constexpr int kMBlocks = D / 32;
 
   int qb, qh_local, b;
-  if (!pp_work_item(a, kPPRows, qb, qh_local, b)) return;
+  if (!pp_work_item(a, kPPRows, wg, qb, qh_local, b)) return;
   const int g = a.kv_heads[qh_local / a.gs];
   const int h = g * a.gs + (qh_local % a.gs);
 
@@ -1141,6 +1144,26 @@ __global__ __launch_bounds__(512, 1) void prefill_pp_kernel(PrefillArgs a) {
   }
 }
 
+template <bool STREAM, bool OUT_F32, bool APPEND>
+__global__ __launch_bounds__(512, 1) void prefill_pp_kernel(PrefillArgs a) {
+  __shared__ __align__(1024) PPStage lds[kPPStages];
+  prefill_pp_body<STREAM, OUT_F32, APPEND>(a, blockIdx.x, lds);
+}
+
+// Both head types of a layer in one launch: workgroups [0, n_ret) take the
+// retrieval items, [ret_pad, ret_pad + streaming items) the streaming ones
+// (ret_pad = n_ret rounded up to the 8 XCDs, so both item spaces keep their
+// XCD-aware order).  The light streaming items are dispatched last and fill
+// the CUs that the causal retrieval items leave idle at the end.
+template <bool OUT_F32, bool APPEND>
+__global__ __launch_bounds__(512, 1) void prefill_pp_mixed_kernel(PrefillArgs ar, PrefillArgs as, int n_ret,
+                                                                  int ret_pad) {
+  __shared__ __align__(1024) PPStage lds[kPPStages];
+  const int wg = blockIdx.x;
+  if (wg < n_ret) prefill_pp_body<false, OUT_F32, APPEND>(ar, wg, lds);
+  else if (wg >= ret_pad) prefill_pp_body<true, OUT_F32, APPEND>(as, wg - ret_pad, lds);
+}
+
 #ifndef AOH_PREFILL_PP
 #define AOH_PREFILL_PP 1
 #endif
@@ -1166,6 +1189,35 @@ template <int D, bool STREAM>
 static hipError_t launch_f32(const PrefillArgs& a, hipStream_t s) {
   const int grid = a.n_qblocks * a.n_kv * a.gs * a.B;
   hipLaunchKernelGGL((prefill_f32_kernel<D, STREAM>), dim3(grid), dim3(kPrefillRowsF32), 0, s, a);
+  return hipGetLastError();
+}
+
+// The mixed launch pays where the retrieval items fill only a few rounds of
+// the 256 CUs (one 512-thread workgroup per CU): their causal tail is then a
+// sizeable part of the launch.  Its retrieval path is compiled together with
+// the streaming one and runs ~1-2% slower per tile, so long launches keep two
+// kernels: measured on the 28/4-head d_head-128 layer, 1.6% faster at 32768
+// tokens (7 rounds), even at 65536, 0.5-1.7% slower from 131072 on.
+constexpr int kMixedMaxRetItems = 8 * 256;
+
+bool prefill_mixed_preferred(const PrefillArgs& ar, int dtype, int d) {
+  const int64_t n_ret = (int64_t)ar.n_qblocks * ar.n_kv * ar.gs * ar.B;
+  return AOH_PREFILL_PP && dtype == 0 && d == kPPD && n_ret <= kMixedMaxRetItems;
+}
+
+hipError_t launch_prefill_mixed(const PrefillArgs& ar, const PrefillArgs& as, int out_f32, hipStream_t s) {
+  const int n_ret = ar.n_qblocks * ar.n_kv * ar.gs * ar.B;
+  const int n_str = as.n_qblocks * as.n_kv * as.gs * as.B;
+  const int ret_pad = (n_ret + 7) / 8 * 8;
+  const dim3 grid(ret_pad + n_str), blk(512);
+  const bool app = ar.append;
+  if (out_f32) {
+    if (app) hipLaunchKernelGGL((prefill_pp_mixed_kernel<true, true>), grid, blk, 0, s, ar, as, n_ret, ret_pad);
+    else hipLaunchKernelGGL((prefill_pp_mixed_kernel<true, false>), grid, blk, 0, s, ar, as, n_ret, ret_pad);
+  } else {
+    if (app) hipLaunchKernelGGL((prefill_pp_mixed_kernel<false, true>), grid, blk, 0, s, ar, as, n_ret, ret_pad);
+    else hipLaunchKernelGGL((prefill_pp_mixed_kernel<false, false>), grid, blk, 0, s, ar, as, n_ret, ret_pad);
+  }
   return hipGetLastError();
 }
 
