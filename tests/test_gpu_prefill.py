@@ -175,3 +175,24 @@ def test_chunk_at_least_prompt_is_full_causal():
     b = aoh_prefill(q, k, v, [0, 0], 4, 32)
     torch.cuda.synchronize()
     assert np.array_equal(bits(a), bits(b))
+
+
+@pytest.mark.parametrize("B,T,Hq,Hkv,mask", [
+    (1, 513, 14, 2, [0, 1]),          # 21 retrieval items: the streaming items start after 3 idle pads
+    (2, 700, 8, 4, [1, 0, 0, 1]),
+    (1, 2000, 28, 4, [0, 1, 0, 1]),   # Qwen-shaped heads
+])
+def test_one_launch_equals_per_type_launches(B, T, Hq, Hkv, mask):
+    # A layer with both head types runs its prefill as one launch (retrieval
+    # items, then streaming items).  Each head's output must be bit-identical
+    # to a call holding only the heads of its type (Sec. 5 attention per head).
+    D, gs, n_sink, window = 128, Hq // Hkv, 4, 100
+    q, k, v = _inputs(B, T, Hq, Hkv, D, torch.bfloat16, seed=T + Hq)
+    out = aoh_prefill(q, k, v, mask, n_sink, window)
+    for typ in (0, 1):
+        qi = torch.tensor([h for h in range(Hq) if mask[h // gs] == typ], device=DEV)
+        ki = torch.tensor([g for g in range(Hkv) if mask[g] == typ], device=DEV)
+        one = aoh_prefill(q.index_select(2, qi).contiguous(), k.index_select(2, ki).contiguous(),
+                          v.index_select(2, ki).contiguous(), [typ] * len(ki), n_sink, window)
+        torch.cuda.synchronize()
+        assert np.array_equal(bits(one), bits(out.index_select(2, qi))), f"head type {typ}"
