@@ -14,7 +14,7 @@ Follows the paper's statement of the method:
     (Appendix "GQA Extension", group-level classification and weight
     reordering).
 
-Readings of points the paper leaves open (each also listed in the design doc):
+Readings of points the paper leaves open:
   * the recent window includes the current token: key j is in the window of
     query i when i - j < window, so a streaming query sees at most
     n_sink + window keys, the size of the streaming cache;

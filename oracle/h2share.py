@@ -24,7 +24,7 @@ What is computed
     layer's K/V at the positions borrowed from its mapped anchor group;
     streaming heads attend to sink + window as in any layer.
 
-Readings where the paper leaves room (also listed in the design doc):
+Readings where the paper leaves room:
   * a group's selection score for position j is the mean, over the group's
     query heads, of their attention probabilities p_hj for this step;
   * top-k ties go to the lower position; fewer than k positions (lens < k)
