@@ -56,6 +56,24 @@ def useful_prefill_flops(t, d, hq_ret, hq_str, n_sink, window):
     return 4 * d * (hq_ret * visible_pairs(t, False, n_sink, window) + hq_str * visible_pairs(t, True, n_sink, window))
 
 
+def computed_tile_flops(t, d, hq_ret, hq_str, n_sink, window, rows=256, bn=64, chunk=0):
+    """MFMA FLOPs the prefill kernel issues: 4 D per (row, key) pair of every
+    rows x bn tile a workgroup of `rows` query rows visits (the causal
+    diagonal and band-edge tiles count whole).  Retrieval blocks visit tiles
+    0 .. last; streaming blocks the sink tiles plus the band from the first
+    row's lowest visible key."""
+    per_tile = 4 * d * rows * bn
+    ret = st = 0
+    for i0 in range(0, t, rows):
+        last_tile = (min(i0 + rows, t) - 1) // bn
+        ret += last_tile + 1
+        lo = (i0 // chunk) * chunk - window if chunk else i0 - window + 1
+        band_first = max(0, lo) // bn
+        sink_tiles = min((n_sink + bn - 1) // bn, band_first)
+        st += sink_tiles + (last_tile - band_first + 1)
+    return per_tile * (hq_ret * ret + hq_str * st)
+
+
 def decode_bytes(lens, g_ret, g_str, d, elt, n_sink, window):
     """KV bytes a decode step must read: all retrieval tokens, live ring slots."""
     return sum((g_ret * n + g_str * min(n, n_sink + window)) * d * 2 * elt for n in lens)
@@ -183,6 +201,7 @@ def main():
 
     flops_step = useful_prefill_flops(T, D, gs * n_ret, gs * n_str, n_sink, window)
     flops_ret = useful_prefill_flops(T, D, gs * n_ret, 0, n_sink, window)
+    flops_tiles = computed_tile_flops(T, D, gs * n_ret, gs * n_str, n_sink, window)
 
     def step(m=mask, f=full, r=ring, ev=None):
         if ev is not None:
@@ -209,8 +228,9 @@ def main():
     step_ms = float(np.mean([e[0].elapsed_time(e[2]) for e in evs]))
     log(f"step {step_ms:.3f} ms (prefill {prefill_ms:.3f} ms), wall {wall * 1e3 / args.steps:.3f} ms/step")
 
-    # Dominant kernel: the retrieval prefill launch, timed alone with the same
-    # grid (the retrieval query heads and KV heads as their own tensors).
+    # The retrieval items alone, as their own launch with the same grid (the
+    # retrieval query heads and KV heads as their own tensors): context for
+    # the one-launch figure.
     ret_q = torch.tensor([h for h in range(Hq) if mask[h // gs] == 0], device=dev)
     ret_kv = torch.tensor([g for g in range(Hkv) if mask[g] == 0], device=dev)
     q_r = q.index_select(2, ret_q).contiguous()
@@ -300,11 +320,22 @@ def main():
             "tflops": round(flops_step / (prefill_ms * 1e-3) / 1e12, 2),
             "frac_of_bf16_peak": round(flops_step / (prefill_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         },
+        # The step's dominant kernel: its prefill launch (both head types in
+        # one launch that also fills the caches), timed by the events around
+        # that one launch on the stream it runs on, averaged over the timed steps.
         "roofline": {
-            "kernel": f"prefill_pp_kernel<retrieval> ({gs * n_ret} q heads x {T} rows, d_head 128)",
-            "bound": "mfma", "achieved": round(ret_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-            "frac": round(ret_tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic_for("prefill_retrieval"),
-            "algorithmic_per_launch": f"{flops_ret:.4e} FLOP", "avg_launch_ms": round(ret_ms, 4),
+            "kernel": f"prefill_pp_mixed_kernel<bf16 out, append> ({gs * n_ret} retrieval + {gs * n_str} streaming "
+                      f"q heads x {T} rows, d_head 128)",
+            "bound": "mfma", "achieved": round(flops_step / (prefill_ms * 1e-3) / 1e12, 2), "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(flops_step / (prefill_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "traffic": traffic_for("prefill_mixed"),
+            "algorithmic_per_launch": f"{flops_step:.4e} FLOP (4 D per visible pair)",
+            "avg_launch_ms": round(prefill_ms, 4),
+            "computed_tile_per_launch": f"{flops_tiles:.4e} FLOP (4 D x 256 rows x 64 keys per visited tile)",
+            "computed_tile_tflops": round(flops_tiles / (prefill_ms * 1e-3) / 1e12, 2),
+            "computed_tile_frac": round(flops_tiles / (prefill_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "retrieval_launch_alone": {"ms": round(ret_ms, 4), "tflops": round(ret_tflops, 2),
+                                       "frac": round(ret_tflops / PEAK_BF16_TFLOPS, 4)},
         },
         "all_retrieval": None if all_ret is None else {
             "step_ms": round(all_ret["step_ms"], 4), "prefill_ms": round(all_ret["prefill_ms"], 4),
@@ -552,6 +583,12 @@ def stack_decode_leg(args, torch, synth, PagedCache, RingCache, aoh_decode, aoh_
         one_step(fused=False)
     graph_two_ms = timed(g2.replay)
     by = L * decode_bytes([T + steps], Hkv - c["n_streaming"], c["n_streaming"], D, 2, n_sink, window)
+    # resident KV of the 28 layers' caches at the 262144-token prompt length
+    # (the allocations also hold the decode steps' pages), against every head
+    # keeping all T tokens
+    resident = sum((f.k.numel() + f.v.numel()) // max_pages * ((T + 15) // 16) + r.k.numel() + r.v.numel()
+                   for _, f, r in layers) * 2
+    resident_all = L * Hkv * T * D * 2 * 2
     res = {
         "workload": "decode step through 28 layers of the Qwen2.5-7B attention shape, batch 1, context 262144, "
                     "2 of 4 KV heads streaming per layer (n_sink 64, window 2048); per layer: append 1 token + decode "
@@ -563,6 +600,11 @@ def stack_decode_leg(args, torch, synth, PagedCache, RingCache, aoh_decode, aoh_
         "kv_gb_per_step": round(by / 1e9, 4),
         "kv_gbps_graph": round(by / (graph_ms * 1e-3) / 1e9, 1),
         "frac_of_hbm_peak_graph": round(by / (graph_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+        "kv_gbps_eager": round(by / (eager_ms * 1e-3) / 1e9, 1),
+        "frac_of_hbm_peak_eager": round(by / (eager_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+        "resident_kv_gb": round(resident / 1e9, 4),
+        "resident_kv_gb_all_retrieval": round(resident_all / 1e9, 4),
+        "resident_kv_saving": round(1 - resident / resident_all, 4),
     }
     log(f"stack decode: eager {eager_ms:.3f} ms/step, graph {graph_ms:.3f} ms/step ({graph_two_ms:.3f} as two calls), "
         f"{res['kv_gbps_graph']:.0f} GB/s with the graph")
@@ -670,6 +712,8 @@ def varlen_leg(args, torch, synth):
             ms = timed(lambda: aoh_prefill_varlen(q, k, v, cu, int(lens.max()), mask, n_sink, window, out=out))
             entry = {"streaming_pct": sp, "window": window, "ms": round(ms, 3),
                      "useful_tflop": round(fl / 1e12, 3), "tflops": round(fl / (ms * 1e-3) / 1e12, 1)}
+            entry["decode"] = varlen_decode(torch, q, k, v, cu, lens, mask, n_sink, window, hq, hkv, d,
+                                            c["decode_steps"])
             if sp == 50 and window == 4096:
                 def per_seq():
                     for b in range(len(lens)):
@@ -677,9 +721,50 @@ def varlen_leg(args, torch, synth):
                         aoh_prefill(q[sl][None], k[sl][None], v[sl][None], mask, n_sink, window, out=out[sl][None])
                 entry["per_sequence_calls_ms"] = round(timed(per_seq), 3)
             res["settings"].append(entry)
-            log(f"varlen {sp}% w{window}: {ms:.2f} ms, {entry['tflops']} TFLOP/s")
+            log(f"varlen {sp}% w{window}: {ms:.2f} ms, {entry['tflops']} TFLOP/s; decode "
+                f"{entry['decode']['ms_per_step']:.4f} ms/step, {entry['decode']['kv_gbps']:.0f} GB/s")
     del q, k, v, out
     return res
+
+
+def varlen_decode(torch, q, k, v, cu, lens, mask, n_sink, window, hq, hkv, d, steps):
+    """The sweep's decode: the packed prefill fills a paged cache and a ring
+    for the 16 sequences, then `steps` batched single-token steps (one
+    aoh_decode_step call each: store the token, decode) are timed."""
+    from paper_2608_06849_amd import (PagedCache, RingCache, aoh_decode_step, aoh_decode_workspace_bytes,
+                                      aoh_prefill_varlen)
+    B, bf, dev = len(lens), torch.bfloat16, "cuda"
+    n_ret, n_str = mask.count(0), mask.count(1)
+    max_pages = (int(lens.max()) + steps + 15) // 16
+    bt = torch.arange(B * max_pages, dtype=torch.int32).reshape(B, max_pages)
+    full = PagedCache.allocate(B * max_pages, n_ret, d, bf, bt) if n_ret else None
+    ring = RingCache.allocate(B, n_str, n_sink, window, d, bf) if n_str else None
+    out = torch.empty_like(q)
+    aoh_prefill_varlen(q, k, v, cu, int(lens.max()), mask, n_sink, window, kv_full=full, kv_ring=ring, out=out)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(4321)
+    qs = torch.randn((steps, B, hq, d), device=dev, generator=gen).to(bf)
+    kvs = torch.randn((steps, 2, B, hkv, d), device=dev, generator=gen).to(bf)
+    lens_dev = [torch.tensor(lens + s + 1, dtype=torch.int32, device=dev) for s in range(steps)]
+    ws = torch.empty(aoh_decode_workspace_bytes(B, hq, d, max_pages, n_sink + window), dtype=torch.uint8, device=dev)
+    o = torch.empty((B, hq, d), dtype=bf, device=dev)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    for s in range(steps):
+        aoh_decode_step(qs[s], kvs[s, 0], kvs[s, 1], full, ring, mask, lens_dev[s], n_sink, window, out=o,
+                        workspace=ws)
+    ev[1].record()
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1]) / steps
+    by = np.mean([decode_bytes([int(n) + s + 1 for n in lens], n_ret, n_str, d, 2, n_sink, window)
+                  for s in range(steps)])
+    resident = sum((c.k.numel() + c.v.numel()) for c in (full, ring) if c is not None) * 2
+    del full, ring, out, qs, kvs
+    return {"steps": steps, "ms_per_step": round(ms, 4), "tokens_per_s": round(B / (ms * 1e-3), 1),
+            "kv_gb_per_step": round(by / 1e9, 4), "kv_gbps": round(by / (ms * 1e-3) / 1e9, 1),
+            "frac_of_hbm_peak": round(by / (ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+            "allocated_kv_gb": round(resident / 1e9, 4)}
 
 
 def classify_leg(args, torch, synth):
@@ -737,6 +822,8 @@ def cpu_baseline(q, k, v, mask, n_sink, window, T, D, gs, target_s=15.0):
     from oracle import accounting as C
     from oracle import attention as OA
 
+    cores = len(os.sched_getaffinity(0))
+    limiter = threadpoolctl.threadpool_limits(limits=cores)
     qh = q.float().cpu().numpy().astype(np.float64)
     kh = k.float().cpu().numpy().astype(np.float64)
     vh = v.float().cpu().numpy().astype(np.float64)
@@ -751,16 +838,16 @@ def cpu_baseline(q, k, v, mask, n_sink, window, T, D, gs, target_s=15.0):
         if dt >= target_s / 3 or n_rows >= 4096:
             break
         n_rows = int(n_rows * max(2.0, target_s / max(dt, 1e-3) / 1.5))
+    limiter.restore_original_limits()
     flops = 0
     for g, st in enumerate(mask):
         per_row = sum(C.visible_pairs_row(int(i), bool(st), n_sink, window) for i in rows)
         flops += 4 * D * gs * per_row
-    info = threadpoolctl.threadpool_info()
-    threads = max([p.get("num_threads", 1) for p in info] + [1])
-    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
             "seconds": round(dt, 2),
             "sample": f"{len(rows)} query rows (mask boundaries + seeded random) x {q.shape[2]} heads of the "
-                      f"{T}-token prefill, float64 numpy; BLAS threads = cores"}
+                      f"{T}-token prefill, float64 numpy, BLAS threads limited to the {cores} cores this "
+                      "process may run on"}
 
 
 if __name__ == "__main__":

@@ -88,8 +88,10 @@ typedef struct {
  * (contiguous, dtype = the call's dtype):
  *   k: [num_pages][n_heads][16][D]   token-major inside a page
  *   v: [num_pages][n_heads][D][16]   dimension-major inside a page
- * block_table is a DEVICE int32 array [B][max_pages_per_seq]; the caller
- * allocates pages and fills it for every page a call touches.
+ * block_table is a DEVICE int32 array [n_seqs][max_pages_per_seq]; the caller
+ * allocates pages and fills it for every page a call touches.  A call with B
+ * sequences requires n_seqs >= B (AOH_ERR_INVALID_ARG otherwise), so no row
+ * outside the table is ever read.
  */
 typedef struct {
   void* k;
@@ -98,6 +100,7 @@ typedef struct {
   int64_t num_pages;
   int32_t max_pages_per_seq;
   int32_t n_heads;
+  int32_t n_seqs; /* rows of block_table */
 } aoh_paged_cache;
 
 /*
@@ -110,13 +113,15 @@ typedef struct {
  *   k: [B][n_heads][Cpad/16][16][D]
  *   v: [B][n_heads][Cpad/16][D][16]
  * After any sequence of appends each slot holds the token of greatest
- * position that maps to it.
+ * position that maps to it.  A call with B sequences requires batch >= B
+ * (AOH_ERR_INVALID_ARG otherwise), so no write leaves the ring.
  */
 typedef struct {
   void* k;
   void* v;
   int32_t n_heads;
   int32_t capacity;
+  int32_t batch; /* sequences the ring holds (its first dimension) */
 } aoh_ring_cache;
 
 /*

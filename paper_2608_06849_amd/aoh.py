@@ -38,12 +38,12 @@ class AohTensor(ctypes.Structure):
 class AohPagedCache(ctypes.Structure):
     _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("block_table", ctypes.c_void_p),
                 ("num_pages", ctypes.c_int64), ("max_pages_per_seq", ctypes.c_int32),
-                ("n_heads", ctypes.c_int32)]
+                ("n_heads", ctypes.c_int32), ("n_seqs", ctypes.c_int32)]
 
 
 class AohRingCache(ctypes.Structure):
     _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("n_heads", ctypes.c_int32),
-                ("capacity", ctypes.c_int32)]
+                ("capacity", ctypes.c_int32), ("batch", ctypes.c_int32)]
 
 
 _lib = None
@@ -194,6 +194,7 @@ class PagedCache:
         c.num_pages = self.k.shape[0]
         c.max_pages_per_seq = self.block_table.shape[1]
         c.n_heads = self.k.shape[1]
+        c.n_seqs = self.block_table.shape[0]
         return c
 
 
@@ -217,6 +218,7 @@ class RingCache:
         c.k, c.v = self.k.data_ptr(), self.v.data_ptr()
         c.n_heads = self.k.shape[1]
         c.capacity = self.capacity
+        c.batch = self.k.shape[0]
         return c
 
 

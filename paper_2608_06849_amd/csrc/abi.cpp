@@ -109,9 +109,7 @@ aoh_status check_mask_params(int n_sink, int window) {
 // The ring is cut the same way with ~kTargetWaves / 8 waves.  n_ret (retrieval
 // KV heads) may be unknown (workspace sizing): then the plan for n_ret = 1 is
 // used, which has the most splits and so bounds every real plan.
-#ifndef AOH_DECODE_TARGET_WAVES
-#define AOH_DECODE_TARGET_WAVES 2048
-#endif
+constexpr int kDecodeTargetWaves = 2048;
 struct SplitPlan {
   int split_blocks_full, n_splits_full;
   int split_blocks_ring, n_splits_ring;
@@ -121,7 +119,7 @@ struct SplitPlan {
 
 SplitPlan plan_splits(int batch, int max_pages, int ring_cap, int n_ret, int n_str) {
   SplitPlan p;
-  const int64_t per_head = std::max<int64_t>(1, (int64_t)AOH_DECODE_TARGET_WAVES / ((int64_t)batch * std::max(n_ret, 1)));
+  const int64_t per_head = std::max<int64_t>(1, (int64_t)kDecodeTargetWaves / ((int64_t)batch * std::max(n_ret, 1)));
   const int target_full = (int)std::min<int64_t>(per_head, kMaxSplits);
   int sb = (int)std::max<int64_t>(2, ceil_div(max_pages, target_full));
   sb += sb & 1;
@@ -129,7 +127,7 @@ SplitPlan plan_splits(int batch, int max_pages, int ring_cap, int n_ret, int n_s
   p.n_splits_full = (int)ceil_div(max_pages, sb);
   p.ring_blocks = (int)ceil_div(std::max(ring_cap, 1), kPageTokens);
   const int64_t per_head_ring =
-      std::max<int64_t>(1, (int64_t)(AOH_DECODE_TARGET_WAVES / 8) / ((int64_t)batch * std::max(n_str, 1)));
+      std::max<int64_t>(1, (int64_t)(kDecodeTargetWaves / 8) / ((int64_t)batch * std::max(n_str, 1)));
   const int target_ring = (int)std::min<int64_t>(per_head_ring, kMaxSplits);
   int sbr = (int)std::max<int64_t>(2, ceil_div(p.ring_blocks, target_ring));
   sbr += sbr & 1;
@@ -154,7 +152,7 @@ int32_t aoh_version(void) { return 100; }
 const char* aoh_last_error(void) { return g_err; }
 
 static aoh_status check_paged(const aoh_paged_cache* c, int n_ret, int64_t B);
-static aoh_status check_ring(const aoh_ring_cache* c, int n_str, int n_sink, int window);
+static aoh_status check_ring(const aoh_ring_cache* c, int n_str, int n_sink, int window, int64_t B);
 
 // Prefill; with append set, also writes the prompt's K/V (positions 0..T-1 of
 // every sequence) into kv_full / kv_ring.
@@ -214,8 +212,10 @@ static aoh_status prefill_impl(const aoh_tensor* q, const aoh_tensor* k, const a
   if (n_qblocks * Hq * B >= (1ll << 31)) return fail(AOH_ERR_UNSUPPORTED, "grid too large");
   if (append) {
     if ((st = check_paged(kv_full, hs.n_ret, B))) return st;
-    if ((st = check_ring(kv_ring, hs.n_str, n_sink, window))) return st;
+    if ((st = check_ring(kv_ring, hs.n_str, n_sink, window, B))) return st;
     if (B > 65535) return fail(AOH_ERR_UNSUPPORTED, "batch too large");
+    // fp32 prompts are appended by a separate launch, which has no packed form
+    if (packed && dt != AOH_BF16) return fail(AOH_ERR_UNSUPPORTED, "packed prefill with cache append needs bf16");
   }
 
   PrefillArgs a;
@@ -284,8 +284,6 @@ static aoh_status prefill_impl(const aoh_tensor* q, const aoh_tensor* k, const a
       if (e != hipSuccess) return fail(AOH_ERR_HIP, "prefill streaming launch: %s", hipGetErrorString(e));
     }
   }
-  if (append && !fused && packed)
-    return fail(AOH_ERR_UNSUPPORTED, "packed prefill with cache append needs bf16");
   if (append && !fused) {
     AppendArgs ap;
     std::memset(&ap, 0, sizeof(ap));
@@ -355,13 +353,15 @@ static aoh_status check_paged(const aoh_paged_cache* c, int n_ret, int64_t B) {
   if (c->num_pages < 1 || c->max_pages_per_seq < 1) return fail(AOH_ERR_INVALID_ARG, "kv_full: empty cache");
   if (c->num_pages > (1ll << 31) - 1) return fail(AOH_ERR_UNSUPPORTED, "kv_full: too many pages");
   if ((int64_t)c->max_pages_per_seq * kPageTokens > (1ll << 30)) return fail(AOH_ERR_UNSUPPORTED, "kv_full: too many pages per sequence");
+  if (c->n_seqs < B)
+    return fail(AOH_ERR_INVALID_ARG, "kv_full.n_seqs=%d: the block table has fewer rows than the %lld sequences",
+                c->n_seqs, (long long)B);
   if (reinterpret_cast<uintptr_t>(c->k) % 16 || reinterpret_cast<uintptr_t>(c->v) % 16)
     return fail(AOH_ERR_INVALID_ARG, "kv_full: cache pointers must be 16-byte aligned");
-  (void)B;
   return AOH_OK;
 }
 
-static aoh_status check_ring(const aoh_ring_cache* c, int n_str, int n_sink, int window) {
+static aoh_status check_ring(const aoh_ring_cache* c, int n_str, int n_sink, int window, int64_t B) {
   if (!n_str) return AOH_OK;
   if (!c) return fail(AOH_ERR_INVALID_ARG, "kv_ring is null but %d streaming heads exist", n_str);
   if (!c->k || !c->v) return fail(AOH_ERR_INVALID_ARG, "kv_ring: null pointer");
@@ -369,6 +369,9 @@ static aoh_status check_ring(const aoh_ring_cache* c, int n_str, int n_sink, int
     return fail(AOH_ERR_INVALID_ARG, "kv_ring.n_heads=%d but the mask has %d streaming heads", c->n_heads, n_str);
   if (c->capacity != n_sink + window)
     return fail(AOH_ERR_INVALID_ARG, "kv_ring.capacity=%d must equal n_sink + window = %d", c->capacity, n_sink + window);
+  if (c->batch < B)
+    return fail(AOH_ERR_INVALID_ARG, "kv_ring.batch=%d: the ring holds fewer than the %lld sequences", c->batch,
+                (long long)B);
   if (reinterpret_cast<uintptr_t>(c->k) % 16 || reinterpret_cast<uintptr_t>(c->v) % 16)
     return fail(AOH_ERR_INVALID_ARG, "kv_ring: cache pointers must be 16-byte aligned");
   return AOH_OK;
@@ -393,7 +396,7 @@ aoh_status aoh_kv_append(const aoh_tensor* k_new, const aoh_tensor* v_new,
   HeadSchedule hs;
   if ((st = schedule_heads(head_is_streaming, (int)Hkv, &hs))) return st;
   if ((st = check_paged(kv_full, hs.n_ret, B))) return st;
-  if ((st = check_ring(kv_ring, hs.n_str, n_sink, window))) return st;
+  if ((st = check_ring(kv_ring, hs.n_str, n_sink, window, B))) return st;
 
   AppendArgs a;
   std::memset(&a, 0, sizeof(a));
@@ -488,7 +491,7 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
   HeadSchedule hs;
   if ((st = schedule_heads(head_is_streaming, (int)Hkv, &hs))) return st;
   if ((st = check_paged(kv_full, hs.n_ret, B))) return st;
-  if ((st = check_ring(kv_ring, hs.n_str, n_sink, window))) return st;
+  if ((st = check_ring(kv_ring, hs.n_str, n_sink, window, B))) return st;
   const int gs = (int)(Hq / Hkv);
   if (dt == AOH_BF16 && gs > 16) return fail(AOH_ERR_UNSUPPORTED, "Hq/Hkv=%d > 16", gs);
   const bool step = x.k_new != nullptr;
@@ -505,6 +508,9 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
     if (x.top_k < 1 || x.top_k > (1 << 30)) return fail(AOH_ERR_INVALID_ARG, "top_k=%d must be >= 1", x.top_k);
   }
   if (x.mode == kAnchor && hs.n_ret && !x.sel_out) return fail(AOH_ERR_INVALID_ARG, "indices: null pointer");
+  // the append of an fp32 step and the top-k launch put the batch in grid.z
+  if ((x.mode == kAnchor || (step && dt == AOH_F32)) && B > 65535)
+    return fail(AOH_ERR_UNSUPPORTED, "batch too large");
   uint8_t sel_rank[kMaxKvHeads] = {0};
   if (x.mode == kReuse && hs.n_ret) {
     if (!x.sel_in) return fail(AOH_ERR_INVALID_ARG, "indices: null pointer");
@@ -584,7 +590,6 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
     ap.n_chunks = 2;
     ap.streaming_mask = hs.streaming_mask;
     std::memcpy(ap.rank, hs.rank, sizeof(ap.rank));
-    if (B > 65535) return fail(AOH_ERR_UNSUPPORTED, "batch too large");
     hipError_t e = launch_append(ap, dt, (int)D, s);
     if (e != hipSuccess) return fail(AOH_ERR_HIP, "append launch: %s", hipGetErrorString(e));
   }
@@ -659,7 +664,6 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
     t.n_sel = x.top_k;
     t.part = part; t.counts = counts;
     std::memcpy(t.kv_heads, hs.ret, hs.n_ret);
-    if (B > 65535) return fail(AOH_ERR_UNSUPPORTED, "batch too large");
     e = launch_topk(t, s);
     if (e != hipSuccess) return fail(AOH_ERR_HIP, "top-k launch: %s", hipGetErrorString(e));
   }

@@ -59,15 +59,8 @@ __device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4
 __device__ __forceinline__ u32x2 ld8(const void* p) { return *reinterpret_cast<const u32x2*>(p); }
 
 // 16-byte load of data read exactly once (KV cache streaming in decode).
-#ifndef AOH_DECODE_NT
-#define AOH_DECODE_NT 1
-#endif
 __device__ __forceinline__ u32x4 ld16_stream(const void* p) {
-#if AOH_DECODE_NT
   return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
-#else
-  return *reinterpret_cast<const u32x4*>(p);
-#endif
 }
 
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {

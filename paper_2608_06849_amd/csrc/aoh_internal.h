@@ -218,14 +218,8 @@ constexpr int kSplitWaves = 4;
 
 // Query rows per bf16 prefill workgroup, and 32-row MFMA blocks per wave
 // (the workgroup has kPrefillRows / (32 * kPrefillRB) waves).
-#ifndef AOH_PREFILL_RB
-#define AOH_PREFILL_RB 1
-#endif
-#ifndef AOH_PREFILL_ROWS
-#define AOH_PREFILL_ROWS 256
-#endif
-constexpr int kPrefillRB = AOH_PREFILL_RB;
-constexpr int kPrefillRows = AOH_PREFILL_ROWS;
+constexpr int kPrefillRB = 1;
+constexpr int kPrefillRows = 256;
 constexpr int kPrefillRowsF32 = 64;
 
 }  // namespace aoh

@@ -192,10 +192,13 @@ __device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const Cac
       // Anchor layer: keep the scaled scores for the top-k selection.  Every
       // lane issues the same two stores in every chunk (a fixed count, so the
       // compiler's wait for the prefetched chunk stays exact): lanes without a
-      // query head write to a dummy area, and masked positions (beyond the
-      // valid length, never read by the selection) get -inf.
-      float* sp = head_ok ? a.scores + ((int64_t)b * a.Hq + hq) * a.score_len + tok0
-                          : a.score_dummy + 8 * lane;
+      // query head, and lanes whose tokens lie past the split's last block (the
+      // missing second block of a split with an odd block count, which at the
+      // end of a full row would be the next row's first positions), write to a
+      // dummy area; masked positions before that (beyond the valid length,
+      // never read by the selection) get -inf.
+      float* sp = (head_ok && tok0 < blk_end * kPage) ? a.scores + ((int64_t)b * a.Hq + hq) * a.score_len + tok0
+                                                       : a.score_dummy + 8 * lane;
       *reinterpret_cast<f32x4*>(sp) = f32x4{x[0], x[1], x[2], x[3]};
       *reinterpret_cast<f32x4*>(sp + 4) = f32x4{x[4], x[5], x[6], x[7]};
     }

@@ -43,14 +43,8 @@ constexpr int kRB = kPrefillRB;                 // 32-row MFMA blocks per wave
 constexpr int kRowsPerWave = 32 * kRB;
 constexpr int kWaves = kPrefillRows / kRowsPerWave;  // waves per workgroup
 
-#ifndef AOH_PREFILL_V_PAD
-#define AOH_PREFILL_V_PAD 32
-#endif
-#ifndef AOH_PREFILL_STAGE_TILES
-#define AOH_PREFILL_STAGE_TILES 1
-#endif
 // 64-key tiles per LDS stage (one barrier per stage).
-constexpr int kStageTiles = AOH_PREFILL_STAGE_TILES;
+constexpr int kStageTiles = 1;
 
 template <int D>
 struct PrefillLds {
@@ -58,7 +52,7 @@ struct PrefillLds {
   // rows; V rows are read by the transpose read as 4 rows x 32 bytes per
   // 16 lanes.  Each padding spreads its access pattern over distinct banks.
   static constexpr int kStrideK = D + 8;
-  static constexpr int kStrideV = D + AOH_PREFILL_V_PAD;
+  static constexpr int kStrideV = D + 32;
   uint16_t k[kBN * kStageTiles][kStrideK];
   uint16_t v[kBN * kStageTiles][kStrideV];
 };
@@ -342,22 +336,15 @@ __global__ __launch_bounds__(kWaves * kWave, kRB == 1 ? 2 : 1) void prefill_bf16
         for (int i = 0; i < 16; ++i) acc_o[rb][mb][i] *= alpha;
     }
   };
-#ifndef AOH_PREFILL_DOT2_SUM
-#define AOH_PREFILL_DOT2_SUM 1
-#endif
   auto block_exp = [&](int rb, const f32x16& sb, bf16x8& p_lo, bf16x8& p_hi) {
     const float m_use = (m_run[rb] == -INFINITY) ? 0.f : m_run[rb];
     float psum = 0.f;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const float p = fast_exp2(fmaf(sb[i], c, -m_use));
-#if !AOH_PREFILL_DOT2_SUM
-      psum += p;
-#endif
       if (i < 8) p_lo[i] = f32_to_bf16(p);
       else p_hi[i - 8] = f32_to_bf16(p);
     }
-#if AOH_PREFILL_DOT2_SUM
     // Row sum of the bf16 P actually fed to P.V: one dot2 with (1, 1) per pair.
     const bf16x2 ones = {(bf16)1.f, (bf16)1.f};
 #define AOH_DOT2_PAIR(v, j) \
@@ -371,7 +358,6 @@ __global__ __launch_bounds__(kWaves * kWave, kRB == 1 ? 2 : 1) void prefill_bf16
     AOH_DOT2_PAIR(p_hi, 4);
     AOH_DOT2_PAIR(p_hi, 6);
 #undef AOH_DOT2_PAIR
-#endif
     l_run[rb] += psum;
   };
 
@@ -416,19 +402,12 @@ __global__ __launch_bounds__(kWaves * kWave, kRB == 1 ? 2 : 1) void prefill_bf16
   // MFMAs of block 1 next to the exponentials of block 0 and the P.V MFMAs of
   // block 0 next to the max of block 1 (same scheduling region, independent
   // work for the matrix core and the vector ALU); then block 1.
-#ifndef AOH_PREFILL_SETPRIO
-#define AOH_PREFILL_SETPRIO 1
-#endif
   // Wave issue priority (s_setprio, inside this wave only): raised while a wave
   // issues its MFMA clusters so the matrix core is fed first and the other
   // wave's vector work fills the gaps.
   auto prio = [&](int p) {
-#if AOH_PREFILL_SETPRIO
     if (p) __builtin_amdgcn_s_setprio(1);
     else __builtin_amdgcn_s_setprio(0);
-#else
-    (void)p;
-#endif
   };
   auto tile_step = [&](const PrefillLds<D>& buf, int u, int kb, auto masked) {
     f32x16 s0[kRB], s1[kRB];
@@ -628,18 +607,8 @@ __global__ __launch_bounds__(kPrefillRowsF32) void prefill_f32_kernel(PrefillArg
 // the same time (3.68 ms): this one needs ~4% more cycles and the GPU holds a
 // higher clock for it (2.10 vs 2.01 GHz), i.e. both run at the clock the chip
 // sustains for this mix of MFMA, LDS and vector work.
-#ifndef AOH_PP_STAGES
-#define AOH_PP_STAGES 4
-#endif
-#ifndef AOH_PP_XCD
-#define AOH_PP_XCD 1
-#endif
-constexpr int kPPStages = AOH_PP_STAGES;
-static_assert(kPPStages == 4 || kPPStages == 5, "4 or 5 LDS stages (32 KB each)");
+constexpr int kPPStages = 4;  // LDS stages of 32 KB
 constexpr int kPPD = 128;
-#ifndef AOH_PP_SCHED
-#define AOH_PP_SCHED 1
-#endif
 constexpr int kPPRows = kPrefillRows;     // query rows per workgroup (8 waves x 32)
 static_assert(kPPRows == 256 && kPrefillRB == 1, "phase-shifted kernel: 8 waves x 32 rows");
 
@@ -682,7 +651,6 @@ __device__ __forceinline__ bool pp_work_item(const PrefillArgs& a, int rows, int
   const int rem = wg % per_block;
   qh_local = rem % n_qh;
   b = rem / n_qh;
-#if AOH_PP_XCD
   if (!a.seq_major) {
     // XCD-aware order.  Workgroups go to the 8 XCDs (each with its own L2)
     // in turn; work item group j = (query block, sequence, KV head), heaviest
@@ -707,7 +675,6 @@ __device__ __forceinline__ bool pp_work_item(const PrefillArgs& a, int rows, int
     b = r2 / a.n_kv;
     qh_local = (r2 % a.n_kv) * a.gs + hl;
   }
-#endif
   if (a.seq_major) {
     int unit = wg / n_qh;
     qh_local = wg % n_qh;
@@ -971,7 +938,6 @@ __device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PP
     append_tile(t);
     pv_part();
     qk_part(t);
-#if AOH_PP_SCHED
     // Operands are read four MFMAs ahead of their products, the first K
     // operands while the last P.V products run.
     __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
@@ -986,7 +952,6 @@ __device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PP
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-#endif
   };
 
   // Vector phase of tile t: mask, row max, lazy rescale, exponentials into
@@ -1164,24 +1129,20 @@ __global__ __launch_bounds__(512, 1) void prefill_pp_mixed_kernel(PrefillArgs ar
   else if (wg >= ret_pad) prefill_pp_body<true, OUT_F32, APPEND>(as, wg - ret_pad, lds);
 }
 
-#ifndef AOH_PREFILL_PP
-#define AOH_PREFILL_PP 1
-#endif
-
 template <int D, bool STREAM, bool OUT_F32>
 static hipError_t launch_bf16(const PrefillArgs& a, hipStream_t s) {
   const int grid = a.n_qblocks * a.n_kv * a.gs * a.B;
-  if (AOH_PREFILL_PP && D == kPPD) {
+  if constexpr (D == kPPD) {
     if (a.append)
       hipLaunchKernelGGL((prefill_pp_kernel<STREAM, OUT_F32, true>), dim3(grid), dim3(512), 0, s, a);
     else
       hipLaunchKernelGGL((prefill_pp_kernel<STREAM, OUT_F32, false>), dim3(grid), dim3(512), 0, s, a);
-    return hipGetLastError();
+  } else {
+    if (a.append)
+      hipLaunchKernelGGL((prefill_bf16_kernel<D, STREAM, OUT_F32, true>), dim3(grid), dim3(kWaves * kWave), 0, s, a);
+    else
+      hipLaunchKernelGGL((prefill_bf16_kernel<D, STREAM, OUT_F32, false>), dim3(grid), dim3(kWaves * kWave), 0, s, a);
   }
-  if (a.append)
-    hipLaunchKernelGGL((prefill_bf16_kernel<D, STREAM, OUT_F32, true>), dim3(grid), dim3(kWaves * kWave), 0, s, a);
-  else
-    hipLaunchKernelGGL((prefill_bf16_kernel<D, STREAM, OUT_F32, false>), dim3(grid), dim3(kWaves * kWave), 0, s, a);
   return hipGetLastError();
 }
 
@@ -1202,7 +1163,7 @@ constexpr int kMixedMaxRetItems = 8 * 256;
 
 bool prefill_mixed_preferred(const PrefillArgs& ar, int dtype, int d) {
   const int64_t n_ret = (int64_t)ar.n_qblocks * ar.n_kv * ar.gs * ar.B;
-  return AOH_PREFILL_PP && dtype == 0 && d == kPPD && n_ret <= kMixedMaxRetItems;
+  return dtype == 0 && d == kPPD && n_ret <= kMixedMaxRetItems;
 }
 
 hipError_t launch_prefill_mixed(const PrefillArgs& ar, const PrefillArgs& as, int out_f32, hipStream_t s) {

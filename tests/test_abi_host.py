@@ -133,8 +133,8 @@ def test_decode_workspace_size_and_checks():
     assert A.aoh_decode_workspace_bytes(1, 32, 96, 16, 64) == 0
     # a decode call with a too-small workspace fails before launching
     q, out = _t((2, 8, 128)), _t((2, 8, 128))
-    full = A.AohPagedCache(k=FAKE, v=FAKE, block_table=FAKE, num_pages=8, max_pages_per_seq=4, n_heads=1)
-    ring = A.AohRingCache(k=FAKE, v=FAKE, n_heads=1, capacity=4 + 32)
+    full = A.AohPagedCache(k=FAKE, v=FAKE, block_table=FAKE, num_pages=8, max_pages_per_seq=4, n_heads=1, n_seqs=2)
+    ring = A.AohRingCache(k=FAKE, v=FAKE, n_heads=1, capacity=4 + 32, batch=2)
     mask = ctypes.create_string_buffer(b"\x00\x01", 2)
     need = A.aoh_decode_workspace_bytes(2, 8, 128, 4, 36)
     st = L.aoh_decode(ctypes.byref(q), ctypes.byref(full), ctypes.byref(ring), ctypes.cast(mask, ctypes.c_void_p),
@@ -161,8 +161,8 @@ def test_decode_step_validation():
     # the fused step validates its new-token tensors on top of the decode checks
     L = A.lib()
     q, out = _t((2, 8, 128)), _t((2, 8, 128))
-    full = A.AohPagedCache(k=FAKE, v=FAKE, block_table=FAKE, num_pages=8, max_pages_per_seq=4, n_heads=1)
-    ring = A.AohRingCache(k=FAKE, v=FAKE, n_heads=1, capacity=4 + 32)
+    full = A.AohPagedCache(k=FAKE, v=FAKE, block_table=FAKE, num_pages=8, max_pages_per_seq=4, n_heads=1, n_seqs=2)
+    ring = A.AohRingCache(k=FAKE, v=FAKE, n_heads=1, capacity=4 + 32, batch=2)
     mask = ctypes.create_string_buffer(b"\x00\x01", 2)
     need = A.aoh_decode_workspace_bytes(2, 8, 128, 4, 36)
 
@@ -194,13 +194,13 @@ def test_append_validation():
     L = A.lib()
     k, v = _t((2, 5, 2, 128)), _t((2, 5, 2, 128))
     mask = ctypes.create_string_buffer(b"\x00\x01", 2)
-    ring = A.AohRingCache(k=FAKE, v=FAKE, n_heads=1, capacity=36)
+    ring = A.AohRingCache(k=FAKE, v=FAKE, n_heads=1, capacity=36, batch=2)
     # retrieval head present but no paged cache
     st = L.aoh_kv_append(ctypes.byref(k), ctypes.byref(v), ctypes.cast(mask, ctypes.c_void_p),
                          ctypes.c_void_p(FAKE), None, ctypes.byref(ring), 4, 32, None)
     assert st == A.AOH_ERR_INVALID_ARG and "kv_full" in A.aoh_last_error()
     # null start positions
-    full = A.AohPagedCache(k=FAKE, v=FAKE, block_table=FAKE, num_pages=8, max_pages_per_seq=4, n_heads=1)
+    full = A.AohPagedCache(k=FAKE, v=FAKE, block_table=FAKE, num_pages=8, max_pages_per_seq=4, n_heads=1, n_seqs=2)
     st = L.aoh_kv_append(ctypes.byref(k), ctypes.byref(v), ctypes.cast(mask, ctypes.c_void_p),
                          None, ctypes.byref(full), ctypes.byref(ring), 4, 32, None)
     assert st == A.AOH_ERR_INVALID_ARG and "start_pos" in A.aoh_last_error()
@@ -275,11 +275,70 @@ def test_prefill_append_validation():
     st = fn(ctypes.byref(q), ctypes.byref(k), ctypes.byref(v), ctypes.cast(buf, ctypes.c_void_p), 4, 32, 0,
             None, None, ctypes.byref(out), None)
     assert st == A.AOH_ERR_INVALID_ARG and "kv_full is null" in A.aoh_last_error()
-    full = A.AohPagedCache(FAKE, FAKE, FAKE, 10, 20, 1)
+    full = A.AohPagedCache(FAKE, FAKE, FAKE, 10, 20, 1, 1)
     st = fn(ctypes.byref(q), ctypes.byref(k), ctypes.byref(v), ctypes.cast(buf, ctypes.c_void_p), 4, 32, 0,
             ctypes.byref(full), None, ctypes.byref(out), None)
     assert st == A.AOH_ERR_INVALID_ARG and "kv_ring is null" in A.aoh_last_error()
-    ring = A.AohRingCache(FAKE, FAKE, 1, 35)
+    ring = A.AohRingCache(FAKE, FAKE, 1, 35, 1)
     st = fn(ctypes.byref(q), ctypes.byref(k), ctypes.byref(v), ctypes.cast(buf, ctypes.c_void_p), 4, 32, 0,
             ctypes.byref(full), ctypes.byref(ring), ctypes.byref(out), None)
     assert st == A.AOH_ERR_INVALID_ARG and "capacity" in A.aoh_last_error()
+
+
+# Checks that depend on the whole request run before the first launch: with
+# fake device pointers and no GPU, a launch would return AOH_ERR_HIP, so a
+# validation status here also shows that nothing was enqueued.
+
+def test_cache_batch_must_cover_the_call():
+    L = A.lib()
+    q, out = _t((3, 8, 128)), _t((3, 8, 128))
+    mask = ctypes.create_string_buffer(b"\x00\x01", 2)
+    need = A.aoh_decode_workspace_bytes(3, 8, 128, 4, 36)
+
+    def dec(full, ring):
+        st = L.aoh_decode(ctypes.byref(q), ctypes.byref(full), ctypes.byref(ring), ctypes.cast(mask, ctypes.c_void_p),
+                          ctypes.c_void_p(FAKE), 4, 32, ctypes.byref(out), ctypes.c_void_p(FAKE), need, None)
+        return st, A.aoh_last_error()
+
+    full = A.AohPagedCache(k=FAKE, v=FAKE, block_table=FAKE, num_pages=8, max_pages_per_seq=4, n_heads=1, n_seqs=2)
+    ring = A.AohRingCache(k=FAKE, v=FAKE, n_heads=1, capacity=36, batch=3)
+    st, err = dec(full, ring)
+    assert st == A.AOH_ERR_INVALID_ARG and "n_seqs" in err
+    full.n_seqs = 3
+    ring.batch = 2
+    st, err = dec(full, ring)
+    assert st == A.AOH_ERR_INVALID_ARG and "kv_ring.batch" in err
+    # the same rule for an append of 3 sequences
+    k, v = _t((3, 5, 2, 128)), _t((3, 5, 2, 128))
+    st = L.aoh_kv_append(ctypes.byref(k), ctypes.byref(v), ctypes.cast(mask, ctypes.c_void_p),
+                         ctypes.c_void_p(FAKE), ctypes.byref(full), ctypes.byref(ring), 4, 32, None)
+    assert st == A.AOH_ERR_INVALID_ARG and "kv_ring.batch" in A.aoh_last_error()
+    # and for a prefill that fills the caches
+    q4, k4, v4, o4 = _t((3, 64, 4, 128)), _t((3, 64, 2, 128)), _t((3, 64, 2, 128)), _t((3, 64, 4, 128))
+    st = L.aoh_prefill_append(ctypes.byref(q4), ctypes.byref(k4), ctypes.byref(v4), ctypes.cast(mask, ctypes.c_void_p),
+                              4, 32, 0, ctypes.byref(full), ctypes.byref(ring), ctypes.byref(o4), None)
+    assert st == A.AOH_ERR_INVALID_ARG and "kv_ring.batch" in A.aoh_last_error()
+
+
+def test_packed_fp32_append_rejected_before_launch():
+    q, k, v, out = _t((300, 4, 64), A.AOH_F32), _t((300, 2, 64), A.AOH_F32), _t((300, 2, 64), A.AOH_F32), \
+        _t((300, 4, 64), A.AOH_F32)
+    mask = ctypes.create_string_buffer(b"\x00\x01", 2)
+    full = A.AohPagedCache(FAKE, FAKE, FAKE, 64, 20, 1, 2)
+    ring = A.AohRingCache(FAKE, FAKE, 1, 36, 2)
+    st = A.lib().aoh_prefill_varlen(ctypes.byref(q), ctypes.byref(k), ctypes.byref(v), ctypes.c_void_p(FAKE), 2, 200,
+                                    ctypes.cast(mask, ctypes.c_void_p), 4, 32, 0, ctypes.byref(full),
+                                    ctypes.byref(ring), ctypes.byref(out), None)
+    assert st == A.AOH_ERR_UNSUPPORTED and "needs bf16" in A.aoh_last_error()
+
+
+def test_anchor_large_batch_rejected_before_launch():
+    B = 65536
+    q, out = _t((B, 8, 128)), _t((B, 8, 128))
+    mask = ctypes.create_string_buffer(b"\x00\x01", 2)
+    full = A.AohPagedCache(FAKE, FAKE, FAKE, 8, 4, 1, B)
+    ring = A.AohRingCache(FAKE, FAKE, 1, 36, B)
+    st = A.lib().aoh_decode_anchor(ctypes.byref(q), ctypes.byref(full), ctypes.byref(ring),
+                                   ctypes.cast(mask, ctypes.c_void_p), ctypes.c_void_p(FAKE), 4, 32, 16,
+                                   ctypes.c_void_p(FAKE), ctypes.byref(out), ctypes.c_void_p(FAKE), 1 << 62, None)
+    assert st == A.AOH_ERR_UNSUPPORTED and "batch" in A.aoh_last_error()

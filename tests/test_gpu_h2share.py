@@ -263,3 +263,93 @@ def test_anchor_then_reuse_chain():
     assert np.array_equal(idx.cpu().numpy(), want_idx), "anchor selection differs from the oracle's"
     want = HS.reuse_decode(f64(qr), f64(kr), f64(vr), lens, mask, 4, 32, want_idx, mapping)
     assert_parity(out, want, BF, "anchor -> reuse chain")
+
+
+# ------------------------------------------------------------------------- top-k over several segments
+#
+# The selection cuts each list into 8 segments of whole 4096-position tiles and
+# combines per-segment histograms, counts and compaction offsets.  A list of
+# 131072 positions has 8 full segments of 16384; one of 40000 has segments of
+# 8192 with a ragged fifth and three empty ones.
+
+def _plant_threshold_ties(kk, qa, lens, n_super, tie_at, n_tie, gs, seed):
+    """Group 0 of every sequence: n_super planted keys of distinct strength,
+    above n_tie identical keys centred on position tie_at[b] (a segment
+    boundary); everything else stays N(0, 1).  With top_k = n_super + n_tie / 2
+    the selection threshold falls inside the tied run."""
+    d = kk.shape[-1]
+    for b, n in enumerate(lens):
+        u = qa[b, :gs].sum(0)
+        u /= np.linalg.norm(u)
+        ties = np.arange(tie_at[b] - n_tie // 2, tie_at[b] + n_tie // 2)
+        free = np.setdiff1d(np.arange(n), ties)
+        sup = synth.rng(seed, "h2-super", b).choice(free, n_super, replace=False)
+        kk[b, sup, 0] = (4.0 + np.arange(n_super)[:, None] / n_super) * np.sqrt(d) * u
+        kk[b, ties, 0] = 3.0 * np.sqrt(d) * u
+    return kk
+
+
+@pytest.mark.parametrize("planted", [False, True])
+def test_anchor_topk_several_segments(planted):
+    B, L, hq, hkv, d, top_k = 2, 131072, 8, 2, 128, 2048
+    lens = [131072, 40000]
+    mask, n_sink, window, seed = [0, 1], 64, 1024, 21
+    gs = hq // hkv
+    qa = synth.gaussian((B, hq, d), seed, "h2-q")
+    tie_at = [16384, 32768]
+    n_super, n_tie = top_k - 8, 16
+    boost = (lambda kk: _plant_threshold_ties(kk, qa, lens, n_super, tie_at, n_tie, gs, seed)) if planted else None
+    k, v, full, ring = _decode_setup(B, L, hq, hkv, d, mask, n_sink, window, seed, k_boost=boost)
+    _fill(k, v, mask, lens, full, ring, n_sink, window)
+    q = _bf(qa)
+    lens_t = torch.tensor(lens, dtype=torch.int32, device=DEV)
+    out_a, idx = aoh_decode_anchor(q.to(DEV), full, ring, mask, lens_t, n_sink, window, top_k)
+    ws = torch.empty(aoh_decode_workspace_bytes(B, hq, d, full.block_table.shape[1], n_sink + window) // 4 + 4,
+                     dtype=torch.float32, device=DEV)
+    out_d = aoh_decode(q.to(DEV), full, ring, mask, lens_t, n_sink, window, workspace=ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits(out_a), bits(out_d)), "anchor output differs from aoh_decode"
+    got = idx.cpu().numpy()
+    n_exact = _check_selection(got, q, k, lens, mask, top_k, f"anchor multi-segment planted={planted}")
+    if planted:
+        for b in range(B):
+            sel = set(got[b, 0].tolist())
+            ties = list(range(tie_at[b] - n_tie // 2, tie_at[b] + n_tie // 2))
+            # exactly the 8 lowest tied positions (all before the boundary) are taken
+            assert [p for p in ties if p in sel] == ties[:n_tie // 2], f"b{b}: tie order across the segment boundary"
+            # every planted key above the tie level is taken
+            assert len(sel) == top_k and len(sel - set(ties)) == n_super
+    print(f"anchor multi-segment planted={planted}: {n_exact} lists exact")
+
+
+def test_anchor_odd_page_count_full_last_page():
+    # 19 pages per sequence (odd) with the length in the last page: the last
+    # split of a row covers one block, and its second block's score slots lie
+    # past the row.  Strong keys at positions 0..15 of every group make any
+    # overwrite of a neighbouring row's first positions change the selection.
+    B, L, hq, hkv, d, top_k = 2, 293, 8, 2, 128, 24
+    lens = [293, 290]
+    mask, n_sink, window, seed = [0, 0], 4, 32, 22
+    qa = synth.gaussian((B, hq, d), seed, "h2-q")
+
+    def early(kk):
+        for b in range(B):
+            for g in range(hkv):
+                u = qa[b, g * 4:(g + 1) * 4].sum(0)
+                u /= np.linalg.norm(u)
+                kk[b, :16, g] = (2.0 + np.arange(16)[:, None] / 16.0) * np.sqrt(d) * u
+
+    k, v, full, ring = _decode_setup(B, L, hq, hkv, d, mask, n_sink, window, seed, k_boost=early)
+    assert full.block_table.shape[1] == 19
+    _fill(k, v, mask, lens, full, ring, n_sink, window)
+    q = _bf(qa)
+    _, idx = aoh_decode_anchor(q.to(DEV), full, ring, mask, torch.tensor(lens, dtype=torch.int32, device=DEV),
+                               n_sink, window, top_k)
+    torch.cuda.synchronize()
+    got = idx.cpu().numpy()
+    _check_selection(got, q, k, lens, mask, top_k, "anchor odd page count")
+    want = HS.anchor_select(f64(q), f64(k), lens, mask, top_k)
+    assert np.array_equal(got, want), "selection differs from the oracle's"
+    for b in range(B):
+        for r in range(2):
+            assert set(range(16)) <= set(got[b, r].tolist())

@@ -130,3 +130,157 @@ def test_vectorised_readers_match_per_token_readers():
         slot = M.ring_slot(int(p), 5, 37)
         kk, vv = M.ring_read_slot(kr_, vr_, 1, 0, slot)
         assert np.array_equal(K[i], kk) and np.array_equal(V[i], vv)
+
+
+# ---------------------------------------------------------------- negative pins of the bit-exact checkers
+#
+# A correct cache image is built here by direct index arithmetic from the
+# documented layout (not through the oracle's readers), the checkers must find
+# no mismatch in it, and every planted fault must be counted.
+
+def _cache_image(seed=0, B=2, lens=(45, 70), mask=(0, 1, 0, 1), n_sink=3, window=20, d=8, n_pages=16):
+    rng = np.random.default_rng(seed)
+    T = max(lens)
+    hkv = len(mask)
+    ks = rng.standard_normal((B, T, hkv, d)).astype(np.float32)
+    vs = rng.standard_normal((B, T, hkv, d)).astype(np.float32)
+    ret = [g for g in range(hkv) if not mask[g]]
+    st = [g for g in range(hkv) if mask[g]]
+    max_pages = (T + 15) // 16
+    bt = rng.permutation(n_pages)[:B * max_pages].reshape(B, max_pages)
+    kp = np.full((n_pages, len(ret), 16, d), np.nan, np.float32)
+    vp = np.full((n_pages, len(ret), d, 16), np.nan, np.float32)
+    cap = n_sink + window
+    nblk = (cap + 15) // 16
+    kr = np.full((B, len(st), nblk, 16, d), np.nan, np.float32)
+    vr = np.full((B, len(st), nblk, d, 16), np.nan, np.float32)
+    for b in range(B):
+        for p in range(lens[b]):
+            page, row = bt[b, p // 16], p % 16
+            for r, g in enumerate(ret):
+                kp[page, r, row] = ks[b, p, g]
+                vp[page, r, :, row] = vs[b, p, g]
+            # ring: sinks keep their slot; later tokens cycle through the window
+            slot = p if p < n_sink else n_sink + (p - n_sink) % window
+            for s, g in enumerate(st):
+                kr[b, s, slot // 16, slot % 16] = ks[b, p, g]
+                vr[b, s, slot // 16, :, slot % 16] = vs[b, p, g]
+    return dict(ks=ks, vs=vs, kp=kp, vp=vp, kr=kr, vr=vr, bt=bt, lens=np.array(lens), mask=mask,
+                n_sink=n_sink, window=window)
+
+
+def _bad_paged(c):
+    return M.check_paged(c["kp"], c["vp"], c["bt"], c["ks"], c["vs"], c["lens"], c["mask"])
+
+
+def _bad_ring(c):
+    return M.check_ring(c["kr"], c["vr"], c["ks"], c["vs"], c["lens"], c["mask"], c["n_sink"], c["window"])
+
+
+def test_checkers_accept_a_correct_image():
+    c = _cache_image()
+    assert _bad_paged(c) == 0 and _bad_ring(c) == 0
+
+
+def test_checker_counts_a_flipped_bit_in_a_k_row():
+    c = _cache_image()
+    page, row = c["bt"][1, 33 // 16], 33 % 16
+    k = c["kp"][page, 1, row].view(np.uint32)
+    k[3] ^= 1                                       # lowest mantissa bit of one element
+    assert _bad_paged(c) == 1
+
+
+def test_checker_counts_a_v_column_of_the_wrong_token():
+    c = _cache_image()
+    page = c["bt"][0, 0]
+    c["vp"][page, 0, :, 5] = c["vs"][0, 6, 0]       # token 5's V column holds token 6
+    assert _bad_paged(c) == 1
+
+
+def test_checker_counts_a_stale_ring_slot_after_wrap():
+    c = _cache_image()
+    n_sink, window = c["n_sink"], c["window"]
+    p = c["lens"][1] - 1                            # newest token of sequence 1, past the wrap
+    slot = n_sink + (p - n_sink) % window
+    stale = p - window                              # the token that slot held one lap earlier
+    g = [h for h in range(4) if c["mask"][h]][1]
+    c["kr"][1, 1, slot // 16, slot % 16] = c["ks"][1, stale, g]
+    c["vr"][1, 1, slot // 16, :, slot % 16] = c["vs"][1, stale, g]
+    assert _bad_ring(c) == 1
+
+
+def test_checker_counts_swapped_retrieval_ranks():
+    c = _cache_image()
+    c["kp"][:, [0, 1]] = c["kp"][:, [1, 0]]
+    c["vp"][:, [0, 1]] = c["vp"][:, [1, 0]]
+    assert _bad_paged(c) == 2 * int(c["lens"].sum())
+
+
+def test_checker_counts_swapped_streaming_ranks_and_sink_loss():
+    c = _cache_image()
+    c["kr"][:, [0, 1]] = c["kr"][:, [1, 0]]
+    assert _bad_ring(c) == 2 * 2 * (c["n_sink"] + c["window"])
+    c = _cache_image()
+    c["vr"][0, 0, 0, :, 1] = c["vs"][0, 1 + c["window"], 1]   # sink slot 1 overwritten as if it cycled
+    assert _bad_ring(c) == 1
+
+
+# ---------------------------------------------------------------- decode bytes
+
+def test_decode_kv_bytes_hand_cases():
+    # (2 retrieval heads x 5 tokens + 1 ring of min(5, 2+3)) and (2 x 100 + min(100, 5)), d 4, bf16, K and V
+    assert C.decode_kv_bytes([5, 100], 2, 1, 4, 2, 2, 3) == (15 + 205) * 4 * 2 * 2
+    assert C.decode_kv_bytes([], 3, 1, 128, 2, 64, 1024) == 0
+    assert C.decode_kv_bytes([1], 0, 4, 128, 4, 64, 1024) == 4 * 1 * 128 * 2 * 4
+    # the batch-8 x 131072 Llama-3-8B-shaped step: 4 + 4 KV heads, ring 64 + 1024
+    b = C.decode_kv_bytes([131072] * 8, 4, 4, 128, 2, 64, 1024)
+    assert b == 8 * (4 * 131072 + 4 * 1088) * 128 * 2 * 2
+    assert math.isclose(b / 1e9, 2.1653, abs_tol=5e-5)
+
+
+@pytest.mark.parametrize("n_sink,window", [(0, 1), (3, 20), (64, 16)])
+def test_decode_kv_bytes_equals_the_cache_image(n_sink, window):
+    # bytes read by a step = tokens stored in the paged cache + live ring slots
+    # (ring replay, independent of the min() in the formula), K and V
+    for lens in ([1], [7, 50], [200, 3, 81]):
+        live = sum(int((M.ring_tokens(n, n_sink, window) >= 0).sum()) for n in lens)
+        want = (2 * sum(lens) + 3 * live) * 16 * 2 * 2
+        assert C.decode_kv_bytes(lens, 2, 3, 16, 2, n_sink, window) == want
+        # and one layer of the resident-KV formula per sequence
+        assert C.decode_kv_bytes(lens, 2, 3, 16, 2, n_sink, window) == \
+            sum(C.kv_cache_bytes(1, 16, 2, 2, 3, n, n_sink, window) for n in lens)
+
+
+def test_decode_kv_bytes_rejects_planted_mistakes():
+    lens, args = [37, 5000], (2, 3, 128, 2, 64, 1024)
+    good = C.decode_kv_bytes(lens, *args)
+    no_v = sum((2 * n + 3 * min(n, 1088)) * 128 * 2 for n in lens)          # K only
+    full_ring = sum((2 * n + 3 * n) * 128 * 2 * 2 for n in lens)            # streaming heads read everything
+    window_only = sum((2 * n + 3 * min(n, 1024)) * 128 * 2 * 2 for n in lens)  # sink forgotten
+    assert good not in (no_v, full_ring, window_only)
+
+
+# ---------------------------------------------------------------- the benchmark's own counters
+
+def _bench():
+    import importlib.util
+    spec = importlib.util.spec_from_file_location("bench", os.path.join(os.path.dirname(GOLDEN), "..", "bench.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+def test_bench_counters_equal_the_oracle_accounting():
+    bench = _bench()
+    for t in (1, 2, 63, 64, 65, 255, 1000, 4096, 32768, 262144):
+        for n_sink, window in ((0, 1), (4, 32), (64, 1024), (64, 2048), (2000, 10), (5, 100000)):
+            for st in (False, True):
+                assert bench.visible_pairs(t, st, n_sink, window) == C.visible_pairs(t, st, n_sink, window)
+            for hr, hs in ((14, 14), (28, 0), (0, 28), (7, 21)):
+                assert bench.useful_prefill_flops(t, 128, hr, hs, n_sink, window) == \
+                    C.prefill_flops(t, 128, hr, hs, n_sink, window)
+    for lens in ([131072] * 8, [1, 17, 1088, 1089], [262144]):
+        for gr, gs in ((4, 4), (2, 2), (8, 0), (0, 8)):
+            for n_sink, window in ((64, 1024), (64, 2048), (0, 1)):
+                assert bench.decode_bytes(lens, gr, gs, 128, 2, n_sink, window) == \
+                    C.decode_kv_bytes(lens, gr, gs, 128, 2, n_sink, window)
