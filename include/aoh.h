@@ -262,6 +262,26 @@ aoh_status aoh_decode_step(const aoh_tensor* q, const aoh_tensor* k_new, const a
                            void* stream);
 
 /*
+ * aoh_decode_step for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same call without a workspace argument.  The split-K partials go to a
+ * static 64 MiB device array of the library (one per GPU, held until the
+ * process ends); this call allocates nothing and calls no allocating routine.
+ * Results and caches are bit-identical to aoh_decode_step.
+ * Errors: as aoh_decode_step; AOH_ERR_UNSUPPORTED when the step would need
+ * more than 64 MiB of workspace (aoh_decode_workspace_bytes > 64 MiB, e.g. a
+ * batch far above 8 x 131072 tokens at 32 query heads of width 128);
+ * AOH_ERR_HIP when the array's device address cannot be obtained.  All calls
+ * on one GPU share its array, which keeps the last call's contents: calls
+ * that overlap on one GPU (other streams, other threads) race and must be
+ * serialised by the caller.
+ */
+aoh_status aoh_decode_step_noalloc(const aoh_tensor* q, const aoh_tensor* k_new, const aoh_tensor* v_new,
+                                   const aoh_paged_cache* kv_full, const aoh_ring_cache* kv_ring,
+                                   const uint8_t* head_is_streaming, const int32_t* lens, int32_t n_sink,
+                                   int32_t window, aoh_tensor* out, void* stream);
+
+/*
  * ---------------------------------------------------------------- H2Share
  * AoH-guided cross-layer sparse attention (paper section "AoH-Guided Sparse
  * Attention: H2Share" and its Inference Phase; GQA appendix, group-level head

@@ -49,6 +49,7 @@ class AohRingCache(ctypes.Structure):
 _lib = None
 
 EXPORTS = ("aoh_prefill", "aoh_prefill_chunked", "aoh_prefill_append", "aoh_prefill_varlen", "aoh_kv_append", "aoh_decode_workspace_bytes", "aoh_decode", "aoh_decode_step",
+           "aoh_decode_step_noalloc",
            "aoh_classify_workspace_bytes", "aoh_classify", "aoh_retrieval_group_count",
            "aoh_head_mapping_workspace_bytes", "aoh_head_mapping", "aoh_decode_anchor_workspace_bytes",
            "aoh_decode_anchor", "aoh_decode_reuse_workspace_bytes", "aoh_decode_reuse",
@@ -93,6 +94,10 @@ def lib():
                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                       P(AohTensor), ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
         L.aoh_decode_step.restype = ctypes.c_int
+        L.aoh_decode_step_noalloc.argtypes = [P(AohTensor), P(AohTensor), P(AohTensor), P(AohPagedCache),
+                                              P(AohRingCache), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                              ctypes.c_int32, P(AohTensor), ctypes.c_void_p]
+        L.aoh_decode_step_noalloc.restype = ctypes.c_int
         L.aoh_classify_workspace_bytes.argtypes = [ctypes.c_int32] * 4
         L.aoh_classify_workspace_bytes.restype = ctypes.c_size_t
         L.aoh_classify.argtypes = [P(AohTensor), P(AohTensor), ctypes.c_int32, ctypes.c_int32,
@@ -328,6 +333,22 @@ def aoh_decode_step(q, k_new, v_new, kv_full, kv_ring, head_is_streaming, lens, 
                                  ctypes.byref(fd) if fd else None, ctypes.byref(rd) if rd else None, m.ptr,
                                  _ptr(lens), n_sink, window, ctypes.byref(od), ctypes.c_void_p(ws_ptr),
                                  ws_bytes, _stream(stream)))
+    return out
+
+
+def aoh_decode_step_noalloc(q, k_new, v_new, kv_full, kv_ring, head_is_streaming, lens, n_sink, window, out=None,
+                            stream=None):
+    """aoh_decode_step without a workspace: the library's static scratch area
+    holds the split partials (calls on one GPU must not overlap)."""
+    if out is None:
+        out = torch.empty_like(q)
+    qd, kd, vd, od = tensor_desc(q), tensor_desc(k_new), tensor_desc(v_new), tensor_desc(out)
+    fd = kv_full.desc() if kv_full is not None else None
+    rd = kv_ring.desc() if kv_ring is not None else None
+    m = _Mask(head_is_streaming)
+    _check(lib().aoh_decode_step_noalloc(ctypes.byref(qd), ctypes.byref(kd), ctypes.byref(vd),
+                                         ctypes.byref(fd) if fd else None, ctypes.byref(rd) if rd else None, m.ptr,
+                                         _ptr(lens), n_sink, window, ctypes.byref(od), _stream(stream)))
     return out
 
 

@@ -17,7 +17,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libaoh.so")
-SOURCES = ["abi.cpp", "prefill.hip", "decode.hip", "kv_append.hip", "classify.hip", "topk.hip"]
+SOURCES = ["abi.cpp", "prefill.hip", "decode.hip", "kv_append.hip", "classify.hip", "topk.hip", "noalloc.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 # Packed-fp32 VALU instructions are kept out of generated code on purpose.

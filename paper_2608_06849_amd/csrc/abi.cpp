@@ -465,6 +465,7 @@ struct DecodeExtra {
   const int32_t* mapping = nullptr;  // reuse: HOST [Hkv], list rank per retrieval group
   const aoh_tensor* k_new = nullptr;  // fused step: token at lens - 1, [B][Hkv][D]
   const aoh_tensor* v_new = nullptr;
+  size_t* need_only = nullptr;  // validate only: store the workspace bytes needed, launch nothing
 };
 
 static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_full, const aoh_ring_cache* kv_ring,
@@ -562,6 +563,20 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
     std::memcpy(c.kv_heads, hs.str, hs.n_str);
   }
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if ((int64_t)a.full.n_items + a.ring.n_items >= (1ll << 31)) return fail(AOH_ERR_UNSUPPORTED, "grid too large");
+  // Workspace: split partials (bf16 only; fp32 decodes directly).
+  const size_t base_need = dt == AOH_F32 ? 0 : workspace_bytes((int)B, (int)Hq, (int)D, sp_bound);
+  const size_t need = x.mode == kAnchor ? align256(base_need) + anchor_extra(B, Hq, max_pages) : base_need;
+  if (x.need_only) {
+    *x.need_only = need;
+    return ok();
+  }
+  if (dt == AOH_BF16) {
+    if (!workspace) return fail(AOH_ERR_WORKSPACE, "workspace is null; %zu bytes needed", need);
+    if (workspace_bytes_given < need)
+      return fail(AOH_ERR_WORKSPACE, "workspace has %zu bytes; %zu needed", workspace_bytes_given, need);
+    if (reinterpret_cast<uintptr_t>(workspace) % 16) return fail(AOH_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
+  }
 
   if (step) {
     a.k_new = x.k_new->data; a.v_new = x.v_new->data;
@@ -601,12 +616,6 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
     return ok();
   }
 
-  const size_t base_need = workspace_bytes((int)B, (int)Hq, (int)D, sp_bound);
-  const size_t need = x.mode == kAnchor ? align256(base_need) + anchor_extra(B, Hq, max_pages) : base_need;
-  if (!workspace) return fail(AOH_ERR_WORKSPACE, "workspace is null; %zu bytes needed", need);
-  if (workspace_bytes_given < need)
-    return fail(AOH_ERR_WORKSPACE, "workspace has %zu bytes; %zu needed", workspace_bytes_given, need);
-  if (reinterpret_cast<uintptr_t>(workspace) % 16) return fail(AOH_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
   float* part_acc = reinterpret_cast<float*>(workspace);
   float* part_ml = part_acc + (size_t)B * Hq * sp_bound.max_splits * D;
   a.part_acc = part_acc; a.part_ml = part_ml; a.max_splits = sp_bound.max_splits;
@@ -632,7 +641,6 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
     a.sel = x.sel_in; a.n_sel = x.top_k; a.n_lists = x.n_lists;
     std::memcpy(a.sel_rank, sel_rank, sizeof(sel_rank));
   }
-  if ((int64_t)a.full.n_items + a.ring.n_items >= (1ll << 31)) return fail(AOH_ERR_UNSUPPORTED, "grid too large");
   {
     hipError_t e = launch_decode_split(a, (int)D, step ? 3 : x.mode, s);
     if (e != hipSuccess) return fail(AOH_ERR_HIP, "decode split launch: %s", hipGetErrorString(e));
@@ -690,6 +698,25 @@ aoh_status aoh_decode_step(const aoh_tensor* q, const aoh_tensor* k_new, const a
   return decode_impl(q, kv_full, kv_ring, head_is_streaming, lens, n_sink, window, out, workspace,
                      workspace_bytes_given, stream, x);
 }
+
+}  // extern "C"
+
+// Validation of a fused decode step without launching: on AOH_OK, *need is
+// the workspace aoh_decode_step needs for these arguments.
+aoh_status aoh::decode_step_workspace_need(const aoh_tensor* q, const aoh_tensor* k_new, const aoh_tensor* v_new,
+                                           const aoh_paged_cache* kv_full, const aoh_ring_cache* kv_ring,
+                                           const uint8_t* head_is_streaming, const int32_t* lens, int32_t n_sink,
+                                           int32_t window, aoh_tensor* out, size_t* need) {
+  if (!k_new) return fail(AOH_ERR_INVALID_ARG, "k_new: null descriptor");
+  if (!v_new) return fail(AOH_ERR_INVALID_ARG, "v_new: null descriptor");
+  DecodeExtra x;
+  x.k_new = k_new; x.v_new = v_new; x.need_only = need;
+  return decode_impl(q, kv_full, kv_ring, head_is_streaming, lens, n_sink, window, out, nullptr, 0, nullptr, x);
+}
+
+aoh_status aoh::report(aoh_status st, const char* msg) { return st == AOH_OK ? ok() : fail(st, "%s", msg); }
+
+extern "C" {
 
 size_t aoh_decode_anchor_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t d_head,
                                          int32_t max_pages_per_seq, int32_t ring_capacity) {

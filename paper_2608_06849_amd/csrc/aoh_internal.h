@@ -222,4 +222,15 @@ constexpr int kPrefillRB = 1;
 constexpr int kPrefillRows = 256;
 constexpr int kPrefillRowsF32 = 64;
 
+// Host layer (abi.cpp) services for entry points defined in other units.
+// The aoh_* types come from aoh.h, which the including unit includes first.
+#ifdef AOH_H_
+aoh_status decode_step_workspace_need(const aoh_tensor* q, const aoh_tensor* k_new, const aoh_tensor* v_new,
+                                      const aoh_paged_cache* kv_full, const aoh_ring_cache* kv_ring,
+                                      const uint8_t* head_is_streaming, const int32_t* lens, int32_t n_sink,
+                                      int32_t window, aoh_tensor* out, size_t* need);
+// Sets the thread's last-error text for a status (clears it for AOH_OK) and returns the status.
+aoh_status report(aoh_status st, const char* msg);
+#endif
+
 }  // namespace aoh

@@ -342,3 +342,18 @@ def test_anchor_large_batch_rejected_before_launch():
                                    ctypes.cast(mask, ctypes.c_void_p), ctypes.c_void_p(FAKE), 4, 32, 16,
                                    ctypes.c_void_p(FAKE), ctypes.byref(out), ctypes.c_void_p(FAKE), 1 << 62, None)
     assert st == A.AOH_ERR_UNSUPPORTED and "batch" in A.aoh_last_error()
+
+
+def test_noalloc_step_rejects_a_workspace_beyond_the_static_area():
+    # batch 8192 x 16 query heads of width 128: the split partials need more
+    # than the 64 MiB static area (checked before any GPU call)
+    B, Hq = 8192, 16
+    q, out, kn, vn = _t((B, Hq, 128)), _t((B, Hq, 128)), _t((B, 2, 128)), _t((B, 2, 128))
+    full = A.AohPagedCache(FAKE, FAKE, FAKE, 1 << 20, 1 << 14, 1, B)
+    ring = A.AohRingCache(FAKE, FAKE, 1, 36, B)
+    mask = ctypes.create_string_buffer(b"\x00\x01", 2)
+    assert A.aoh_decode_workspace_bytes(B, Hq, 128, 1 << 14, 36) > 64 << 20
+    st = A.lib().aoh_decode_step_noalloc(ctypes.byref(q), ctypes.byref(kn), ctypes.byref(vn), ctypes.byref(full),
+                                         ctypes.byref(ring), ctypes.cast(mask, ctypes.c_void_p), ctypes.c_void_p(FAKE),
+                                         4, 32, ctypes.byref(out), None)
+    assert st == A.AOH_ERR_UNSUPPORTED and "static scratch" in A.aoh_last_error()
