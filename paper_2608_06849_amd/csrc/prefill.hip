@@ -955,7 +955,7 @@ __device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PP
   };
 
   // Vector phase of tile t: mask, row max, lazy rescale, exponentials into
-  // the P^T operands, row sums of the bf16 P actually used.
+  // the P^T operands, row sums.
   auto apply_mask = [&](int kb) {
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk)
@@ -985,22 +985,26 @@ __device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PP
         for (int i = 0; i < 16; ++i) acc_o[mb][i] *= alpha;
     }
     const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
-    float psum = 0.f;
-    const bf16x2 ones = {(bf16)1.f, (bf16)1.f};
+    // Row sum of the tile's exponentials, added as balanced trees of fp32
+    // values: the phase ends on the longest dependency chain of its vector
+    // work, and a running accumulator (or a chain of bf16 dot products) makes
+    // the sum that chain.
+    float psum[4];
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
         bf16x8 pv;
+        float pf[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) pv[i] = f32_to_bf16(fast_exp2(fmaf(sacc[blk][8 * hf + i], c, -m_use)));
-        psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pv, pv, 0, 1), ones, psum, false);
-        psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pv, pv, 2, 3), ones, psum, false);
-        psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pv, pv, 4, 5), ones, psum, false);
-        psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pv, pv, 6, 7), ones, psum, false);
+        for (int i = 0; i < 8; ++i) {
+          pf[i] = fast_exp2(fmaf(sacc[blk][8 * hf + i], c, -m_use));
+          pv[i] = f32_to_bf16(pf[i]);
+        }
+        psum[2 * blk + hf] = ((pf[0] + pf[1]) + (pf[2] + pf[3])) + ((pf[4] + pf[5]) + (pf[6] + pf[7]));
         pop[2 * blk + hf] = pv;
       }
-    l_run += psum;
+    l_run += (psum[0] + psum[1]) + (psum[2] + psum[3]);
   };
   auto valu_phase = [&](int t) {
     v_tile = t;
