@@ -546,6 +546,8 @@ def stack_decode_leg(args, torch, synth, PagedCache, RingCache, aoh_decode, aoh_
     from paper_2608_06849_amd import aoh_decode_step
 
     def one_step(fused=True):
+        # the position advances once per step (one small device add, as a
+        # serving loop does); the two-call form also moves the append position
         for l, (mask, full, ring) in enumerate(layers):
             if fused:
                 aoh_decode_step(q[l], kv[l, 0, :, 0], kv[l, 1, :, 0], full, ring, mask, lens_after, n_sink, window,
@@ -553,8 +555,9 @@ def stack_decode_leg(args, torch, synth, PagedCache, RingCache, aoh_decode, aoh_
             else:
                 aoh_kv_append(kv[l, 0], kv[l, 1], mask, lens_before, full, ring, n_sink, window)
                 aoh_decode(q[l], full, ring, mask, lens_after, n_sink, window, out=outs[l], workspace=ws)
-        lens_before.add_(1)
         lens_after.add_(1)
+        if not fused:
+            lens_before.add_(1)
 
     def timed(fn):
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
@@ -578,6 +581,7 @@ def stack_decode_leg(args, torch, synth, PagedCache, RingCache, aoh_decode, aoh_
     with torch.cuda.graph(g):
         one_step()
     graph_ms = timed(g.replay)
+    lens_before.copy_(lens_after - 1)
     g2 = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g2):
         one_step(fused=False)

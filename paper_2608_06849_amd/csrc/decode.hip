@@ -538,20 +538,26 @@ __global__ __launch_bounds__(kWave) void decode_f32_kernel(DecodeArgs a, void* o
 
 constexpr int kMergeDims = 32;      // output dimensions per merge workgroup
 constexpr int kMergeThreads = 512;  // kMergeDims x 16 split groups
+constexpr int kMergeGroups = kMergeThreads / kMergeDims;
+// Partials per (sequence, head): one per split workgroup, at most
+// kMaxSplits / kSplitWaves, so each of the 16 groups holds at most 16.
+constexpr int kMergePerGroup = kMaxSplits / kSplitWaves / kMergeGroups;
+static_assert(kMergePerGroup * kMergeGroups * kSplitWaves == kMaxSplits, "merge covers every partial");
 
 // Log-sum-exp merge of the split partials of one (sequence, query head), for
-// one slice of kMergeDims output dimensions.  The per-split (m, l) are loaded
-// by all threads at once and reduced in LDS; the weighted sum over splits of
-// acc[d] is spread over kMergeThreads / kMergeDims groups (coalesced 128-byte
-// rows), so many loads are in flight even for a single long sequence.
+// one slice of kMergeDims output dimensions.  Every load the workgroup needs
+// (each partial's (m, l), and acc[d] of this slice for all partials, spread
+// over 16 groups of 32 threads reading coalesced 128-byte rows) is issued up
+// front, so the pass costs one round trip to memory; the statistics are then
+// reduced in LDS and the weighted sums combined.
 template <int D, bool OUT_F32>
 __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(MergeArgs a) {
-  constexpr int kGroups = kMergeThreads / kMergeDims;
   constexpr int kWaves = kMergeThreads / kWave;
   constexpr int kSlices = D / kMergeDims;
-  __shared__ float s_w[kMaxSplits];
+  static_assert(kMergeThreads >= kMaxSplits / kSplitWaves, "one (m, l) pair per thread");
+  __shared__ float s_w[kMaxSplits / kSplitWaves];
   __shared__ float s_red[kWaves];
-  __shared__ float s_acc[kGroups][kMergeDims];
+  __shared__ float s_acc[kMergeGroups][kMergeDims];
   const int wg = blockIdx.x;
   const int slice = wg % kSlices;
   const int hq = (wg / kSlices) % a.Hq;
@@ -565,13 +571,23 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(MergeArgs a
   const int split_tok = streaming ? a.split_tokens_ring : a.split_tokens_full;
   const int ns = min((n_valid + split_tok - 1) / split_tok, streaming ? a.n_splits_ring : a.n_splits_full);
   const int64_t base = ((int64_t)b * a.Hq + hq) * a.max_splits;
+  const int dd = tid % kMergeDims, grp = tid / kMergeDims;
+  const int d = slice * kMergeDims + dd;
 
-  float mloc = -INFINITY;
-  for (int s = tid; s < ns; s += kMergeThreads) {
-    const float m = a.part_ml[(base + s) * 2];
-    s_w[s] = m;
-    mloc = fmaxf(mloc, m);
+  // All loads first.
+  float m = -INFINITY, l = 0.f;
+  if (tid < ns) {
+    m = a.part_ml[(base + tid) * 2];
+    l = a.part_ml[(base + tid) * 2 + 1];
   }
+  float av[kMergePerGroup];
+#pragma unroll
+  for (int k = 0; k < kMergePerGroup; ++k) {
+    const int s = grp + kMergeGroups * k;
+    av[k] = s < ns ? a.part_acc[(base + s) * D + d] : 0.f;
+  }
+
+  float mloc = m;
 #pragma unroll
   for (int o = kWave / 2; o > 0; o >>= 1) mloc = fmaxf(mloc, __shfl_xor(mloc, o, kWave));
   if (lane == 0) s_red[wave] = mloc;
@@ -580,12 +596,9 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(MergeArgs a
 #pragma unroll
   for (int i = 1; i < kWaves; ++i) mx = fmaxf(mx, s_red[i]);
   __syncthreads();
-  float lloc = 0.f;
-  for (int s = tid; s < ns; s += kMergeThreads) {
-    const float w = fast_exp2(s_w[s] - mx);
-    s_w[s] = w;
-    lloc += w * a.part_ml[(base + s) * 2 + 1];
-  }
+  const float w = tid < ns ? fast_exp2(m - mx) : 0.f;
+  if (tid < ns) s_w[tid] = w;
+  float lloc = w * l;
 #pragma unroll
   for (int o = kWave / 2; o > 0; o >>= 1) lloc += __shfl_xor(lloc, o, kWave);
   if (lane == 0) s_red[wave] = lloc;
@@ -594,11 +607,12 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(MergeArgs a
 #pragma unroll
   for (int i = 0; i < kWaves; ++i) L += s_red[i];
 
-  const int dd = tid % kMergeDims, grp = tid / kMergeDims;
-  const int d = slice * kMergeDims + dd;
   float acc = 0.f;
-#pragma unroll 8
-  for (int s = grp; s < ns; s += kGroups) acc += s_w[s] * a.part_acc[(base + s) * D + d];
+#pragma unroll
+  for (int k = 0; k < kMergePerGroup; ++k) {
+    const int s = grp + kMergeGroups * k;
+    if (s < ns) acc += s_w[s] * av[k];
+  }
   s_acc[grp][dd] = acc;
   __syncthreads();
   if (a.ml_out && !streaming && slice == 0 && tid == 0) {
@@ -608,7 +622,7 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(MergeArgs a
   if (grp == 0) {
     float tot = 0.f;
 #pragma unroll
-    for (int i = 0; i < kGroups; ++i) tot += s_acc[i][dd];
+    for (int i = 0; i < kMergeGroups; ++i) tot += s_acc[i][dd];
     const float o = tot / L;
     if (OUT_F32) {
       reinterpret_cast<float*>(a.out)[(int64_t)b * a.o_sb + (int64_t)hq * a.o_sh + d] = o;
