@@ -6,21 +6,26 @@
 Step = one pass of the whole hot path over the Qwen2.5-7B-shaped layer
 (28 query heads, 4 KV heads of which 1 and 3 are streaming, d_head 128, bf16,
 one 32768-token sequence, n_sink 64, window 1024):
-  head scheduling -> retrieval prefill launch -> streaming prefill launch,
-  both writing the prompt's K/V into the paged cache and the ring as they go
-  -> one decode step (append the next token, split-K decode, merge).
+  head scheduling -> one prefill launch holding the retrieval and the
+  streaming work items, which also writes the prompt's K/V into the paged
+  cache and the ring -> one decode step (store the next token, split-K
+  decode, merge).
 `value` is the useful prefill FLOPs of a step (4 D per visible query-key pair)
-divided by the step time.
-
-A classifier leg times the offline head classification of all 28 layers of a
-Qwen2.5-7B-shaped model (seeded synthetic projection weights).
+divided by the step time.  `roofline` is the step's prefill launch, timed by
+HIP events around that launch on its stream, against the bf16 MFMA peak, with
+the useful and the computed-tile FLOP counts.
 
 A decode leg runs the Llama-3-8B-shaped batch (32 query heads, 8 KV heads of
 which 4 streaming, batch 8, 131072-token contexts on a paged cache of shuffled
 16-token pages, ring n_sink 64 + window 1024) for 64 single-token steps and
 reports KV GB/s and tokens/s.  Both legs are also run all-retrieval with the
-same kernels for the speedup.  Inputs are seeded synthetic data (synth) and
-resident in HBM before timing.  One JSON line goes to stdout; progress goes to
+same kernels for the speedup.  A stack leg runs decode steps through the 28
+layers of a 262144-token Qwen2.5-7B-shaped stack (eager and as one HIP graph)
+and one layer's prefill, with the resident KV of the 28 layers; a sweep leg
+runs the 16-sequence variable-length workload (packed prefill and 32 batched
+decode steps per setting); a classifier leg times the offline head
+classification of a 28-layer model.  Inputs are seeded synthetic data (synth)
+and resident in HBM before timing.  One JSON line goes to stdout; progress goes to
 stderr.
 """
 import argparse
