@@ -114,26 +114,30 @@ def copy_calibration():
 
 # HBM traffic per launch measured with rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE
 # (KiB per dispatch), divided by the ratio those counters read for a plain
-# 1 GiB copy (bench.py --copy-calibration), and the hash of the kernel sources
-# they were taken on: a source change makes the figure stale and it is dropped.
+# 1 GiB copy (bench.py --copy-calibration).  Each figure carries the hash of
+# the sources its kernel is built from: a change to them makes the figure
+# stale and it is dropped.
+PREFILL_SOURCES = ("prefill.hip", "aoh_device.h", "aoh_internal.h")
+DECODE_SOURCES = ("decode.hip", "aoh_device.h", "aoh_internal.h")
 TRAFFIC = {
-    "source_hash": "9108489038aaa09d",
     "fetch_factor": 524301.2 / 1048576.0,   # FETCH_SIZE of a 1 GiB copy / 1 GiB
     "write_factor": 1048576.0 / 1048576.0,  # WRITE_SIZE of a 1 GiB copy / 1 GiB
-    "prefill_retrieval": {"fetch_kib": 325257.7, "write_kib": 114688.0},
-    "decode_split": {"fetch_kib": 1078223.1, "write_kib": 1224.1},
+    "prefill_mixed": {"fetch_kib": 459489.5, "write_kib": 263253.5,
+                      "sources": PREFILL_SOURCES, "source_hash": "c63d0cc6ab386835"},
+    "decode_split": {"fetch_kib": 1078214.7, "write_kib": 1224.1,
+                     "sources": DECODE_SOURCES, "source_hash": "57f114fe30e953c0"},
 }
 
 
-def kernel_source_hash(read=None):
-    """Hash of the kernel sources the traffic figures were measured on: their
-    code lines, with // comments and blank lines dropped (comments do not
-    change the kernels)."""
+def kernel_source_hash(names, read=None):
+    """Hash of the kernel sources a traffic figure was measured on: their code
+    lines, with // comments and blank lines dropped (comments do not change
+    the kernels)."""
     import hashlib
     import re
     root = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2608_06849_amd", "csrc")
     h = hashlib.sha256()
-    for name in ("prefill.hip", "decode.hip", "aoh_device.h", "aoh_internal.h"):
+    for name in names:
         if read is None:
             with open(os.path.join(root, name), "rb") as f:
                 text = f.read().decode()
@@ -147,9 +151,9 @@ def kernel_source_hash(read=None):
 
 
 def traffic_for(kernel):
-    if TRAFFIC is None or TRAFFIC.get("source_hash") != kernel_source_hash():
+    t = TRAFFIC.get(kernel) if TRAFFIC else None
+    if t is None or t["source_hash"] != kernel_source_hash(t["sources"]):
         return None
-    t = TRAFFIC[kernel]
     return round((t["fetch_kib"] / TRAFFIC["fetch_factor"] + t["write_kib"] / TRAFFIC["write_factor"]) * 1024)
 
 
