@@ -102,14 +102,15 @@ aoh_status check_mask_params(int n_sink, int window) {
   return AOH_OK;
 }
 
-// Decode split plan.  A paged split is split_blocks_full 16-token blocks
-// (even, so a wave always reads whole 32-token chunks).  The split count per
-// (sequence, KV head) aims at ~kTargetWaves paged waves over the whole launch
-// (8 per CU: enough loads in flight to stream HBM), never above kMaxSplits.
-// The ring is cut the same way with ~kTargetWaves / 8 waves.  n_ret (retrieval
-// KV heads) may be unknown (workspace sizing): then the plan for n_ret = 1 is
-// used, which has the most splits and so bounds every real plan.
-constexpr int kDecodeTargetWaves = 2048;
+// Decode split plan from the cache capacity.  A paged split is
+// split_blocks_full 16-token blocks (even, so a wave always reads whole
+// 32-token chunks).  The split count per (sequence, KV head) aims at
+// ~kDecodeTargetWaves paged waves over the whole launch (enough loads in
+// flight to stream HBM), never above kMaxSplits; the ring is cut the same way
+// (its wave count below).  n_ret (retrieval KV heads) may be unknown
+// (workspace sizing): then the plan for n_ret = 0, n_str = 1 is used,
+// which has the most splits of either type (its paged items are cut as for
+// one KV head, its ring as the whole step) and so bounds every real plan.
 struct SplitPlan {
   int split_blocks_full, n_splits_full;
   int split_blocks_ring, n_splits_ring;
@@ -126,8 +127,15 @@ SplitPlan plan_splits(int batch, int max_pages, int ring_cap, int n_ret, int n_s
   p.split_blocks_full = sb;
   p.n_splits_full = (int)ceil_div(max_pages, sb);
   p.ring_blocks = (int)ceil_div(std::max(ring_cap, 1), kPageTokens);
-  const int64_t per_head_ring =
-      std::max<int64_t>(1, (int64_t)(kDecodeTargetWaves / 8) / ((int64_t)batch * std::max(n_str, 1)));
+  // Ring waves: at least kDecodeTargetWaves / 8, more when the rings hold a
+  // larger share of the step's blocks at full length (up to
+  // kBalancedTargetWaves for rings alone), so a ring wave does not outlast
+  // the paged ones.
+  const int64_t ring_work = (int64_t)std::max(n_str, 1) * p.ring_blocks;
+  const int64_t paged_work = (int64_t)n_ret * max_pages;
+  const int64_t ring_target = std::max<int64_t>(kDecodeTargetWaves / 8,
+                                                kBalancedTargetWaves * ring_work / (ring_work + paged_work));
+  const int64_t per_head_ring = std::max<int64_t>(1, ring_target / ((int64_t)batch * std::max(n_str, 1)));
   const int target_ring = (int)std::min<int64_t>(per_head_ring, kMaxSplits);
   int sbr = (int)std::max<int64_t>(2, ceil_div(p.ring_blocks, target_ring));
   sbr += sbr & 1;
@@ -427,7 +435,7 @@ size_t aoh_decode_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t d_he
   if (batch < 1 || n_q_heads < 1 || (d_head != 64 && d_head != 128) || max_pages_per_seq < 1 ||
       ring_capacity < 0)
     return 0;
-  return workspace_bytes(batch, n_q_heads, d_head, plan_splits(batch, max_pages_per_seq, ring_capacity, 1, 1));
+  return workspace_bytes(batch, n_q_heads, d_head, plan_splits(batch, max_pages_per_seq, ring_capacity, 0, 1));
 }
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -531,8 +539,8 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
   // ceil(top_k / 16) blocks.
   const int plan_pages = x.mode == kReuse ? (int)ceil_div(x.top_k, kPageTokens) : max_pages;
   const SplitPlan sp = plan_splits((int)B, plan_pages, ring_cap, hs.n_ret, hs.n_str);
-  // The workspace is sized for the n_ret = n_str = 1 plan, which bounds this one.
-  const SplitPlan sp_bound = plan_splits((int)B, plan_pages, ring_cap, 1, 1);
+  // The workspace is sized for the n_ret = 0, n_str = 1 plan, which bounds this one.
+  const SplitPlan sp_bound = plan_splits((int)B, plan_pages, ring_cap, 0, 1);
 
   DecodeArgs a;
   std::memset(&a, 0, sizeof(a));
@@ -551,6 +559,18 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
     c.n_groups = (int)ceil_div(sp.n_splits_full, kSplitWaves);
     c.n_items = (int)(B * hs.n_ret * c.n_groups);
     std::memcpy(c.kv_heads, hs.ret, hs.n_ret);
+    // Batches of mixed lengths: a plan cut from the capacity sizes every
+    // sequence's splits for the longest one, so most waves of the shorter ones
+    // find no token.  For 2 to kBalancedMaxBatch sequences the split length
+    // follows the step's total length on the device instead (decode.hip); its
+    // workgroups number at most kBalancedTargetWaves / kSplitWaves + one partly
+    // filled group per (sequence, KV head), and at most one per two-block split
+    // per wave at full capacity, which sizes the grid.
+    if (x.mode != kReuse && B >= 2 && B <= kBalancedMaxBatch && B * (int64_t)max_pages < (1ll << 30)) {
+      a.bal_max_groups = std::min(kMaxSplits / kSplitWaves, sp_bound.max_splits);
+      c.n_items = (int)std::min<int64_t>(kBalancedTargetWaves / kSplitWaves + (int64_t)hs.n_ret * B,
+                                         (int64_t)hs.n_ret * B * ceil_div(max_pages, 2 * kSplitWaves));
+    }
   }
   if (hs.n_str) {
     CacheView& c = a.ring;
@@ -658,6 +678,7 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
   // reuse: a retrieval head's "length" is its number of borrowed entries
   m.max_len = x.mode == kReuse ? x.top_k : max_pages * kPageTokens;
   m.ring_cap = ring_cap;
+  m.bal_max_groups = a.bal_max_groups; m.bal_n_ret = hs.n_ret; m.bal_max_pages = max_pages;
   m.streaming_mask = hs.streaming_mask;
   m.ml_out = ml;
   const int out_f32 = out->dtype == AOH_F32;

@@ -25,12 +25,95 @@
 
 namespace aoh {
 
+// Folds one 32-token chunk (token blocks c and c + 1 of the cache row; tokens
+// at or past tok_end masked, none of them at or past blk_end * 16 kept as a
+// score) into a wave's running softmax state: K rows in kcur, the V^T operand
+// in vcur (zeroed where masked), Q^T in qreg.
+template <int D, bool SCORES>
+__device__ __forceinline__ void fold_chunk(const DecodeArgs& a, const u32x4 (&kcur)[2][D / 32],
+                                           u32x4 (&vcur)[D / 16], const bf16x8 (&qreg)[D / 32], int c, int tok_end,
+                                           int blk_end, bool head_ok, float* score_row, f32x4 (&acc)[D / 16],
+                                           float& m_run, float& l_run) {
+  constexpr int kKSteps = D / 32;
+  constexpr int kDimBlocks = D / 16;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int G = lane >> 4;
+  // S^T for the two 16-token blocks.
+  f32x4 sc[2];
+#pragma unroll
+  for (int X = 0; X < 2; ++X) {
+    sc[X] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < kKSteps; ++s) sc[X] = mfma16(__builtin_bit_cast(bf16x8, kcur[X][s]), qreg[s], sc[X]);
+  }
+  // This lane's 8 scores: chunk tokens 8G + j, j = 4X + i.
+  const int tok0 = c * kPage + 8 * G;
+  const bool partial = (c * kPage + 2 * kPage) > tok_end;
+  float x[8];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int X = 0; X < 2; ++X)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float v = sc[X][i] * a.scale_log2;
+      if (partial && tok0 + 4 * X + i >= tok_end) v = -INFINITY;
+      x[4 * X + i] = v;
+      mx = fmaxf(mx, v);
+    }
+  if (SCORES) {
+    // Anchor layer: keep the scaled scores for the top-k selection.  Every
+    // lane issues the same two stores in every chunk (a fixed count, so the
+    // compiler's wait for the prefetched chunk stays exact): lanes without a
+    // query head, and lanes whose tokens lie past the range's last block (the
+    // missing second block of a range with an odd block count, which at the
+    // end of a full row would be the next row's first positions), write to a
+    // dummy area; masked positions before that (beyond the valid length,
+    // never read by the selection) get -inf.
+    float* sp = (head_ok && tok0 < blk_end * kPage) ? score_row + tok0 : a.score_dummy + 8 * lane;
+    *reinterpret_cast<f32x4*>(sp) = f32x4{x[0], x[1], x[2], x[3]};
+    *reinterpret_cast<f32x4*>(sp + 4) = f32x4{x[4], x[5], x[6], x[7]};
+  }
+  mx = wave_xor_max(mx, 16);
+  mx = wave_xor_max(mx, 32);
+  const float m_new = fmaxf(m_run, mx);  // finite: every chunk holds a valid token
+  const float alpha = fast_exp2(m_run - m_new);
+  m_run = m_new;
+  bf16x8 pop;
+  float psum = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const float p = fast_exp2(x[j] - m_new);
+    psum += p;
+    pop[j] = f32_to_bf16(p);
+  }
+  l_run = l_run * alpha + psum;
+  if (partial) {
+    // Slots past the valid range may hold stale or uninitialised data: zero
+    // their V so 0 * garbage cannot poison the product.
+#pragma unroll
+    for (int nb = 0; nb < kDimBlocks; ++nb) {
+      bf16x8 vv = __builtin_bit_cast(bf16x8, vcur[nb]);
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (tok0 + j >= tok_end) vv[j] = (bf16)0.f;
+      vcur[nb] = __builtin_bit_cast(u32x4, vv);
+    }
+  }
+#pragma unroll
+  for (int nb = 0; nb < kDimBlocks; ++nb) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[nb][i] *= alpha;
+    acc[nb] = mfma16(__builtin_bit_cast(bf16x8, vcur[nb]), pop, acc[nb]);
+  }
+}
+
 // One split of the cache of (sequence b, KV head kvl) for one wave; its
 // partial results (unnormalised acc, running max m in log2 units, sum l) are
 // left in acc / m_out / l_out (unchanged when the split holds no token).
 template <int D, bool RING, bool SCORES = false, bool APPEND = false>
 __device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const CacheView& cv, int b, int kvl,
-                                                  int split, f32x4 (&acc)[D / 16], float& m_out, float& l_out) {
+                                                  int len, int split, int split_blocks, f32x4 (&acc)[D / 16],
+                                                  float& m_out, float& l_out) {
   constexpr int kKSteps = D / 32;   // 32-dim k-steps for Q K^T
   constexpr int kDimBlocks = D / 16;
   const int g = cv.kv_heads[kvl];
@@ -39,12 +122,11 @@ __device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const Cac
   const int col = lane & 15;   // query head within the group (MFMA column)
   const int G = lane >> 4;     // lane group
 
-  const int len = a.lens[b];
   // Lengths beyond the cache capacity are clamped so no read leaves the cache.
   const int n_valid = RING ? min(len, a.ring_cap) : min(len, cv.max_pages * kPage);
   const int n_blocks_valid = (n_valid + kPage - 1) / kPage;
-  const int blk0 = split * cv.split_blocks;
-  const int blk_end = min(blk0 + cv.split_blocks, n_blocks_valid);
+  const int blk0 = split * split_blocks;
+  const int blk_end = min(blk0 + split_blocks, n_blocks_valid);
   if (blk0 >= blk_end) return;
   const int tok_end = min(n_valid, blk_end * kPage);
 
@@ -166,74 +248,8 @@ __device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const Cac
       if (c + 4 < blk_end) fetch_entries(c + 4, ent);  // entries of chunk c + 4
     }
 
-    // S^T for the two 16-token blocks.
-    f32x4 sc[2];
-#pragma unroll
-    for (int X = 0; X < 2; ++X) {
-      sc[X] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s = 0; s < kKSteps; ++s) sc[X] = mfma16(__builtin_bit_cast(bf16x8, kcur[X][s]), qreg[s], sc[X]);
-    }
-    // This lane's 8 scores: chunk tokens 8G + j, j = 4X + i.
-    const int tok0 = c * kPage + 8 * G;
-    const bool partial = (c * kPage + 2 * kPage) > tok_end;
-    float x[8];
-    float mx = -INFINITY;
-#pragma unroll
-    for (int X = 0; X < 2; ++X)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float v = sc[X][i] * a.scale_log2;
-        if (partial && tok0 + 4 * X + i >= tok_end) v = -INFINITY;
-        x[4 * X + i] = v;
-        mx = fmaxf(mx, v);
-      }
-    if (SCORES) {
-      // Anchor layer: keep the scaled scores for the top-k selection.  Every
-      // lane issues the same two stores in every chunk (a fixed count, so the
-      // compiler's wait for the prefetched chunk stays exact): lanes without a
-      // query head, and lanes whose tokens lie past the split's last block (the
-      // missing second block of a split with an odd block count, which at the
-      // end of a full row would be the next row's first positions), write to a
-      // dummy area; masked positions before that (beyond the valid length,
-      // never read by the selection) get -inf.
-      float* sp = (head_ok && tok0 < blk_end * kPage) ? a.scores + ((int64_t)b * a.Hq + hq) * a.score_len + tok0
-                                                       : a.score_dummy + 8 * lane;
-      *reinterpret_cast<f32x4*>(sp) = f32x4{x[0], x[1], x[2], x[3]};
-      *reinterpret_cast<f32x4*>(sp + 4) = f32x4{x[4], x[5], x[6], x[7]};
-    }
-    mx = wave_xor_max(mx, 16);
-    mx = wave_xor_max(mx, 32);
-    const float m_new = fmaxf(m_run, mx);  // finite: every chunk holds a valid token
-    const float alpha = fast_exp2(m_run - m_new);
-    m_run = m_new;
-    bf16x8 pop;
-    float psum = 0.f;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const float p = fast_exp2(x[j] - m_new);
-      psum += p;
-      pop[j] = f32_to_bf16(p);
-    }
-    l_run = l_run * alpha + psum;
-    if (partial) {
-      // Slots past the valid range may hold stale or uninitialised data: zero
-      // their V so 0 * garbage cannot poison the product.
-#pragma unroll
-      for (int nb = 0; nb < kDimBlocks; ++nb) {
-        bf16x8 vv = __builtin_bit_cast(bf16x8, vcur[nb]);
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-          if (tok0 + j >= tok_end) vv[j] = (bf16)0.f;
-        vcur[nb] = __builtin_bit_cast(u32x4, vv);
-      }
-    }
-#pragma unroll
-    for (int nb = 0; nb < kDimBlocks; ++nb) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) acc[nb][i] *= alpha;
-      acc[nb] = mfma16(__builtin_bit_cast(bf16x8, vcur[nb]), pop, acc[nb]);
-    }
+    fold_chunk<D, SCORES>(a, kcur, vcur, qreg, c, tok_end, blk_end, head_ok,
+                          SCORES ? a.scores + ((int64_t)b * a.Hq + hq) * a.score_len : nullptr, acc, m_run, l_run);
   }
 
   // Partial results of this split: m (log2 units), l, acc[D] for each head.
@@ -373,6 +389,34 @@ __device__ __forceinline__ void decode_sparse_body(const DecodeArgs& a, const Ca
   l_out = l_tot;
 }
 
+// Length-balanced split length of the paged items (see the host plan).  Every
+// lane of a wave calls it; lane b gets sequence b's length (len) and valid
+// 16-token block count (nb), zeros for lanes >= B.  The split length makes
+// about kBalancedTargetWaves waves over all sequences and KV heads, and no
+// sequence more than max_groups workgroups (its partial slots).  Returns
+// blocks per split (even, >= 2).
+__device__ __forceinline__ int balanced_split_blocks(const int32_t* lens, int B, int max_pages, int n_kv,
+                                                     int max_groups, int& len, int& nb) {
+  const int lane = threadIdx.x & (kWave - 1);
+  len = 0;
+  nb = 0;
+  if (lane < B) {
+    len = lens[lane];
+    nb = (min(max(len, 0), max_pages * kPage) + kPage - 1) / kPage;
+  }
+  int sum = nb, mx = nb;
+#pragma unroll
+  for (int o = kWave / 2; o > 0; o >>= 1) {
+    sum += __shfl_xor(sum, o, kWave);
+    mx = max(mx, __shfl_xor(mx, o, kWave));
+  }
+  const int64_t want = ((int64_t)n_kv * sum + kBalancedTargetWaves - 1) / kBalancedTargetWaves;
+  const int per_group = kSplitWaves * max_groups;
+  int sb = (int)max(max(want, (int64_t)2), (int64_t)((mx + per_group - 1) / per_group));
+  sb += sb & 1;
+  return __builtin_amdgcn_readfirstlane(sb);
+}
+
 // One launch for both cache types: paged-cache items first, ring items last.
 // MODE 0: plain decode; 1: anchor layer (paged items also keep their scores);
 // 2: reuse layer (paged items attend to borrowed positions only); 3: plain
@@ -395,20 +439,46 @@ __global__ __launch_bounds__(kSplitWaves * kWave, 2) void decode_split_bf16_kern
   const bool ring = wg >= a.full.n_items;
   if (ring) wg -= a.full.n_items;
   const CacheView& cv = ring ? a.ring : a.full;
-  const int sg = wg % cv.n_groups;
-  const int rest = wg / cv.n_groups;
-  const int kvl = rest % cv.n_kv;
-  const int b = rest / cv.n_kv;
+  int b, kvl, sg, len, split_blocks = cv.split_blocks, n_splits = cv.n_splits;
+  if (MODE != 2 && !ring && a.bal_max_groups) {
+    // Length-balanced paged items in (sequence, KV head, group) order with
+    // G_b groups per head of sequence b: find b from the running item count.
+    int len_lane, nb;
+    split_blocks = balanced_split_blocks(a.lens, a.B, cv.max_pages, cv.n_kv, a.bal_max_groups, len_lane, nb);
+    const int span = kSplitWaves * split_blocks;
+    const int groups = (nb + span - 1) / span;
+    int incl = groups * cv.n_kv;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int t = __shfl_up(incl, o, kWave);
+      if (lane >= o) incl += t;
+    }
+    const uint64_t past = __ballot(incl > wg);
+    if (past == 0) return;  // beyond this step's items (the same for every wave of the group)
+    b = __builtin_amdgcn_readfirstlane((int)__builtin_ctzll(past));
+    len = __builtin_amdgcn_readlane(len_lane, b);
+    const int gb = __builtin_amdgcn_readlane(groups, b);
+    const int r = wg - (__builtin_amdgcn_readlane(incl, b) - gb * cv.n_kv);
+    kvl = r / gb;
+    sg = r % gb;
+    n_splits = gb * kSplitWaves;
+  } else {
+    sg = wg % cv.n_groups;
+    const int rest = wg / cv.n_groups;
+    kvl = rest % cv.n_kv;
+    b = rest / cv.n_kv;
+    len = a.lens[b];
+  }
   const int split = sg * kSplitWaves + wave;
 
   f32x4 acc[kDimBlocks];
 #pragma unroll
   for (int nb = 0; nb < kDimBlocks; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m = -INFINITY, l = 0.f;
-  if (split < cv.n_splits) {
-    if (ring) decode_split_body<D, true, false, MODE == 3>(a, a.ring, b, kvl, split, acc, m, l);
+  if (split < n_splits) {
+    if (ring) decode_split_body<D, true, false, MODE == 3>(a, a.ring, b, kvl, len, split, split_blocks, acc, m, l);
     else if (MODE == 2) decode_sparse_body<D>(a, a.full, b, kvl, split, acc, m, l);
-    else decode_split_body<D, false, MODE == 1, MODE == 3>(a, a.full, b, kvl, split, acc, m, l);
+    else decode_split_body<D, false, MODE == 1, MODE == 3>(a, a.full, b, kvl, len, split, split_blocks, acc, m, l);
   }
 #pragma unroll
   for (int nb = 0; nb < kDimBlocks; ++nb) s_acc[wave][nb][lane] = acc[nb];
@@ -568,8 +638,15 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(MergeArgs a
   const bool streaming = (a.streaming_mask >> g) & 1ull;
   const int len = a.lens[b];
   const int n_valid = streaming ? min(len, a.ring_cap) : min(len, a.max_len);
-  const int split_tok = streaming ? a.split_tokens_ring : a.split_tokens_full;
-  const int ns = min((n_valid + split_tok - 1) / split_tok, streaming ? a.n_splits_ring : a.n_splits_full);
+  int split_tok = streaming ? a.split_tokens_ring : a.split_tokens_full;
+  int max_ns = streaming ? a.n_splits_ring : a.n_splits_full;
+  if (!streaming && a.bal_max_groups) {  // the split pass's length-balanced plan
+    int len_lane, nb;
+    split_tok = kSplitWaves * kPage *
+                balanced_split_blocks(a.lens, a.B, a.bal_max_pages, a.bal_n_ret, a.bal_max_groups, len_lane, nb);
+    max_ns = a.bal_max_groups;
+  }
+  const int ns = min((n_valid + split_tok - 1) / split_tok, max_ns);
   const int64_t base = ((int64_t)b * a.Hq + hq) * a.max_splits;
   const int dd = tid % kMergeDims, grp = tid / kMergeDims;
   const int d = slice * kMergeDims + dd;
