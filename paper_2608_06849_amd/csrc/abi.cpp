@@ -14,6 +14,7 @@
 // splits so each launch has enough independent waves to fill the GPU.
 #include <cstdarg>
 #include <cstdio>
+#include <atomic>
 #include <cstring>
 #include <algorithm>
 #include <cmath>
@@ -41,6 +42,20 @@ aoh_status ok() {
 }
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Compute units of the current device, queried once per device (256 on an
+// MI355X, also the answer when the query fails).
+int compute_units() {
+  constexpr int kMaxDevices = 64;
+  static std::atomic<int> cached[kMaxDevices];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
+  int n = cached[dev].load(std::memory_order_relaxed);
+  if (n > 0) return n;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+  cached[dev].store(n, std::memory_order_relaxed);
+  return n;
+}
 
 int elt_size(int dtype) { return dtype == AOH_BF16 ? 2 : 4; }
 
@@ -128,13 +143,12 @@ SplitPlan plan_splits(int batch, int max_pages, int ring_cap, int n_ret, int n_s
   p.n_splits_full = (int)ceil_div(max_pages, sb);
   p.ring_blocks = (int)ceil_div(std::max(ring_cap, 1), kPageTokens);
   // Ring waves: at least kDecodeTargetWaves / 8, more when the rings hold a
-  // larger share of the step's blocks at full length (up to
-  // kBalancedTargetWaves for rings alone), so a ring wave does not outlast
-  // the paged ones.
+  // larger share of the step's blocks at full length (up to kRingTargetWaves
+  // for rings alone), so a ring wave does not outlast the paged ones.
   const int64_t ring_work = (int64_t)std::max(n_str, 1) * p.ring_blocks;
   const int64_t paged_work = (int64_t)n_ret * max_pages;
   const int64_t ring_target = std::max<int64_t>(kDecodeTargetWaves / 8,
-                                                kBalancedTargetWaves * ring_work / (ring_work + paged_work));
+                                                kRingTargetWaves * ring_work / (ring_work + paged_work));
   const int64_t per_head_ring = std::max<int64_t>(1, ring_target / ((int64_t)batch * std::max(n_str, 1)));
   const int target_ring = (int)std::min<int64_t>(per_head_ring, kMaxSplits);
   int sbr = (int)std::max<int64_t>(2, ceil_div(p.ring_blocks, target_ring));
@@ -145,8 +159,12 @@ SplitPlan plan_splits(int batch, int max_pages, int ring_cap, int n_ret, int n_s
   return p;
 }
 
+// Split partials: fixed splits hold [B][Hq][max_splits] partials; the
+// work-space pass (batches up to kWsMaxBatch) at most kWsMaxWgs + B x Hkv
+// slots of gs heads, bounded by (kWsMaxWgs + B) x Hq.
 size_t workspace_bytes(int batch, int hq, int d, const SplitPlan& p) {
-  const size_t slots = (size_t)batch * hq * p.max_splits;
+  size_t slots = (size_t)batch * hq * p.max_splits;
+  if (batch <= kWsMaxBatch) slots = std::max(slots, (size_t)(kWsMaxWgs + batch) * hq);
   const size_t acc = slots * d * sizeof(float);
   return acc + slots * 2 * sizeof(float);
 }
@@ -559,18 +577,6 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
     c.n_groups = (int)ceil_div(sp.n_splits_full, kSplitWaves);
     c.n_items = (int)(B * hs.n_ret * c.n_groups);
     std::memcpy(c.kv_heads, hs.ret, hs.n_ret);
-    // Batches of mixed lengths: a plan cut from the capacity sizes every
-    // sequence's splits for the longest one, so most waves of the shorter ones
-    // find no token.  For 2 to kBalancedMaxBatch sequences the split length
-    // follows the step's total length on the device instead (decode.hip); its
-    // workgroups number at most kBalancedTargetWaves / kSplitWaves + one partly
-    // filled group per (sequence, KV head), and at most one per two-block split
-    // per wave at full capacity, which sizes the grid.
-    if (x.mode != kReuse && B >= 2 && B <= kBalancedMaxBatch && B * (int64_t)max_pages < (1ll << 30)) {
-      a.bal_max_groups = std::min(kMaxSplits / kSplitWaves, sp_bound.max_splits);
-      c.n_items = (int)std::min<int64_t>(kBalancedTargetWaves / kSplitWaves + (int64_t)hs.n_ret * B,
-                                         (int64_t)hs.n_ret * B * ceil_div(max_pages, 2 * kSplitWaves));
-    }
   }
   if (hs.n_str) {
     CacheView& c = a.ring;
@@ -636,8 +642,18 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
     return ok();
   }
 
+  // Plain, anchor and fused steps of 2 to kWsMaxBatch sequences split the
+  // step's work space on the device (two workgroups per CU), which follows any
+  // mix of lengths; one sequence (no mix to follow, and the plan's cost shows
+  // in its short steps), larger batches and the reuse layer take fixed splits
+  // from the cache capacity.
+  const int64_t ws_blocks = std::max<int64_t>(max_pages, sp.ring_blocks);
+  if (x.mode != kReuse && B >= 2 && B <= kWsMaxBatch && B * Hkv * ws_blocks < (1ll << 30))
+    a.ws_cu = std::min(compute_units(), kWsMaxWgs / 2);
   float* part_acc = reinterpret_cast<float*>(workspace);
-  float* part_ml = part_acc + (size_t)B * Hq * sp_bound.max_splits * D;
+  const size_t acc_floats = a.ws_cu ? (size_t)(2 * a.ws_cu + B * Hkv) * gs * D
+                                    : (size_t)B * Hq * sp_bound.max_splits * D;
+  float* part_ml = part_acc + acc_floats;
   a.part_acc = part_acc; a.part_ml = part_ml; a.max_splits = sp_bound.max_splits;
   float* scores = nullptr;
   float* ml = nullptr;
@@ -678,7 +694,7 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
   // reuse: a retrieval head's "length" is its number of borrowed entries
   m.max_len = x.mode == kReuse ? x.top_k : max_pages * kPageTokens;
   m.ring_cap = ring_cap;
-  m.bal_max_groups = a.bal_max_groups; m.bal_n_ret = hs.n_ret; m.bal_max_pages = max_pages;
+  m.ws_cu = a.ws_cu; m.ws_n_ret = hs.n_ret; m.ws_n_str = hs.n_str; m.ws_max_pages = max_pages;
   m.streaming_mask = hs.streaming_mask;
   m.ml_out = ml;
   const int out_f32 = out->dtype == AOH_F32;

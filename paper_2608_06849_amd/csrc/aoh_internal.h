@@ -76,10 +76,9 @@ struct DecodeArgs {
   int32_t B, Hq, gs;
   int32_t ring_cap;             // n_sink + window
   int32_t max_splits;
-  // > 0: the paged items follow the length-balanced plan (split length from
-  // this step's lengths; full.n_items an upper bound on its workgroups), and
-  // no (sequence, head) takes more than this many partials.
-  int32_t bal_max_groups;
+  // > 0: the work-space split pass (decode_ws_kernel) with 2 * ws_cu
+  // workgroups; part_acc / part_ml then hold [slot][gs][D] / [slot][gs][2].
+  int32_t ws_cu;
   float scale_log2;
   float scale;
   CacheView full;
@@ -117,9 +116,9 @@ struct MergeArgs {
   int32_t n_splits_ring;        // partials written per (b, head), ring
   int32_t max_len;              // 16 * pages per sequence: lens are clamped to it
   int32_t ring_cap;
-  // > 0: paged partials come from the length-balanced plan over bal_n_ret
-  // paged KV heads of bal_max_pages pages per sequence (DecodeArgs).
-  int32_t bal_max_groups, bal_n_ret, bal_max_pages;
+  // > 0: partials of the work-space split pass (DecodeArgs::ws_cu) over
+  // ws_n_ret paged KV heads of ws_max_pages pages and ws_n_str rings.
+  int32_t ws_cu, ws_n_ret, ws_n_str, ws_max_pages;
   uint64_t streaming_mask;      // bit g set = KV head g streaming
   float* ml_out;                // anchor layer: final (m, l) of each paged-cache head, [B][Hq][2]
 };
@@ -222,13 +221,15 @@ constexpr int kMaxSplits = 1024;
 // Decode split pass: waves per workgroup, one split each; the workgroup merges
 // its waves' partial results in LDS and writes one partial per group.
 constexpr int kSplitWaves = 4;
-// Splits of a decode launch: ~kDecodeTargetWaves paged waves when the plan is
-// cut from the cache capacity (8 per CU), ~kBalancedTargetWaves when it
-// follows the step's lengths on the device, for batches of 2 to
-// kBalancedMaxBatch sequences (one lane per sequence).
+// Fixed decode splits: ~kDecodeTargetWaves paged waves (8 per CU), and ring
+// waves up to kRingTargetWaves by the rings' share of the work.
 constexpr int kDecodeTargetWaves = 2048;
-constexpr int kBalancedTargetWaves = 4096;
-constexpr int kBalancedMaxBatch = 64;
+constexpr int kRingTargetWaves = 4096;
+// Work-space decode split pass: batches of 2 to kWsMaxBatch sequences (one
+// lane per sequence), at most kWsMaxWgs workgroups (two per CU), so at most
+// that many partials per item for the merge pass.
+constexpr int kWsMaxBatch = 64;
+constexpr int kWsMaxWgs = 512;
 
 // Query rows per bf16 prefill workgroup, and 32-row MFMA blocks per wave
 // (the workgroup has kPrefillRows / (32 * kPrefillRB) waves).

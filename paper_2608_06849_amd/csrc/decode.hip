@@ -107,12 +107,13 @@ __device__ __forceinline__ void fold_chunk(const DecodeArgs& a, const u32x4 (&kc
   }
 }
 
-// One split of the cache of (sequence b, KV head kvl) for one wave; its
+// Blocks [blk0, blk_lim) of the cache row of (sequence b, KV head kvl) for
+// one wave (blk0 even in the row or at the start of a workgroup's share); its
 // partial results (unnormalised acc, running max m in log2 units, sum l) are
 // left in acc / m_out / l_out (unchanged when the split holds no token).
 template <int D, bool RING, bool SCORES = false, bool APPEND = false>
 __device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const CacheView& cv, int b, int kvl,
-                                                  int len, int split, int split_blocks, f32x4 (&acc)[D / 16],
+                                                  int len, int blk0, int blk_lim, f32x4 (&acc)[D / 16],
                                                   float& m_out, float& l_out) {
   constexpr int kKSteps = D / 32;   // 32-dim k-steps for Q K^T
   constexpr int kDimBlocks = D / 16;
@@ -125,8 +126,7 @@ __device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const Cac
   // Lengths beyond the cache capacity are clamped so no read leaves the cache.
   const int n_valid = RING ? min(len, a.ring_cap) : min(len, cv.max_pages * kPage);
   const int n_blocks_valid = (n_valid + kPage - 1) / kPage;
-  const int blk0 = split * split_blocks;
-  const int blk_end = min(blk0 + split_blocks, n_blocks_valid);
+  const int blk_end = min(blk_lim, n_blocks_valid);
   if (blk0 >= blk_end) return;
   const int tok_end = min(n_valid, blk_end * kPage);
 
@@ -389,34 +389,6 @@ __device__ __forceinline__ void decode_sparse_body(const DecodeArgs& a, const Ca
   l_out = l_tot;
 }
 
-// Length-balanced split length of the paged items (see the host plan).  Every
-// lane of a wave calls it; lane b gets sequence b's length (len) and valid
-// 16-token block count (nb), zeros for lanes >= B.  The split length makes
-// about kBalancedTargetWaves waves over all sequences and KV heads, and no
-// sequence more than max_groups workgroups (its partial slots).  Returns
-// blocks per split (even, >= 2).
-__device__ __forceinline__ int balanced_split_blocks(const int32_t* lens, int B, int max_pages, int n_kv,
-                                                     int max_groups, int& len, int& nb) {
-  const int lane = threadIdx.x & (kWave - 1);
-  len = 0;
-  nb = 0;
-  if (lane < B) {
-    len = lens[lane];
-    nb = (min(max(len, 0), max_pages * kPage) + kPage - 1) / kPage;
-  }
-  int sum = nb, mx = nb;
-#pragma unroll
-  for (int o = kWave / 2; o > 0; o >>= 1) {
-    sum += __shfl_xor(sum, o, kWave);
-    mx = max(mx, __shfl_xor(mx, o, kWave));
-  }
-  const int64_t want = ((int64_t)n_kv * sum + kBalancedTargetWaves - 1) / kBalancedTargetWaves;
-  const int per_group = kSplitWaves * max_groups;
-  int sb = (int)max(max(want, (int64_t)2), (int64_t)((mx + per_group - 1) / per_group));
-  sb += sb & 1;
-  return __builtin_amdgcn_readfirstlane(sb);
-}
-
 // One launch for both cache types: paged-cache items first, ring items last.
 // MODE 0: plain decode; 1: anchor layer (paged items also keep their scores);
 // 2: reuse layer (paged items attend to borrowed positions only); 3: plain
@@ -426,69 +398,27 @@ __device__ __forceinline__ int balanced_split_blocks(const int32_t* lens, int B,
 // weights, as in the merge pass) and the group writes one partial, so the
 // merge pass reads kSplitWaves times fewer.  Each wave then combines a share
 // of the dimension blocks.
-template <int D, int MODE>
-__global__ __launch_bounds__(kSplitWaves * kWave, 2) void decode_split_bf16_kernel(DecodeArgs a) {
+// The kSplitWaves waves' partial states (acc, m in log2 units, l) merged in
+// LDS with log-sum-exp weights; lane (col, G) holds query head col of the
+// group, and each wave writes a share of the dimension blocks of the merged
+// partial to row `row` of part_acc / part_ml (lanes with lane_ok).  A wave
+// without tokens has m = -inf and weight 0; if no wave has tokens the row gets
+// m = -inf (the merge pass never reads such a row).  Starts with a barrier so
+// a workgroup can call it once per segment.
+template <int D>
+__device__ __forceinline__ void merge_waves_store(const DecodeArgs& a, f32x4 (&acc)[D / 16], float m, float l,
+                                                  f32x4 (*s_acc)[D / 16][kWave], float (*s_m)[kWave],
+                                                  float (*s_l)[kWave], bool lane_ok, int64_t row) {
   constexpr int kDimBlocks = D / 16;
   static_assert(kDimBlocks % kSplitWaves == 0, "dimension blocks split evenly over the waves");
-  __shared__ f32x4 s_acc[kSplitWaves][kDimBlocks][kWave];
-  __shared__ float s_m[kSplitWaves][kWave];
-  __shared__ float s_l[kSplitWaves][kWave];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & (kWave - 1);
-  int wg = blockIdx.x;
-  const bool ring = wg >= a.full.n_items;
-  if (ring) wg -= a.full.n_items;
-  const CacheView& cv = ring ? a.ring : a.full;
-  int b, kvl, sg, len, split_blocks = cv.split_blocks, n_splits = cv.n_splits;
-  if (MODE != 2 && !ring && a.bal_max_groups) {
-    // Length-balanced paged items in (sequence, KV head, group) order with
-    // G_b groups per head of sequence b: find b from the running item count.
-    int len_lane, nb;
-    split_blocks = balanced_split_blocks(a.lens, a.B, cv.max_pages, cv.n_kv, a.bal_max_groups, len_lane, nb);
-    const int span = kSplitWaves * split_blocks;
-    const int groups = (nb + span - 1) / span;
-    int incl = groups * cv.n_kv;
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-      const int t = __shfl_up(incl, o, kWave);
-      if (lane >= o) incl += t;
-    }
-    const uint64_t past = __ballot(incl > wg);
-    if (past == 0) return;  // beyond this step's items (the same for every wave of the group)
-    b = __builtin_amdgcn_readfirstlane((int)__builtin_ctzll(past));
-    len = __builtin_amdgcn_readlane(len_lane, b);
-    const int gb = __builtin_amdgcn_readlane(groups, b);
-    const int r = wg - (__builtin_amdgcn_readlane(incl, b) - gb * cv.n_kv);
-    kvl = r / gb;
-    sg = r % gb;
-    n_splits = gb * kSplitWaves;
-  } else {
-    sg = wg % cv.n_groups;
-    const int rest = wg / cv.n_groups;
-    kvl = rest % cv.n_kv;
-    b = rest / cv.n_kv;
-    len = a.lens[b];
-  }
-  const int split = sg * kSplitWaves + wave;
-
-  f32x4 acc[kDimBlocks];
-#pragma unroll
-  for (int nb = 0; nb < kDimBlocks; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m = -INFINITY, l = 0.f;
-  if (split < n_splits) {
-    if (ring) decode_split_body<D, true, false, MODE == 3>(a, a.ring, b, kvl, len, split, split_blocks, acc, m, l);
-    else if (MODE == 2) decode_sparse_body<D>(a, a.full, b, kvl, split, acc, m, l);
-    else decode_split_body<D, false, MODE == 1, MODE == 3>(a, a.full, b, kvl, len, split, split_blocks, acc, m, l);
-  }
+  __syncthreads();
 #pragma unroll
   for (int nb = 0; nb < kDimBlocks; ++nb) s_acc[wave][nb][lane] = acc[nb];
   s_m[wave][lane] = m;
   s_l[wave][lane] = l;
   __syncthreads();
-
-  // Lane (col, G) holds query head col of the group; the four lane groups of
-  // a column carry the same m and l.  A wave without tokens has m = -inf and
-  // weight 0; a group without tokens (never read by the merge) writes m = -inf.
   float M = -INFINITY;
 #pragma unroll
   for (int w = 0; w < kSplitWaves; ++w) M = fmaxf(M, s_m[w][lane]);
@@ -500,11 +430,9 @@ __global__ __launch_bounds__(kSplitWaves * kWave, 2) void decode_split_bf16_kern
     wt[w] = (mw == -INFINITY) ? 0.f : fast_exp2(mw - M);
     L += wt[w] * s_l[w][lane];
   }
-  const int col = lane & 15, G = lane >> 4;
-  if (col < a.gs) {
-    const int hq = cv.kv_heads[kvl] * a.gs + col;
-    const int64_t slot = ((int64_t)b * a.Hq + hq) * a.max_splits + sg;
-    float* pa = a.part_acc + slot * D;
+  if (lane_ok) {
+    const int G = lane >> 4;
+    float* pa = a.part_acc + row * D;
 #pragma unroll
     for (int k = 0; k < kDimBlocks / kSplitWaves; ++k) {
       const int nb = wave * (kDimBlocks / kSplitWaves) + k;
@@ -518,9 +446,201 @@ __global__ __launch_bounds__(kSplitWaves * kWave, 2) void decode_split_bf16_kern
       *reinterpret_cast<f32x4*>(pa + 16 * nb + 4 * G) = o;
     }
     if (wave == 0 && G == 0) {
-      a.part_ml[slot * 2 + 0] = M;
-      a.part_ml[slot * 2 + 1] = L;
+      a.part_ml[row * 2 + 0] = M;
+      a.part_ml[row * 2 + 1] = L;
     }
+  }
+}
+
+// Fixed splits from the cache capacity (one sequence, batches over
+// kWsMaxBatch sequences, and the reuse layer).  One launch for both cache types: paged-cache items
+// first, ring items last.  MODE 0: plain decode; 1: anchor layer (paged items
+// also keep their scores); 2: reuse layer (paged items attend to borrowed
+// positions only); 3: plain decode that first stores the new token at
+// position lens - 1 (fused step).  A workgroup holds kSplitWaves consecutive
+// splits of one (sequence, KV head), one per wave, and writes one merged
+// partial, so the merge pass reads kSplitWaves times fewer.
+template <int D, int MODE>
+__global__ __launch_bounds__(kSplitWaves * kWave, 2) void decode_split_bf16_kernel(DecodeArgs a) {
+  constexpr int kDimBlocks = D / 16;
+  __shared__ f32x4 s_acc[kSplitWaves][kDimBlocks][kWave];
+  __shared__ float s_m[kSplitWaves][kWave];
+  __shared__ float s_l[kSplitWaves][kWave];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & (kWave - 1);
+  int wg = blockIdx.x;
+  const bool ring = wg >= a.full.n_items;
+  if (ring) wg -= a.full.n_items;
+  const CacheView& cv = ring ? a.ring : a.full;
+  const int sg = wg % cv.n_groups;
+  const int rest = wg / cv.n_groups;
+  const int kvl = rest % cv.n_kv;
+  const int b = rest / cv.n_kv;
+  const int split = sg * kSplitWaves + wave;
+  const int blk0 = split * cv.split_blocks;
+
+  f32x4 acc[kDimBlocks];
+#pragma unroll
+  for (int nb = 0; nb < kDimBlocks; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m = -INFINITY, l = 0.f;
+  if (split < cv.n_splits) {
+    const int len = a.lens[b];
+    if (ring)
+      decode_split_body<D, true, false, MODE == 3>(a, a.ring, b, kvl, len, blk0, blk0 + cv.split_blocks, acc, m, l);
+    else if (MODE == 2)
+      decode_sparse_body<D>(a, a.full, b, kvl, split, acc, m, l);
+    else
+      decode_split_body<D, false, MODE == 1, MODE == 3>(a, a.full, b, kvl, len, blk0, blk0 + cv.split_blocks, acc,
+                                                        m, l);
+  }
+  const int col = lane & 15;
+  const int hq = cv.kv_heads[kvl] * a.gs + col;
+  merge_waves_store<D>(a, acc, m, l, s_acc, s_m, s_l, col < a.gs,
+                       ((int64_t)b * a.Hq + hq) * a.max_splits + sg);
+}
+
+// ---------------------------------------------------------------------------
+// Split pass over the step's work space (bf16 plain, anchor and fused-step
+// decode of 2 to kWsMaxBatch sequences).
+//
+// Work space: the valid 16-token blocks of every item (cache type, sequence,
+// KV head) laid end to end, paged items first, each type in (sequence, KV
+// head) order, so one plan covers any mix of lengths and of the two cache
+// types.  Each workgroup takes one contiguous range of it and each of its
+// waves a consecutive quarter of every item segment in that range; the waves'
+// states are merged in LDS and the workgroup writes one partial per segment.
+// The launch has two workgroups per CU: the first n_cu are placed one per CU,
+// and a CU's second workgroup runs about a third slower (its waves lose issue
+// arbitration on every SIMD to the older ones), so first-round ranges hold 4
+// shares and second-round ranges 3, and both rounds end together.  Item i,
+// covered by workgroups first_i..last_i, has its partials in slots
+// first_i + i .. last_i + i (items are contiguous, so no two items share a
+// slot): at most workgroups + items slots of gs heads each.
+constexpr int kWsMinBlocks = 16;  // smallest range a workgroup takes
+
+struct WsPlan {
+  int nb_tot, nbr_tot;  // paged / ring blocks summed over the sequences
+  int total;            // blocks of all items
+  int n_old, n_young;   // workgroups of the first and second round
+  int r_old, r_young;   // blocks per range of each round
+  int g_young;          // first block of the second round's ranges
+};
+
+// The plan from the sequence lengths.  Every lane of a wave calls it; lane b
+// gets sequence b's length, its valid block counts in the paged cache (nb)
+// and the ring (nbr), and their exclusive prefix sums over the sequences
+// (P, Q); lanes >= B get zeros.
+__device__ __forceinline__ WsPlan ws_plan(const int32_t* lens, int B, int max_pages, int n_ret, int ring_cap,
+                                          int n_str, int n_cu, int& len, int& nb, int& nbr, int& P, int& Q) {
+  const int lane = threadIdx.x & (kWave - 1);
+  len = 0;
+  nb = 0;
+  nbr = 0;
+  if (lane < B) {
+    len = lens[lane];
+    const int l = max(len, 0);
+    if (n_ret) nb = (min(l, max_pages * kPage) + kPage - 1) / kPage;
+    if (n_str) nbr = (min(l, ring_cap) + kPage - 1) / kPage;
+  }
+  int ip = nb, iq = nbr;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int tp = __shfl_up(ip, o, kWave), tq = __shfl_up(iq, o, kWave);
+    if (lane >= o) {
+      ip += tp;
+      iq += tq;
+    }
+  }
+  P = ip - nb;
+  Q = iq - nbr;
+  WsPlan p;
+  p.nb_tot = __builtin_amdgcn_readlane(ip, kWave - 1);
+  p.nbr_tot = __builtin_amdgcn_readlane(iq, kWave - 1);
+  p.total = n_ret * p.nb_tot + n_str * p.nbr_tot;
+  const int n_wg = min(2 * n_cu, max(1, (p.total + kWsMinBlocks - 1) / kWsMinBlocks));
+  p.n_old = min(n_wg, n_cu);
+  p.n_young = n_wg - p.n_old;
+  const int64_t weight = 4 * (int64_t)p.n_old + 3 * (int64_t)p.n_young;
+  p.r_old = (int)((4 * (int64_t)p.total + weight - 1) / weight);
+  p.g_young = min(p.total, p.n_old * p.r_old);
+  p.r_young = p.n_young ? (p.total - p.g_young + p.n_young - 1) / p.n_young : 0;
+  return p;
+}
+
+// Workgroup whose range holds block g (g < total).
+__device__ __forceinline__ int ws_wg_of(int g, const WsPlan& p) {
+  return g < p.g_young ? g / p.r_old : p.n_old + (g - p.g_young) / p.r_young;
+}
+
+// The item holding block g of the work space (g < total): its type, sequence,
+// KV head rank, first block in the work space, valid blocks and item index.
+struct WsItem {
+  bool ring;
+  int b, kvl, off, len, idx;
+};
+
+__device__ __forceinline__ WsItem ws_item(int g, const WsPlan& p, int B, int n_ret, int n_str, int nb, int nbr, int P,
+                                          int Q) {
+  const int lane = threadIdx.x & (kWave - 1);
+  WsItem it;
+  const int paged_end = n_ret * p.nb_tot;
+  it.ring = g >= paged_end;
+  const int heads = it.ring ? n_str : n_ret;
+  const int blocks = it.ring ? nbr : nb;
+  const int start = (it.ring ? paged_end : 0) + heads * (it.ring ? Q : P);
+  const uint64_t hit = __ballot(lane < B && g >= start && g < start + heads * blocks);
+  if (hit == 0) {  // not reached for g < total
+    it.b = it.kvl = it.off = it.idx = it.len = 0;
+    return it;
+  }
+  it.b = __builtin_amdgcn_readfirstlane((int)__builtin_ctzll(hit));
+  const int first = __builtin_amdgcn_readlane(start, it.b);
+  it.len = __builtin_amdgcn_readlane(blocks, it.b);
+  it.kvl = (g - first) / it.len;
+  it.off = first + it.kvl * it.len;
+  it.idx = it.ring ? B * n_ret + it.b * n_str + it.kvl : it.b * n_ret + it.kvl;
+  return it;
+}
+
+template <int D, int MODE>
+__global__ __launch_bounds__(kSplitWaves * kWave, 2) void decode_ws_kernel(DecodeArgs a) {
+  constexpr int kDimBlocks = D / 16;
+  __shared__ f32x4 s_acc[kSplitWaves][kDimBlocks][kWave];
+  __shared__ float s_m[kSplitWaves][kWave];
+  __shared__ float s_l[kSplitWaves][kWave];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & (kWave - 1);
+  int len_l, nb_l, nbr_l, P_l, Q_l;
+  const WsPlan p = ws_plan(a.lens, a.B, a.full.max_pages, a.full.n_kv, a.ring_cap, a.ring.n_kv, a.ws_cu, len_l, nb_l,
+                           nbr_l, P_l, Q_l);
+  const int w = blockIdx.x;
+  int g0, g1;
+  if (w < p.n_old) {
+    g0 = w * p.r_old;
+    g1 = min(g0 + p.r_old, p.g_young);
+  } else {
+    g0 = p.g_young + (w - p.n_old) * p.r_young;
+    g1 = w < p.n_old + p.n_young ? min(g0 + p.r_young, p.total) : g0;
+  }
+  for (int g = g0; g < g1;) {  // uniform: every wave walks the same segments
+    const WsItem it = ws_item(g, p, a.B, a.full.n_kv, a.ring.n_kv, nb_l, nbr_l, P_l, Q_l);
+    if (it.len == 0) break;
+    const int s0 = g - it.off, s1 = min(g1 - it.off, it.len);
+    const int len = __builtin_amdgcn_readlane(len_l, it.b);
+    // This wave's consecutive quarter of the segment's 32-token chunks.
+    const int per = ((s1 - s0 + 1) / 2 + kSplitWaves - 1) / kSplitWaves;
+    const int c0 = min(s1, s0 + 2 * per * wave), c1 = min(s1, c0 + 2 * per);
+    f32x4 acc[kDimBlocks];
+#pragma unroll
+    for (int nb = 0; nb < kDimBlocks; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float m = -INFINITY, l = 0.f;
+    if (c0 < c1) {
+      if (it.ring) decode_split_body<D, true, false, MODE == 3>(a, a.ring, it.b, it.kvl, len, c0, c1, acc, m, l);
+      else decode_split_body<D, false, MODE == 1, MODE == 3>(a, a.full, it.b, it.kvl, len, c0, c1, acc, m, l);
+    }
+    const int col = lane & 15;
+    merge_waves_store<D>(a, acc, m, l, s_acc, s_m, s_l, col < a.gs, (int64_t)(w + it.idx) * a.gs + col);
+    g = it.off + s1;
   }
 }
 
@@ -609,10 +729,6 @@ __global__ __launch_bounds__(kWave) void decode_f32_kernel(DecodeArgs a, void* o
 constexpr int kMergeDims = 32;      // output dimensions per merge workgroup
 constexpr int kMergeThreads = 512;  // kMergeDims x 16 split groups
 constexpr int kMergeGroups = kMergeThreads / kMergeDims;
-// Partials per (sequence, head): one per split workgroup, at most
-// kMaxSplits / kSplitWaves, so each of the 16 groups holds at most 16.
-constexpr int kMergePerGroup = kMaxSplits / kSplitWaves / kMergeGroups;
-static_assert(kMergePerGroup * kMergeGroups * kSplitWaves == kMaxSplits, "merge covers every partial");
 
 // Log-sum-exp merge of the split partials of one (sequence, query head), for
 // one slice of kMergeDims output dimensions.  Every load the workgroup needs
@@ -620,12 +736,17 @@ static_assert(kMergePerGroup * kMergeGroups * kSplitWaves == kMaxSplits, "merge 
 // over 16 groups of 32 threads reading coalesced 128-byte rows) is issued up
 // front, so the pass costs one round trip to memory; the statistics are then
 // reduced in LDS and the weighted sums combined.
-template <int D, bool OUT_F32>
+template <int D, bool OUT_F32, bool WS>
 __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(MergeArgs a) {
   constexpr int kWaves = kMergeThreads / kWave;
   constexpr int kSlices = D / kMergeDims;
-  static_assert(kMergeThreads >= kMaxSplits / kSplitWaves, "one (m, l) pair per thread");
-  __shared__ float s_w[kMaxSplits / kSplitWaves];
+  // Partials per (sequence, head): fixed splits write up to kMaxSplits /
+  // kSplitWaves, the work-space pass up to kWsMaxWgs.
+  constexpr int kMaxPartials = WS ? kWsMaxWgs : kMaxSplits / kSplitWaves;
+  constexpr int kPerGroup = kMaxPartials / kMergeGroups;
+  static_assert(kPerGroup * kMergeGroups == kMaxPartials, "merge covers every partial");
+  static_assert(kMergeThreads >= kMaxPartials, "one (m, l) pair per thread");
+  __shared__ float s_w[kMaxPartials];
   __shared__ float s_red[kWaves];
   __shared__ float s_acc[kMergeGroups][kMergeDims];
   const int wg = blockIdx.x;
@@ -636,32 +757,47 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(MergeArgs a
   const int lane = tid & (kWave - 1), wave = tid / kWave;
   const int g = hq / a.gs;
   const bool streaming = (a.streaming_mask >> g) & 1ull;
-  const int len = a.lens[b];
-  const int n_valid = streaming ? min(len, a.ring_cap) : min(len, a.max_len);
-  int split_tok = streaming ? a.split_tokens_ring : a.split_tokens_full;
-  int max_ns = streaming ? a.n_splits_ring : a.n_splits_full;
-  if (!streaming && a.bal_max_groups) {  // the split pass's length-balanced plan
-    int len_lane, nb;
-    split_tok = kSplitWaves * kPage *
-                balanced_split_blocks(a.lens, a.B, a.bal_max_pages, a.bal_n_ret, a.bal_max_groups, len_lane, nb);
-    max_ns = a.bal_max_groups;
+  int ns;
+  int64_t base;
+  constexpr int64_t stride_c = 1;
+  int64_t stride = stride_c;
+  if constexpr (WS) {
+    // Partials of the work-space split pass: the item's slots (see there).
+    int len_l, nb_l, nbr_l, P_l, Q_l;
+    const WsPlan p = ws_plan(a.lens, a.B, a.ws_max_pages, a.ws_n_ret, a.ring_cap, a.ws_n_str, a.ws_cu, len_l, nb_l,
+                             nbr_l, P_l, Q_l);
+    const uint64_t below = (1ull << g) - 1;
+    const int rank = __builtin_popcountll((streaming ? a.streaming_mask : ~a.streaming_mask) & below);
+    const int blocks = __builtin_amdgcn_readlane(streaming ? nbr_l : nb_l, b);
+    const int first_blk = (streaming ? a.ws_n_ret * p.nb_tot + a.ws_n_str * __builtin_amdgcn_readlane(Q_l, b)
+                                     : a.ws_n_ret * __builtin_amdgcn_readlane(P_l, b)) +
+                          rank * blocks;
+    const int idx = streaming ? a.B * a.ws_n_ret + b * a.ws_n_str + rank : b * a.ws_n_ret + rank;
+    const int first = blocks > 0 ? ws_wg_of(first_blk, p) : 0;
+    ns = blocks > 0 ? ws_wg_of(first_blk + blocks - 1, p) - first + 1 : 0;
+    base = (int64_t)(first + idx) * a.gs + (hq - g * a.gs);
+    stride = a.gs;
+  } else {
+    const int len = a.lens[b];
+    const int n_valid = streaming ? min(len, a.ring_cap) : min(len, a.max_len);
+    const int split_tok = streaming ? a.split_tokens_ring : a.split_tokens_full;
+    ns = min((n_valid + split_tok - 1) / split_tok, streaming ? a.n_splits_ring : a.n_splits_full);
+    base = ((int64_t)b * a.Hq + hq) * a.max_splits;
   }
-  const int ns = min((n_valid + split_tok - 1) / split_tok, max_ns);
-  const int64_t base = ((int64_t)b * a.Hq + hq) * a.max_splits;
   const int dd = tid % kMergeDims, grp = tid / kMergeDims;
   const int d = slice * kMergeDims + dd;
 
   // All loads first.
   float m = -INFINITY, l = 0.f;
   if (tid < ns) {
-    m = a.part_ml[(base + tid) * 2];
-    l = a.part_ml[(base + tid) * 2 + 1];
+    m = a.part_ml[(base + tid * stride) * 2];
+    l = a.part_ml[(base + tid * stride) * 2 + 1];
   }
-  float av[kMergePerGroup];
+  float av[kPerGroup];
 #pragma unroll
-  for (int k = 0; k < kMergePerGroup; ++k) {
+  for (int k = 0; k < kPerGroup; ++k) {
     const int s = grp + kMergeGroups * k;
-    av[k] = s < ns ? a.part_acc[(base + s) * D + d] : 0.f;
+    av[k] = s < ns ? a.part_acc[(base + s * stride) * D + d] : 0.f;
   }
 
   float mloc = m;
@@ -686,7 +822,7 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(MergeArgs a
 
   float acc = 0.f;
 #pragma unroll
-  for (int k = 0; k < kMergePerGroup; ++k) {
+  for (int k = 0; k < kPerGroup; ++k) {
     const int s = grp + kMergeGroups * k;
     if (s < ns) acc += s_w[s] * av[k];
   }
@@ -718,7 +854,20 @@ static void launch_split_d(const DecodeArgs& a, int mode, int grid, hipStream_t 
   else hipLaunchKernelGGL((decode_split_bf16_kernel<D, 0>), dim3(grid), blk, 0, s, a);
 }
 
+template <int D>
+void launch_ws_d(const DecodeArgs& a, int mode, hipStream_t s) {
+  const dim3 grid(2 * a.ws_cu), blk(kSplitWaves * kWave);
+  if (mode == 1) hipLaunchKernelGGL((decode_ws_kernel<D, 1>), grid, blk, 0, s, a);
+  else if (mode == 3) hipLaunchKernelGGL((decode_ws_kernel<D, 3>), grid, blk, 0, s, a);
+  else hipLaunchKernelGGL((decode_ws_kernel<D, 0>), grid, blk, 0, s, a);
+}
+
 hipError_t launch_decode_split(const DecodeArgs& a, int d, int mode, hipStream_t s) {
+  if (a.ws_cu) {
+    if (d == 64) launch_ws_d<64>(a, mode, s);
+    else launch_ws_d<128>(a, mode, s);
+    return hipGetLastError();
+  }
   const int grid = a.full.n_items + a.ring.n_items;
   if (d == 64) launch_split_d<64>(a, mode, grid, s);
   else launch_split_d<128>(a, mode, grid, s);
@@ -732,15 +881,21 @@ hipError_t launch_decode_f32(const DecodeArgs& a, int d, void* out, int64_t o_sb
   return hipGetLastError();
 }
 
+template <int D, bool WS>
+void launch_merge_d(const MergeArgs& a, int out_f32, int grid, hipStream_t s) {
+  if (out_f32) hipLaunchKernelGGL((decode_merge_kernel<D, true, WS>), dim3(grid), dim3(kMergeThreads), 0, s, a);
+  else hipLaunchKernelGGL((decode_merge_kernel<D, false, WS>), dim3(grid), dim3(kMergeThreads), 0, s, a);
+}
+
 hipError_t launch_decode_merge(const MergeArgs& a, int dtype, int out_f32, int d, hipStream_t s) {
   (void)dtype;
   const int grid = a.B * a.Hq * (d / kMergeDims);
   if (d == 64) {
-    if (out_f32) hipLaunchKernelGGL((decode_merge_kernel<64, true>), dim3(grid), dim3(kMergeThreads), 0, s, a);
-    else hipLaunchKernelGGL((decode_merge_kernel<64, false>), dim3(grid), dim3(kMergeThreads), 0, s, a);
+    if (a.ws_cu) launch_merge_d<64, true>(a, out_f32, grid, s);
+    else launch_merge_d<64, false>(a, out_f32, grid, s);
   } else {
-    if (out_f32) hipLaunchKernelGGL((decode_merge_kernel<128, true>), dim3(grid), dim3(kMergeThreads), 0, s, a);
-    else hipLaunchKernelGGL((decode_merge_kernel<128, false>), dim3(grid), dim3(kMergeThreads), 0, s, a);
+    if (a.ws_cu) launch_merge_d<128, true>(a, out_f32, grid, s);
+    else launch_merge_d<128, false>(a, out_f32, grid, s);
   }
   return hipGetLastError();
 }
