@@ -446,7 +446,7 @@ def decode_leg(args, torch, synth, PagedCache, RingCache, aoh_decode, aoh_decode
         "frac_of_hbm_peak": round(gbps / PEAK_HBM_GBPS, 4),
         "resident_kv_gb": round((full.k.numel() + full.v.numel() + ring.k.numel() + ring.v.numel()) * 2 / 1e9, 4),
         "roofline": {
-            "kernel": "decode_split_bf16_kernel<128,paged> + ring split + merge (one aoh_decode call)",
+            "kernel": "decode_ws_kernel<128> (paged and ring items in one work-space split) + merge (one aoh_decode call)",
             "bound": "hbm", "achieved": round(b_last / (dec_ms * 1e-3) / 1e9, 1), "peak": PEAK_HBM_GBPS,
             "unit": "GB/s", "frac": round(b_last / (dec_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
             "traffic": traffic_for("decode_split"),
@@ -851,9 +851,9 @@ def cpu_baseline(q, k, v, mask, n_sink, window, T, D, gs, target_s=15.0):
         t0 = time.perf_counter()
         OA.prefill(qh, kh, vh, mask, n_sink, window, rows=rows)
         dt = time.perf_counter() - t0
-        if dt >= target_s / 3 or n_rows >= 4096:
+        if dt >= target_s * 2 / 3 or n_rows >= 8192:
             break
-        n_rows = int(n_rows * max(2.0, target_s / max(dt, 1e-3) / 1.5))
+        n_rows = int(n_rows * max(2.0, target_s / max(dt, 1e-3)))
     limiter.restore_original_limits()
     flops = 0
     for g, st in enumerate(mask):

@@ -161,12 +161,13 @@ SplitPlan plan_splits(int batch, int max_pages, int ring_cap, int n_ret, int n_s
 
 // Split partials: fixed splits hold [B][Hq][max_splits] partials; the
 // work-space pass (batches up to kWsMaxBatch) at most kWsMaxWgs + B x Hkv
-// slots of gs heads, bounded by (kWsMaxWgs + B) x Hq.
+// slots of gs heads, bounded by (kWsMaxWgs + B) x Hq, and two int32 per item
+// (B x Hkv <= B x Hq) after them.
 size_t workspace_bytes(int batch, int hq, int d, const SplitPlan& p) {
-  size_t slots = (size_t)batch * hq * p.max_splits;
-  if (batch <= kWsMaxBatch) slots = std::max(slots, (size_t)(kWsMaxWgs + batch) * hq);
-  const size_t acc = slots * d * sizeof(float);
-  return acc + slots * 2 * sizeof(float);
+  const size_t fixed = (size_t)batch * hq * p.max_splits * (d + 2) * sizeof(float);
+  if (batch > kWsMaxBatch) return fixed;
+  const size_t ws = (size_t)(kWsMaxWgs + batch) * hq * (d + 2) * sizeof(float) + (size_t)batch * hq * 2 * sizeof(int32_t);
+  return std::max(fixed, ws);
 }
 
 }  // namespace
@@ -655,6 +656,7 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
                                     : (size_t)B * Hq * sp_bound.max_splits * D;
   float* part_ml = part_acc + acc_floats;
   a.part_acc = part_acc; a.part_ml = part_ml; a.max_splits = sp_bound.max_splits;
+  if (a.ws_cu) a.ws_items = reinterpret_cast<int32_t*>(part_ml + acc_floats / D * 2);
   float* scores = nullptr;
   float* ml = nullptr;
   uint32_t* part = nullptr;
@@ -694,7 +696,7 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
   // reuse: a retrieval head's "length" is its number of borrowed entries
   m.max_len = x.mode == kReuse ? x.top_k : max_pages * kPageTokens;
   m.ring_cap = ring_cap;
-  m.ws_cu = a.ws_cu; m.ws_n_ret = hs.n_ret; m.ws_n_str = hs.n_str; m.ws_max_pages = max_pages;
+  m.ws_cu = a.ws_cu; m.ws_n_ret = hs.n_ret; m.ws_n_str = hs.n_str; m.ws_items = a.ws_items;
   m.streaming_mask = hs.streaming_mask;
   m.ml_out = ml;
   const int out_f32 = out->dtype == AOH_F32;

@@ -77,8 +77,10 @@ struct DecodeArgs {
   int32_t ring_cap;             // n_sink + window
   int32_t max_splits;
   // > 0: the work-space split pass (decode_ws_kernel) with 2 * ws_cu
-  // workgroups; part_acc / part_ml then hold [slot][gs][D] / [slot][gs][2].
+  // workgroups; part_acc / part_ml then hold [slot][gs][D] / [slot][gs][2],
+  // and ws_items [B * Hkv][2] each item's first partial slot and count.
   int32_t ws_cu;
+  int32_t* ws_items;
   float scale_log2;
   float scale;
   CacheView full;
@@ -117,8 +119,9 @@ struct MergeArgs {
   int32_t max_len;              // 16 * pages per sequence: lens are clamped to it
   int32_t ring_cap;
   // > 0: partials of the work-space split pass (DecodeArgs::ws_cu) over
-  // ws_n_ret paged KV heads of ws_max_pages pages and ws_n_str rings.
-  int32_t ws_cu, ws_n_ret, ws_n_str, ws_max_pages;
+  // ws_n_ret paged KV heads and ws_n_str rings, located through ws_items.
+  int32_t ws_cu, ws_n_ret, ws_n_str;
+  const int32_t* ws_items;
   uint64_t streaming_mask;      // bit g set = KV head g streaming
   float* ml_out;                // anchor layer: final (m, l) of each paged-cache head, [B][Hq][2]
 };

@@ -640,6 +640,12 @@ __global__ __launch_bounds__(kSplitWaves * kWave, 2) void decode_ws_kernel(Decod
     }
     const int col = lane & 15;
     merge_waves_store<D>(a, acc, m, l, s_acc, s_m, s_l, col < a.gs, (int64_t)(w + it.idx) * a.gs + col);
+    if (s0 == 0 && threadIdx.x == 0) {
+      // The workgroup holding the item's first block records where the item's
+      // partials are for the merge pass: first slot and count.
+      a.ws_items[2 * it.idx + 0] = w + it.idx;
+      a.ws_items[2 * it.idx + 1] = ws_wg_of(it.off + it.len - 1, p) - w + 1;
+    }
     g = it.off + s1;
   }
 }
@@ -762,20 +768,18 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(MergeArgs a
   constexpr int64_t stride_c = 1;
   int64_t stride = stride_c;
   if constexpr (WS) {
-    // Partials of the work-space split pass: the item's slots (see there).
-    int len_l, nb_l, nbr_l, P_l, Q_l;
-    const WsPlan p = ws_plan(a.lens, a.B, a.ws_max_pages, a.ws_n_ret, a.ring_cap, a.ws_n_str, a.ws_cu, len_l, nb_l,
-                             nbr_l, P_l, Q_l);
+    // Partials of the work-space split pass: the item's slots, as recorded by
+    // the workgroup that held its first block (an item without valid blocks
+    // has none and records nothing).
+    const int len = a.lens[b];
+    const int n_valid = streaming ? min(len, a.ring_cap) : min(len, a.max_len);
     const uint64_t below = (1ull << g) - 1;
     const int rank = __builtin_popcountll((streaming ? a.streaming_mask : ~a.streaming_mask) & below);
-    const int blocks = __builtin_amdgcn_readlane(streaming ? nbr_l : nb_l, b);
-    const int first_blk = (streaming ? a.ws_n_ret * p.nb_tot + a.ws_n_str * __builtin_amdgcn_readlane(Q_l, b)
-                                     : a.ws_n_ret * __builtin_amdgcn_readlane(P_l, b)) +
-                          rank * blocks;
     const int idx = streaming ? a.B * a.ws_n_ret + b * a.ws_n_str + rank : b * a.ws_n_ret + rank;
-    const int first = blocks > 0 ? ws_wg_of(first_blk, p) : 0;
-    ns = blocks > 0 ? ws_wg_of(first_blk + blocks - 1, p) - first + 1 : 0;
-    base = (int64_t)(first + idx) * a.gs + (hq - g * a.gs);
+    const int slot0 = a.ws_items[2 * idx + 0];
+    const int count = a.ws_items[2 * idx + 1];
+    ns = n_valid > 0 ? count : 0;
+    base = (int64_t)slot0 * a.gs + (hq - g * a.gs);
     stride = a.gs;
   } else {
     const int len = a.lens[b];
