@@ -689,8 +689,6 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
   m.out = out->data; m.o_sb = out->stride[0]; m.o_sh = out->stride[1];
   m.B = (int)B; m.Hq = (int)Hq; m.gs = gs; m.max_splits = sp_bound.max_splits;
   // One partial per split workgroup (kSplitWaves consecutive splits).
-  m.split_tokens_full = kSplitWaves * sp.split_blocks_full * kPageTokens;
-  m.split_tokens_ring = kSplitWaves * sp.split_blocks_ring * kPageTokens;
   m.n_splits_full = a.full.n_groups;
   m.n_splits_ring = a.ring.n_groups;
   // reuse: a retrieval head's "length" is its number of borrowed entries

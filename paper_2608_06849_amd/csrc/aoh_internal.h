@@ -112,8 +112,6 @@ struct MergeArgs {
   int64_t o_sb, o_sh;
   int32_t B, Hq, gs;
   int32_t max_splits;
-  int32_t split_tokens_full;    // tokens per partial (split workgroup), paged cache
-  int32_t split_tokens_ring;    // tokens per partial (split workgroup), ring
   int32_t n_splits_full;        // partials written per (b, head), paged cache
   int32_t n_splits_ring;        // partials written per (b, head), ring
   int32_t max_len;              // 16 * pages per sequence: lens are clamped to it

@@ -782,10 +782,9 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(MergeArgs a
     base = (int64_t)slot0 * a.gs + (hq - g * a.gs);
     stride = a.gs;
   } else {
-    const int len = a.lens[b];
-    const int n_valid = streaming ? min(len, a.ring_cap) : min(len, a.max_len);
-    const int split_tok = streaming ? a.split_tokens_ring : a.split_tokens_full;
-    ns = min((n_valid + split_tok - 1) / split_tok, streaming ? a.n_splits_ring : a.n_splits_full);
+    // Every split workgroup writes its partial, one without tokens m = -inf
+    // (weight 0), so all of them are merged and the length is not needed.
+    ns = streaming ? a.n_splits_ring : a.n_splits_full;
     base = ((int64_t)b * a.Hq + hq) * a.max_splits;
   }
   const int dd = tid % kMergeDims, grp = tid / kMergeDims;
