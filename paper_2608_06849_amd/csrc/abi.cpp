@@ -643,13 +643,12 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
     return ok();
   }
 
-  // Plain, anchor and fused steps of 2 to kWsMaxBatch sequences split the
+  // Plain, anchor and fused steps of up to kWsMaxBatch sequences split the
   // step's work space on the device (two workgroups per CU), which follows any
-  // mix of lengths; one sequence (no mix to follow, and the plan's cost shows
-  // in its short steps), larger batches and the reuse layer take fixed splits
-  // from the cache capacity.
+  // mix of lengths and of cache types; larger batches and the reuse layer take
+  // fixed splits from the cache capacity.
   const int64_t ws_blocks = std::max<int64_t>(max_pages, sp.ring_blocks);
-  if (x.mode != kReuse && B >= 2 && B <= kWsMaxBatch && B * Hkv * ws_blocks < (1ll << 30))
+  if (x.mode != kReuse && B <= kWsMaxBatch && B * Hkv * ws_blocks < (1ll << 30))
     a.ws_cu = std::min(compute_units(), kWsMaxWgs / 2);
   float* part_acc = reinterpret_cast<float*>(workspace);
   const size_t acc_floats = a.ws_cu ? (size_t)(2 * a.ws_cu + B * Hkv) * gs * D

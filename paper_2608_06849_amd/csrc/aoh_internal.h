@@ -226,7 +226,7 @@ constexpr int kSplitWaves = 4;
 // waves up to kRingTargetWaves by the rings' share of the work.
 constexpr int kDecodeTargetWaves = 2048;
 constexpr int kRingTargetWaves = 4096;
-// Work-space decode split pass: batches of 2 to kWsMaxBatch sequences (one
+// Work-space decode split pass: batches of up to kWsMaxBatch sequences (one
 // lane per sequence), at most kWsMaxWgs workgroups (two per CU), so at most
 // that many partials per item for the merge pass.
 constexpr int kWsMaxBatch = 64;

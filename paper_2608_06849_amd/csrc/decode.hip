@@ -452,8 +452,8 @@ __device__ __forceinline__ void merge_waves_store(const DecodeArgs& a, f32x4 (&a
   }
 }
 
-// Fixed splits from the cache capacity (one sequence, batches over
-// kWsMaxBatch sequences, and the reuse layer).  One launch for both cache types: paged-cache items
+// Fixed splits from the cache capacity (batches over kWsMaxBatch sequences,
+// and the reuse layer).  One launch for both cache types: paged-cache items
 // first, ring items last.  MODE 0: plain decode; 1: anchor layer (paged items
 // also keep their scores); 2: reuse layer (paged items attend to borrowed
 // positions only); 3: plain decode that first stores the new token at
@@ -501,7 +501,7 @@ __global__ __launch_bounds__(kSplitWaves * kWave, 2) void decode_split_bf16_kern
 
 // ---------------------------------------------------------------------------
 // Split pass over the step's work space (bf16 plain, anchor and fused-step
-// decode of 2 to kWsMaxBatch sequences).
+// decode of up to kWsMaxBatch sequences).
 //
 // Work space: the valid 16-token blocks of every item (cache type, sequence,
 // KV head) laid end to end, paged items first, each type in (sequence, KV
