@@ -742,51 +742,16 @@ constexpr int kMergeGroups = kMergeThreads / kMergeDims;
 // over 16 groups of 32 threads reading coalesced 128-byte rows) is issued up
 // front, so the pass costs one round trip to memory; the statistics are then
 // reduced in LDS and the weighted sums combined.
-template <int D, bool OUT_F32, bool WS>
-__global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(MergeArgs a) {
+// Loads and log-sum-exp merge of ns partials (rows base + s * stride, at most
+// kMergeGroups * PER_GROUP of them) for slice `slice` of (sequence b, query
+// head hq), and the output store.
+template <int D, bool OUT_F32, int PER_GROUP>
+__device__ __forceinline__ void merge_partials(const MergeArgs& a, int b, int hq, int slice, bool streaming, int ns,
+                                               int64_t base, int64_t stride, float* s_w, float* s_red,
+                                               float (*s_acc)[kMergeDims]) {
   constexpr int kWaves = kMergeThreads / kWave;
-  constexpr int kSlices = D / kMergeDims;
-  // Partials per (sequence, head): fixed splits write up to kMaxSplits /
-  // kSplitWaves, the work-space pass up to kWsMaxWgs.
-  constexpr int kMaxPartials = WS ? kWsMaxWgs : kMaxSplits / kSplitWaves;
-  constexpr int kPerGroup = kMaxPartials / kMergeGroups;
-  static_assert(kPerGroup * kMergeGroups == kMaxPartials, "merge covers every partial");
-  static_assert(kMergeThreads >= kMaxPartials, "one (m, l) pair per thread");
-  __shared__ float s_w[kMaxPartials];
-  __shared__ float s_red[kWaves];
-  __shared__ float s_acc[kMergeGroups][kMergeDims];
-  const int wg = blockIdx.x;
-  const int slice = wg % kSlices;
-  const int hq = (wg / kSlices) % a.Hq;
-  const int b = wg / (kSlices * a.Hq);
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1), wave = tid / kWave;
-  const int g = hq / a.gs;
-  const bool streaming = (a.streaming_mask >> g) & 1ull;
-  int ns;
-  int64_t base;
-  constexpr int64_t stride_c = 1;
-  int64_t stride = stride_c;
-  if constexpr (WS) {
-    // Partials of the work-space split pass: the item's slots, as recorded by
-    // the workgroup that held its first block (an item without valid blocks
-    // has none and records nothing).
-    const int len = a.lens[b];
-    const int n_valid = streaming ? min(len, a.ring_cap) : min(len, a.max_len);
-    const uint64_t below = (1ull << g) - 1;
-    const int rank = __builtin_popcountll((streaming ? a.streaming_mask : ~a.streaming_mask) & below);
-    const int idx = streaming ? a.B * a.ws_n_ret + b * a.ws_n_str + rank : b * a.ws_n_ret + rank;
-    const int slot0 = a.ws_items[2 * idx + 0];
-    const int count = a.ws_items[2 * idx + 1];
-    ns = n_valid > 0 ? count : 0;
-    base = (int64_t)slot0 * a.gs + (hq - g * a.gs);
-    stride = a.gs;
-  } else {
-    // Every split workgroup writes its partial, one without tokens m = -inf
-    // (weight 0), so all of them are merged and the length is not needed.
-    ns = streaming ? a.n_splits_ring : a.n_splits_full;
-    base = ((int64_t)b * a.Hq + hq) * a.max_splits;
-  }
   const int dd = tid % kMergeDims, grp = tid / kMergeDims;
   const int d = slice * kMergeDims + dd;
 
@@ -796,9 +761,9 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(MergeArgs a
     m = a.part_ml[(base + tid * stride) * 2];
     l = a.part_ml[(base + tid * stride) * 2 + 1];
   }
-  float av[kPerGroup];
+  float av[PER_GROUP];
 #pragma unroll
-  for (int k = 0; k < kPerGroup; ++k) {
+  for (int k = 0; k < PER_GROUP; ++k) {
     const int s = grp + kMergeGroups * k;
     av[k] = s < ns ? a.part_acc[(base + s * stride) * D + d] : 0.f;
   }
@@ -825,7 +790,7 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(MergeArgs a
 
   float acc = 0.f;
 #pragma unroll
-  for (int k = 0; k < kPerGroup; ++k) {
+  for (int k = 0; k < PER_GROUP; ++k) {
     const int s = grp + kMergeGroups * k;
     if (s < ns) acc += s_w[s] * av[k];
   }
@@ -845,6 +810,53 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(MergeArgs a
     } else {
       reinterpret_cast<uint16_t*>(a.out)[(int64_t)b * a.o_sb + (int64_t)hq * a.o_sh + d] = f32_to_bf16_bits(o);
     }
+  }
+}
+
+template <int D, bool OUT_F32, bool WS>
+__global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(MergeArgs a) {
+  constexpr int kSlices = D / kMergeDims;
+  // Partials per (sequence, head): fixed splits write up to kMaxSplits /
+  // kSplitWaves, the work-space pass up to kWsMaxWgs (in practice no more than
+  // that first bound unless an item spans most of the launch).
+  constexpr int kFewPartials = kMaxSplits / kSplitWaves;
+  constexpr int kMaxPartials = WS ? kWsMaxWgs : kFewPartials;
+  static_assert(kFewPartials % kMergeGroups == 0 && kMaxPartials % kMergeGroups == 0, "merge covers every partial");
+  static_assert(kMergeThreads >= kMaxPartials, "one (m, l) pair per thread");
+  __shared__ float s_w[kMaxPartials];
+  __shared__ float s_red[kMergeThreads / kWave];
+  __shared__ float s_acc[kMergeGroups][kMergeDims];
+  const int wg = blockIdx.x;
+  const int slice = wg % kSlices;
+  const int hq = (wg / kSlices) % a.Hq;
+  const int b = wg / (kSlices * a.Hq);
+  const int g = hq / a.gs;
+  const bool streaming = (a.streaming_mask >> g) & 1ull;
+  if constexpr (WS) {
+    // Partials of the work-space split pass: the item's slots, as recorded by
+    // the workgroup that held its first block (an item without valid blocks
+    // has none and records nothing).
+    const int len = a.lens[b];
+    const int n_valid = streaming ? min(len, a.ring_cap) : min(len, a.max_len);
+    const uint64_t below = (1ull << g) - 1;
+    const int rank = __builtin_popcountll((streaming ? a.streaming_mask : ~a.streaming_mask) & below);
+    const int idx = streaming ? a.B * a.ws_n_ret + b * a.ws_n_str + rank : b * a.ws_n_ret + rank;
+    const int slot0 = a.ws_items[2 * idx + 0];
+    const int ns = n_valid > 0 ? a.ws_items[2 * idx + 1] : 0;
+    const int64_t base = (int64_t)slot0 * a.gs + (hq - g * a.gs);
+    if (ns <= kFewPartials)
+      merge_partials<D, OUT_F32, kFewPartials / kMergeGroups>(a, b, hq, slice, streaming, ns, base, a.gs, s_w, s_red,
+                                                              s_acc);
+    else
+      merge_partials<D, OUT_F32, kMaxPartials / kMergeGroups>(a, b, hq, slice, streaming, ns, base, a.gs, s_w, s_red,
+                                                              s_acc);
+  } else {
+    // Every split workgroup writes its partial, one without tokens m = -inf
+    // (weight 0), so all of them are merged and the length is not needed.
+    const int ns = streaming ? a.n_splits_ring : a.n_splits_full;
+    merge_partials<D, OUT_F32, kFewPartials / kMergeGroups>(a, b, hq, slice, streaming, ns,
+                                                            ((int64_t)b * a.Hq + hq) * a.max_splits, 1, s_w, s_red,
+                                                            s_acc);
   }
 }
 
