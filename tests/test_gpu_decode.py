@@ -109,11 +109,13 @@ DECODE_CASES = [
     (1, 32, 8, 128, [0, 1, 0, 1, 1, 0, 1, 0], 64, 1024, [5000], 3),
     (2, 4, 1, 128, [0], 4, 32, [31, 32], 34),           # all retrieval, page crossings
     (2, 4, 1, 128, [1], 4, 32, [31, 100], 40),          # all streaming, ring wrap
-    # mixed lengths: the split length follows the step's total length, so the
-    # sequences take different numbers of split workgroups
+    # mixed lengths: the step's work space is split by its total length, so
+    # the sequences take different numbers of split workgroups
     (16, 8, 2, 128, [0, 1], 16, 256,
      [1, 5000, 37, 900, 16, 17, 3000, 2, 64, 65, 1200, 4096, 8, 333, 2047, 60], 3),
-    (64, 4, 1, 64, [0], 4, 32, [(37 * i) % 500 + 1 for i in range(64)], 2),       # largest length-balanced batch
+    (64, 4, 1, 64, [0], 4, 32, [(37 * i) % 500 + 1 for i in range(64)], 2),       # largest work-space batch
+    (24, 8, 4, 128, [1, 1, 1, 1], 8, 100, [(71 * i) % 400 + 1 for i in range(24)], 2),  # rings only
+    (9, 16, 2, 64, [0, 0], 4, 32, [1, 2, 3, 17, 250, 900, 1, 4000, 33], 2),         # paged only, 1-token prompts
     (70, 4, 2, 64, [0, 1], 4, 32, [(53 * i) % 300 + 1 for i in range(70)], 2),   # beyond it: capacity plan
 ]
 
