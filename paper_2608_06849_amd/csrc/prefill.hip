@@ -62,6 +62,10 @@ struct PrefillLds {
 // this, so P stays below 2^8 and the O rescale is skipped on most tiles.
 constexpr float kRescaleThreshold = 8.0f;
 
+// d_head-128 kernel: largest sum of a lane's 32 exponentials of one tile,
+// taken against the trailing reference max, that is accepted as it is.
+constexpr float kSumHi = 65536.f;
+
 // First non-sink key visible to row i of a streaming head (may be negative).
 __device__ __forceinline__ int lo_of(int i, int chunk, int window) {
   return chunk ? (i / chunk) * chunk - window : i - window + 1;
@@ -586,9 +590,9 @@ __global__ __launch_bounds__(kPrefillRowsF32) void prefill_f32_kernel(PrefillArg
 // ---------------------------------------------------------------------------
 // D = 128 bf16 kernel, phase-shifted wave groups.
 //
-// Same work item and math as prefill_bf16_kernel (256 query rows of one query
-// head, 32 rows per wave, S^T = K.Q^T and O^T += V^T.P^T on the 32x32x16 bf16
-// MFMA, online softmax in fp32 with lazy rescaling); differences:
+// Same work item and products as prefill_bf16_kernel (256 query rows of one
+// query head, 32 rows per wave, S^T = K.Q^T and O^T += V^T.P^T on the 32x32x16
+// bf16 MFMA, online softmax in fp32); differences:
 //  * K/V tiles move global -> LDS with direct loads (global_load_lds_dwordx4),
 //    no register staging, into a ring of four 32 KB stages, issued two tiles
 //    ahead of their first use.
@@ -596,17 +600,15 @@ __global__ __launch_bounds__(kPrefillRowsF32) void prefill_f32_kernel(PrefillArg
 //    at c ^ (r & 15) for K and c ^ 4 (r & 3) for V, which keeps the K row
 //    reads and the V transpose reads free of bank conflicts and makes every
 //    operand address one base register XOR a constant.
-//  * Per tile t a wave runs an MFMA phase (P(t-1).V(t-1) then K(t).Q^T) and a
-//    vector phase (mask, max, exponentials of S(t)); waves 0-3 and waves 4-7
-//    (one of each per SIMD) run one phase apart, separated by workgroup
-//    barriers.  The loop has a single path (a tile with no visible key for a
-//    wave yields P = 0), so the accumulators never move between registers.
+//  * Per tile t a wave runs an MFMA phase (P(t-1).V(t-1) then K(t).Q^T, at
+//    raised wave priority) and a vector phase (mask, exponentials of S(t)
+//    against a trailing reference max, no max pass unless the tile's
+//    exponentials grow too large); waves 0-3 and waves 4-7 (one of each per
+//    SIMD) run one phase apart, separated by workgroup barriers.  The loop
+//    has a single path (a tile with no visible key for a wave yields P = 0),
+//    so the accumulators never move between registers.
 //  * Workgroups are ordered so that the query heads of one KV group and query
 //    block run on the same XCD (one L2).
-// On the 32K Qwen2.5-7B-shaped layer this kernel and prefill_bf16_kernel take
-// the same time (3.68 ms): this one needs ~4% more cycles and the GPU holds a
-// higher clock for it (2.10 vs 2.01 GHz), i.e. both run at the clock the chip
-// sustains for this mix of MFMA, LDS and vector work.
 constexpr int kPPStages = 4;  // LDS stages of 32 KB
 constexpr int kPPD = 128;
 constexpr int kPPRows = kPrefillRows;     // query rows per workgroup (8 waves x 32)
@@ -854,6 +856,7 @@ __device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PP
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc_o[mb][i] = 0.f;
   float m_run = -INFINITY;  // reference max (log2 units) of this lane's row
+  float m_use = 0.f;        // m_run, or 0 while the row has seen no visible key
   float l_run = 0.f;        // this lane's partial row sum (partner lane has the rest)
   f32x16 sacc[2];           // S^T of the current tile, two 32-key blocks
   bf16x8 pop[4];            // P^T operands of the previous tile's 4 key steps
@@ -934,8 +937,12 @@ __device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PP
   // Steady-state MFMA phase.  Both products run unconditionally (a wave with
   // no visible key in a tile gets P = 0 from its vector phase), so the loop
   // has one path and the O accumulators stay in place.
+  // The MFMA phase runs at raised wave priority (s_setprio, this wave only):
+  // its SIMD also holds a wave of the other group in its vector phase, and
+  // the matrix core is kept fed first (2-3% faster than equal priority).
   auto mfma_phase = [&](int t) {
     append_tile(t);
+    __builtin_amdgcn_s_setprio(1);
     pv_part();
     qk_part(t);
     // Operands are read four MFMAs ahead of their products, the first K
@@ -952,10 +959,12 @@ __device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PP
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_setprio(0);
   };
 
-  // Vector phase of tile t: mask, row max, lazy rescale, exponentials into
-  // the P^T operands, row sums.
+  // Vector phase of tile t: mask, exponentials into the P^T operands, row
+  // sums (and, rarely, a new reference max with the rescale).
   auto apply_mask = [&](int kb) {
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk)
@@ -967,15 +976,44 @@ __device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PP
         sacc[blk][i] = vis ? sacc[blk][i] : -INFINITY;
       }
   };
+  // Softmax of a tile without a max pass: the exponentials are taken against
+  // the reference max m_use as it stands (it trails the true row max) and the
+  // tile is accepted when each lane's 32 exponentials sum to at most kSumHi,
+  // which bounds every P by it (P, l and O stay far from fp32 overflow and P
+  // keeps bf16's relative precision).  A lane whose row has seen no visible
+  // key yet, or whose sum is larger or NaN, sends the wave through the exact
+  // step: the true row max of the tile becomes the reference, O and l are
+  // rescaled and the exponentials are taken again.  Row sums of the fp32
+  // exponentials are added as balanced trees: the phase ends on its longest
+  // dependency chain, and a running accumulator, a chain of bf16 dot products
+  // or a max pass ahead of the exponentials lengthens it.
   auto softmax_tile = [&]() {
-    float mx = -INFINITY;
+    auto exps = [&]() {
+      float psum[4];
 #pragma unroll
-    for (int blk = 0; blk < 2; ++blk)
+      for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[blk][i]);
-    mx = xor32_max(mx) * c;
-    if (__any(mx > m_run + kRescaleThreshold)) {
-      const float m_new = fmaxf(m_run, mx);
+        for (int hf = 0; hf < 2; ++hf) {
+          bf16x8 pv;
+          float pf[8];
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            pf[i] = fast_exp2(fmaf(sacc[blk][8 * hf + i], c, -m_use));
+            pv[i] = f32_to_bf16(pf[i]);
+          }
+          psum[2 * blk + hf] = ((pf[0] + pf[1]) + (pf[2] + pf[3])) + ((pf[4] + pf[5]) + (pf[6] + pf[7]));
+          pop[2 * blk + hf] = pv;
+        }
+      return (psum[0] + psum[1]) + (psum[2] + psum[3]);
+    };
+    float tsum = exps();
+    if (__any(!(tsum <= kSumHi) || m_run == -INFINITY)) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[blk][i]);
+      const float m_new = fmaxf(m_run, xor32_max(mx) * c);
       const float alpha = (m_new == -INFINITY) ? 1.f : fast_exp2(m_run - m_new);
       m_run = m_new;
       l_run *= alpha;
@@ -983,28 +1021,10 @@ __device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PP
       for (int mb = 0; mb < kMBlocks; ++mb)
 #pragma unroll
         for (int i = 0; i < 16; ++i) acc_o[mb][i] *= alpha;
+      m_use = (m_run == -INFINITY) ? 0.f : m_run;
+      tsum = exps();
     }
-    const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
-    // Row sum of the tile's exponentials, added as balanced trees of fp32
-    // values: the phase ends on the longest dependency chain of its vector
-    // work, and a running accumulator (or a chain of bf16 dot products) makes
-    // the sum that chain.
-    float psum[4];
-#pragma unroll
-    for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-      for (int hf = 0; hf < 2; ++hf) {
-        bf16x8 pv;
-        float pf[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          pf[i] = fast_exp2(fmaf(sacc[blk][8 * hf + i], c, -m_use));
-          pv[i] = f32_to_bf16(pf[i]);
-        }
-        psum[2 * blk + hf] = ((pf[0] + pf[1]) + (pf[2] + pf[3])) + ((pf[4] + pf[5]) + (pf[6] + pf[7]));
-        pop[2 * blk + hf] = pv;
-      }
-    l_run += (psum[0] + psum[1]) + (psum[2] + psum[3]);
+    l_run += tsum;
   };
   auto valu_phase = [&](int t) {
     v_tile = t;

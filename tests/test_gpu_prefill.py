@@ -196,3 +196,30 @@ def test_one_launch_equals_per_type_launches(B, T, Hq, Hkv, mask):
                           v.index_select(2, ki).contiguous(), [typ] * len(ki), n_sink, window)
         torch.cuda.synchronize()
         assert np.array_equal(bits(one), bits(out.index_select(2, qi))), f"head type {typ}"
+
+
+@pytest.mark.parametrize("T,n_sink,window,step", [(1500, 4, 600, 20.0), (1100, 64, 300, 3.0), (700, 0, 1000, 40.0)])
+def test_rising_scores_raise_the_max_every_tile(T, n_sink, window, step):
+    # Scores that grow along the sequence: key p carries (p / 64) * step
+    # along the queries' shared direction u, so every 64-key tile a query
+    # block reaches lifts the row max by about step * 10 * log2(e) / sqrt(D)
+    # (log2 units): with step 20 or 40 each tile exceeds any trailing reference
+    # max by far and must be rescaled; with step 3 the growth stays below the
+    # acceptance bound for several tiles.  Retrieval and streaming heads,
+    # d_head 128, bf16 against the fp64 oracle (Sec. 5 attention).
+    B, Hq, Hkv, D = 1, 4, 2, 128
+    rng_q = synth.gaussian((B, T, Hq, D), 37, "rise-q")
+    rng_k = synth.gaussian((B, T, Hkv, D), 37, "rise-k", scale=0.5)
+    rng_v = synth.gaussian((B, T, Hkv, D), 37, "rise-v")
+    u = np.zeros(D, dtype=np.float32)
+    u[1::2] = 1.0 / np.sqrt(D / 2)
+    qn = rng_q + 10.0 * u
+    kn = rng_k + (np.arange(T, dtype=np.float32) / 64.0 * step)[None, :, None, None] * u
+    q = to_dtype(qn, torch.bfloat16).to(DEV)
+    k = to_dtype(kn, torch.bfloat16).to(DEV)
+    v = to_dtype(rng_v, torch.bfloat16).to(DEV)
+    mask = [1, 0]
+    out = aoh_prefill(q, k, v, mask, n_sink, window, out=torch.empty((B, T, Hq, D), dtype=torch.float32, device=DEV))
+    torch.cuda.synchronize()
+    want = OA.prefill(f64(q), f64(k), f64(v), mask, n_sink, window)
+    assert_parity(out, want, torch.bfloat16, f"rising scores T={T} step={step}")
