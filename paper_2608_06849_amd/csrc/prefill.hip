@@ -604,9 +604,10 @@ __global__ __launch_bounds__(kPrefillRowsF32) void prefill_f32_kernel(PrefillArg
 //    raised wave priority) and a vector phase (mask, exponentials of S(t)
 //    against a trailing reference max, no max pass unless the tile's
 //    exponentials grow too large); waves 0-3 and waves 4-7 (one of each per
-//    SIMD) run one phase apart, separated by workgroup barriers.  The loop
-//    has a single path (a tile with no visible key for a wave yields P = 0),
-//    so the accumulators never move between registers.
+//    SIMD) run one phase apart, with one workgroup barrier per tile (after
+//    the vector phase for waves 0-3, after the MFMA phase for waves 4-7).
+//    The loop has a single path (a tile with no visible key for a wave
+//    yields P = 0), so the accumulators never move between registers.
 //  * Workgroups are ordered so that the query heads of one KV group and query
 //    block run on the same XCD (one L2).
 constexpr int kPPStages = 4;  // LDS stages of 32 KB
@@ -1040,36 +1041,24 @@ __device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PP
     softmax_tile();
   };
 
-  // Phase bookkeeping, identical for every wave: phase p ends with (odd p)
-  // the wait for this wave's loads of tile (p+1)/2, first read in phase p+1,
-  // and a barrier; even phases p >= 2 start by loading tile
-  // u = p/2 + kPPStages - 2 into the stage that tile u - kPPStages (last
-  // read in phase p - 1) occupied.
-  const int last_phase = 2 * n + 1;
-  int ph = 0;
+  // One workgroup barrier per tile.  Every wave runs MFMA(0) V(0) MFMA(1)
+  // V(1) ..; waves 0-3 take the barrier of tile t after V(t), waves 4-7 after
+  // MFMA(t), so a SIMD's two waves alternate without a barrier between their
+  // phases.  The barrier closing iteration t
+  // follows each wave's wait for its loads of tile t+1 (those of tile t+2 may
+  // stay in flight); after it, tile t+3 goes into the stage of tile t-1,
+  // whose last reads (P.V of tile t-1) came in iteration t.
   auto barrier = [&]() {
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
   };
-  auto end_phase = [&]() {
-    if (ph & 1) {
-      const int u = (ph + 1) >> 1;
-      if (u < n) {
-        // tiles u+1 .. u+kPPStages-3 (4 loads each) may stay in flight
-        const int later = min(kPPStages - 3, n - 1 - u);
-        if (later >= 2) __builtin_amdgcn_s_waitcnt(kWaitVm8);
-        else if (later == 1) __builtin_amdgcn_s_waitcnt(kWaitVm4);
-        else __builtin_amdgcn_s_waitcnt(kWaitVm0);
-      }
-    }
+  auto sync_tile = [&](int t) {
+    if (t + 2 < n) __builtin_amdgcn_s_waitcnt(kWaitVm4);
+    else __builtin_amdgcn_s_waitcnt(kWaitVm0);
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
-    if (ph < last_phase) barrier();
-    ++ph;
-    if (!(ph & 1) && ph >= 2) {
-      const int u = ph / 2 + kPPStages - 2;
-      if (u < n) issue_tile(u);
-    }
+    barrier();
+    if (t + kPPStages - 1 < n) issue_tile(t + kPPStages - 1);
   };
 
   // Prologue: tiles 0 .. kPPStages-2 and this wave's Q rows in flight, then
@@ -1085,21 +1074,18 @@ __device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PP
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
   barrier();
 
-  if (grp == 1) end_phase();  // waves 4-7 start one phase late
   append_tile(0);
   qk_part(0);
-  end_phase();
+  if (grp == 1) sync_tile(0);
   valu_phase(0);
-  end_phase();
+  if (grp == 0) sync_tile(0);
   for (int t = 1; t < n; ++t) {
     mfma_phase(t);
-    end_phase();
+    if (grp == 1) sync_tile(t);
     valu_phase(t);
-    end_phase();
+    if (grp == 0) sync_tile(t);
   }
   pv_part();
-  end_phase();
-  if (grp == 0) end_phase();  // waves 0-3 idle through the last phase
 
   // Epilogue: normalise by the row sum, store.
   const float l_tot = xor32_sum(l_run);
