@@ -123,10 +123,10 @@ def copy_calibration():
 PREFILL_SOURCES = ("prefill.hip", "aoh_device.h", "aoh_internal.h")
 DECODE_SOURCES = ("decode.hip", "aoh_device.h", "aoh_internal.h")
 TRAFFIC = {
-    "fetch_factor": 524302.6 / 1048576.0,   # FETCH_SIZE of a 1 GiB copy / 1 GiB
+    "fetch_factor": 524301.2 / 1048576.0,   # FETCH_SIZE of a 1 GiB copy / 1 GiB
     "write_factor": 1048576.0 / 1048576.0,  # WRITE_SIZE of a 1 GiB copy / 1 GiB
-    "prefill_mixed": {"fetch_kib": 458102.6, "write_kib": 263240.8,
-                      "sources": PREFILL_SOURCES, "source_hash": "d643930246cc8e1e"},
+    "prefill_mixed": {"fetch_kib": 458095.5, "write_kib": 263256.0,
+                      "sources": PREFILL_SOURCES, "source_hash": "008a466c9abec2b2"},
     "decode_ws": {"fetch_kib": 1081572.9, "write_kib": 1169.7,
                   "sources": DECODE_SOURCES, "source_hash": "12a50a525449c597"},
 }
