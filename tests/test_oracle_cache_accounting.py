@@ -284,3 +284,33 @@ def test_bench_counters_equal_the_oracle_accounting():
             for n_sink, window in ((64, 1024), (64, 2048), (0, 1)):
                 assert bench.decode_bytes(lens, gr, gs, 128, 2, n_sink, window) == \
                     C.decode_kv_bytes(lens, gr, gs, 128, 2, n_sink, window)
+
+
+def _tiles_with_a_visible_pair(t, streaming, n_sink, window, chunk=0, rows=256, bn=64):
+    """(query block, key tile) pairs, blocks of `rows` query rows and tiles of
+    `bn` keys, in which the oracle's mask has at least one visible pair."""
+    m = A.visible_mask(np.arange(t), t, streaming, n_sink, window, chunk)
+    count = 0
+    for i0 in range(0, t, rows):
+        blk = m[i0:i0 + rows]
+        for k0 in range(0, t, bn):
+            count += bool(blk[:, k0:k0 + bn].any())
+    return count
+
+
+@pytest.mark.parametrize("t", [1, 63, 64, 65, 300, 700, 1000, 2113])
+@pytest.mark.parametrize("n_sink,window,chunk", [(0, 1, 0), (4, 32, 0), (64, 128, 0), (70, 200, 0), (130, 5, 0),
+                                                (4, 100, 7), (16, 256, 1024), (8, 64, 600)])
+def test_bench_computed_tiles_are_the_tiles_holding_visible_pairs(t, n_sink, window, chunk):
+    # The computed-tile FLOP count of the benchmark (the work the prefill
+    # kernel issues: 256-row query blocks x 64-key tiles) equals 4 D x 256 x 64
+    # per (block, tile) pair in which the mask of Sec. 5 has a visible
+    # (query, key) pair: the kernel visits exactly those tiles, no others.
+    bench = _bench()
+    per_tile = 4 * 128 * 256 * 64
+    ret = _tiles_with_a_visible_pair(t, False, n_sink, window, chunk)
+    st = _tiles_with_a_visible_pair(t, True, n_sink, window, chunk)
+    assert bench.computed_tile_flops(t, 128, 1, 0, n_sink, window, chunk=chunk) == per_tile * ret
+    assert bench.computed_tile_flops(t, 128, 0, 1, n_sink, window, chunk=chunk) == per_tile * st
+    assert bench.computed_tile_flops(t, 128, 3, 5, n_sink, window, chunk=chunk) == per_tile * (3 * ret + 5 * st)
+
