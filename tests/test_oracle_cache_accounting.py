@@ -314,3 +314,37 @@ def test_bench_computed_tiles_are_the_tiles_holding_visible_pairs(t, n_sink, win
     assert bench.computed_tile_flops(t, 128, 0, 1, n_sink, window, chunk=chunk) == per_tile * st
     assert bench.computed_tile_flops(t, 128, 3, 5, n_sink, window, chunk=chunk) == per_tile * (3 * ret + 5 * st)
 
+
+
+def test_bench_traffic_figure_follows_its_kernel_sources():
+    # roofline.traffic is reported only while the kernel sources it was
+    # measured on are unchanged: the hash covers code lines, not comments.
+    bench = _bench()
+    root = os.path.join(os.path.dirname(GOLDEN), "..", "paper_2608_06849_amd", "csrc")
+
+    def reader(edit):
+        def read(name):
+            with open(os.path.join(root, name)) as f:
+                text = f.read()
+            return edit(name, text)
+        return read
+
+    names = bench.PREFILL_SOURCES
+    same = bench.kernel_source_hash(names)
+    assert bench.kernel_source_hash(names, reader(lambda n, t: t)) == same
+    commented = reader(lambda n, t: t.replace("\n", "\n// a comment line\n", 3) + "\n\n   // trailing\n")
+    assert bench.kernel_source_hash(names, commented) == same
+    changed = reader(lambda n, t: t + "\nint aoh_extra_symbol;\n" if n == "prefill.hip" else t)
+    assert bench.kernel_source_hash(names, changed) != same
+    # a figure keyed to another hash is dropped; one keyed to the current hash is kept
+    saved = bench.TRAFFIC["prefill_mixed"]
+    try:
+        bench.TRAFFIC["prefill_mixed"] = dict(saved, source_hash="0" * 16)
+        assert bench.traffic_for("prefill_mixed") is None
+        bench.TRAFFIC["prefill_mixed"] = dict(saved, source_hash=same)
+        want = round((saved["fetch_kib"] / bench.TRAFFIC["fetch_factor"] +
+                      saved["write_kib"] / bench.TRAFFIC["write_factor"]) * 1024)
+        assert bench.traffic_for("prefill_mixed") == want
+    finally:
+        bench.TRAFFIC["prefill_mixed"] = saved
+    assert bench.traffic_for("no_such_kernel") is None
