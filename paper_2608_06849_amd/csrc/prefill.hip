@@ -1044,10 +1044,10 @@ __device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PP
   // One workgroup barrier per tile.  Every wave runs MFMA(0) V(0) MFMA(1)
   // V(1) ..; waves 0-3 take the barrier of tile t after V(t), waves 4-7 after
   // MFMA(t), so a SIMD's two waves alternate without a barrier between their
-  // phases.  The barrier closing iteration t
-  // follows each wave's wait for its loads of tile t+1 (those of tile t+2 may
-  // stay in flight); after it, tile t+3 goes into the stage of tile t-1,
-  // whose last reads (P.V of tile t-1) came in iteration t.
+  // phases.  The barrier of tile t follows each wave's wait for its loads of
+  // tile t+1 (those of tile t+2 may stay in flight); after it, tile t+3 goes
+  // into the stage of tile t-1, whose last reads (P.V of tile t-1, in MFMA(t))
+  // every wave has completed by then.
   auto barrier = [&]() {
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_barrier();
