@@ -637,7 +637,6 @@ __device__ __forceinline__ void lds_dma16(const void* gptr, const void* lds_row)
 // lgkmcnt [11:8]); a field at its maximum does not wait.
 constexpr int kWaitVm0 = 0x0 | (0x7 << 4) | (0xF << 8);
 constexpr int kWaitVm4 = 0x4 | (0x7 << 4) | (0xF << 8);
-constexpr int kWaitVm8 = 0x8 | (0x7 << 4) | (0xF << 8);
 constexpr int kWaitLgkm0 = 0xF | (0x7 << 4) | (0x0 << 8) | (0x3 << 14);
 
 
