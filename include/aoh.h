@@ -326,8 +326,16 @@ aoh_status aoh_head_mapping(const aoh_tensor* w_q_anchor, const aoh_tensor* w_k_
  * and in addition, for every sequence b and the r-th retrieval KV group g
  * (ascending id), indices[b][r][0..top_k) = the top_k positions p < lens[b]
  * of highest score sum_{h in g} P_h(p) / (Hq/Hkv), P_h the attention
- * probabilities of query head h in this step, in ascending order; ties to the
- * lower position; when lens[b] <= top_k every position, then -1.
+ * probabilities of query head h in this step, in ascending order; when
+ * lens[b] <= top_k every position, then -1.  The ranking uses each score as
+ * the decode pass keeps it: rounded to 2^-11 log2 units (each P_h within
+ * 1.7e-4 of its relative value; equal scores stay equal) and stored as a
+ * 16-bit distance below the rounded maximum of its 32-token chunk, which
+ * saturates just under 32 units, so probabilities below ~2^-32 of their
+ * chunk's maximum rank as that bound (at most 2.3e-10 of the head's
+ * probability mass: only such positions can trade places).  The group's
+ * score is ranked with 13 mantissa bits (within 1.2e-4 of its value); equal
+ * ranked scores go to the lower position.
  *   indices: DEVICE int32 [B][n_retrieval_groups][top_k]; top_k >= 1; bf16 only.
  *   workspace: aoh_decode_anchor_workspace_bytes(B, Hq, D, max_pages, ring_capacity).
  */

@@ -459,22 +459,32 @@ size_t aoh_decode_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t d_he
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Anchor extras: scores [B][Hq][16 * max_pages], final (m, l) [B][Hq][2], and
-// the top-k partial histograms and counts per (sequence, KV head) list (sized
-// with Hq lists per sequence, a bound on the retrieval KV heads).
-static size_t anchor_scores_bytes(int64_t B, int64_t Hq, int64_t max_pages) {
-  return align256((size_t)(B * Hq * max_pages * kPageTokens) * sizeof(float));
+// Anchor extras: score codes [B][Hq][16 * max_pages] (16-bit) and their
+// references [B][Hq][max_pages], final (m, l) [B][Hq][2], and the top-k keys,
+// partial histograms and counts per (sequence, KV head) list (sized with Hq
+// lists per sequence, a bound on the retrieval KV heads).
+static size_t anchor_codes_bytes(int64_t B, int64_t Hq, int64_t max_pages) {
+  return align256((size_t)(B * Hq * max_pages * kPageTokens) * sizeof(uint16_t));
+}
+static size_t anchor_refs_bytes(int64_t B, int64_t Hq, int64_t max_pages) {
+  return align256((size_t)(B * Hq * max_pages) * sizeof(float));
+}
+static size_t anchor_keys_bytes(int64_t B, int64_t Hq, int64_t max_pages) {
+  return align256((size_t)(B * Hq * max_pages * kPageTokens) * sizeof(uint32_t));
 }
 static size_t anchor_ml_bytes(int64_t B, int64_t Hq) { return align256((size_t)(B * Hq * 2) * sizeof(float)); }
 static size_t anchor_part_bytes(int64_t B, int64_t Hq) {
-  return align256((size_t)(B * Hq * 3 * kTopkParts * 2048) * sizeof(uint32_t));
+  return align256((size_t)(B * Hq * kTopkPasses * kTopkParts * 2048) * sizeof(uint32_t));
 }
 static size_t anchor_counts_bytes(int64_t B, int64_t Hq) {
   return align256((size_t)(B * Hq * kTopkParts * 2) * sizeof(uint32_t));
 }
-static constexpr size_t kScoreDummyBytes = 64 * 8 * sizeof(float);
+// dummy targets of the score stores: 64 x 8 codes, then 64 references
+static constexpr size_t kCodeDummyBytes = 64 * 8 * sizeof(uint16_t);
+static constexpr size_t kScoreDummyBytes = kCodeDummyBytes + 64 * sizeof(float);
 static size_t anchor_extra(int64_t B, int64_t Hq, int64_t max_pages) {
-  return anchor_scores_bytes(B, Hq, max_pages) + anchor_ml_bytes(B, Hq) + anchor_part_bytes(B, Hq) +
+  return anchor_codes_bytes(B, Hq, max_pages) + anchor_refs_bytes(B, Hq, max_pages) +
+         anchor_keys_bytes(B, Hq, max_pages) + anchor_ml_bytes(B, Hq) + anchor_part_bytes(B, Hq) +
          anchor_counts_bytes(B, Hq) + kScoreDummyBytes;
 }
 
@@ -656,22 +666,30 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
   float* part_ml = part_acc + acc_floats;
   a.part_acc = part_acc; a.part_ml = part_ml; a.max_splits = sp_bound.max_splits;
   if (a.ws_cu) a.ws_items = reinterpret_cast<int32_t*>(part_ml + acc_floats / D * 2);
-  float* scores = nullptr;
+  uint16_t* codes = nullptr;
+  float* refs = nullptr;
+  uint32_t* keys = nullptr;
   float* ml = nullptr;
   uint32_t* part = nullptr;
   uint32_t* counts = nullptr;
   if (x.mode == kAnchor) {
     char* w = reinterpret_cast<char*>(workspace) + align256(base_need);
-    scores = reinterpret_cast<float*>(w);
-    w += anchor_scores_bytes(B, Hq, max_pages);
+    codes = reinterpret_cast<uint16_t*>(w);
+    w += anchor_codes_bytes(B, Hq, max_pages);
+    refs = reinterpret_cast<float*>(w);
+    w += anchor_refs_bytes(B, Hq, max_pages);
+    keys = reinterpret_cast<uint32_t*>(w);
+    w += anchor_keys_bytes(B, Hq, max_pages);
     ml = reinterpret_cast<float*>(w);
     w += anchor_ml_bytes(B, Hq);
     part = reinterpret_cast<uint32_t*>(w);
     w += anchor_part_bytes(B, Hq);
     counts = reinterpret_cast<uint32_t*>(w);
     w += anchor_counts_bytes(B, Hq);
-    a.score_dummy = reinterpret_cast<float*>(w);
-    a.scores = scores;
+    a.code_dummy = reinterpret_cast<uint16_t*>(w);
+    a.ref_dummy = reinterpret_cast<float*>(w + kCodeDummyBytes);
+    a.score_codes = codes;
+    a.score_refs = refs;
     a.score_len = max_pages * kPageTokens;
   }
   if (x.mode == kReuse) {
@@ -702,7 +720,7 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
   if (x.mode == kAnchor && hs.n_ret) {
     TopkArgs t;
     std::memset(&t, 0, sizeof(t));
-    t.scores = scores; t.ml = ml; t.lens = lens; t.sel = x.sel_out;
+    t.score_codes = codes; t.score_refs = refs; t.keys = keys; t.ml = ml; t.lens = lens; t.sel = x.sel_out;
     t.B = (int)B; t.Hq = (int)Hq; t.gs = gs; t.n_kv = hs.n_ret;
     t.score_len = max_pages * kPageTokens;
     t.n_sel = x.top_k;

@@ -65,6 +65,12 @@ struct CacheView {
   uint8_t kv_heads[kMaxKvHeads];  // KV head ids; rank in the cache = index here
 };
 
+// Anchor score codes: scores rounded to 2^-11 log2 units (a probability moves
+// by at most 2^(2^-12) - 1 < 1.7e-4 of itself); the 16-bit code saturates just
+// under 32 log2 units below the reference, so probabilities below ~2^-32 of
+// their chunk's maximum all read as that bound.
+constexpr float kScoreCodeScale = 2048.f;
+
 // The decode split launch: paged-cache work items first (long), ring work items
 // after them (short, they fill the tail of the launch).
 struct DecodeArgs {
@@ -85,10 +91,17 @@ struct DecodeArgs {
   float scale;
   CacheView full;
   CacheView ring;
-  // Anchor layer (H2Share): scaled scores of the paged-cache heads,
-  // [B][Hq][score_len] in log2 units, for positions < lens.
-  float* scores;
-  float* score_dummy;           // 64 x 8 floats written by lanes without a query head
+  // Anchor layer (H2Share): the scaled scores (log2 units) of the paged-cache
+  // heads for positions < lens, rounded to multiples of 1 / kScoreCodeScale,
+  // each as a 16-bit distance below a reference: score = ref - code /
+  // kScoreCodeScale, with codes [B][Hq][score_len] and one reference per
+  // 16-token block, refs [B][Hq][score_len / 16] (the rounded maximum of the
+  // 32-token chunk the block was scored in).  Distances of 65535 steps and
+  // more saturate at 65535.
+  uint16_t* score_codes;
+  float* score_refs;
+  uint16_t* code_dummy;         // 64 x 8 codes written by lanes without a query head
+  float* ref_dummy;             // 64 references written by those lanes
   int32_t score_len;
   // Reuse layer (H2Share): paged-cache items attend to borrowed positions
   // sel[b][sel_rank[j]][0..n_sel) (ascending, -1 = none) of KV head j of the
@@ -185,18 +198,21 @@ hipError_t launch_classify(const ClassifyArgs& a, int d, hipStream_t s);
 // KV head j of the list), the n_sel positions of highest group-mean attention
 // probability, ascending, padded with -1.
 struct TopkArgs {
-  float* scores;                // [B][Hq][score_len]; the group's first head row is reused for keys
+  const uint16_t* score_codes;  // [B][Hq][score_len] (DecodeArgs::score_codes)
+  const float* score_refs;      // [B][Hq][score_len / 16]
+  uint32_t* keys;               // [B][n_kv][score_len] ranking keys of the lists
   const float* ml;              // [B][Hq][2] final (m, l)
   const int32_t* lens;
   int32_t* sel;                 // [B][n_kv][n_sel]
   int32_t B, Hq, gs, n_kv;
   int32_t score_len;            // positions per row (16 * pages per sequence)
   int32_t n_sel;
-  uint32_t* part;               // [B][n_kv][3][kTopkParts][2048] partial histograms
+  uint32_t* part;               // [B][n_kv][kTopkPasses][kTopkParts][2048] partial histograms
   uint32_t* counts;             // [B][n_kv][kTopkParts][2]  (above, equal to the threshold)
   uint8_t kv_heads[kMaxKvHeads];
 };
 constexpr int kTopkParts = 8;   // workgroups per (sequence, KV head) list
+constexpr int kTopkPasses = 2;  // 11-bit digits of the 22-bit ranking keys
 hipError_t launch_topk(const TopkArgs& a, hipStream_t s);
 
 // Cross-layer head similarity (H2Share): grams of both layers are in gram

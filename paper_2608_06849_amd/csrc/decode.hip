@@ -32,8 +32,8 @@ namespace aoh {
 template <int D, bool SCORES>
 __device__ __forceinline__ void fold_chunk(const DecodeArgs& a, const u32x4 (&kcur)[2][D / 32],
                                            u32x4 (&vcur)[D / 16], const bf16x8 (&qreg)[D / 32], int c, int tok_end,
-                                           int blk_end, bool head_ok, float* score_row, f32x4 (&acc)[D / 16],
-                                           float& m_run, float& l_run) {
+                                           int blk_end, bool head_ok, uint16_t* code_row, float* ref_row,
+                                           f32x4 (&acc)[D / 16], float& m_run, float& l_run) {
   constexpr int kKSteps = D / 32;
   constexpr int kDimBlocks = D / 16;
   const int lane = threadIdx.x & (kWave - 1);
@@ -60,21 +60,39 @@ __device__ __forceinline__ void fold_chunk(const DecodeArgs& a, const u32x4 (&kc
       x[4 * X + i] = v;
       mx = fmaxf(mx, v);
     }
-  if (SCORES) {
-    // Anchor layer: keep the scaled scores for the top-k selection.  Every
-    // lane issues the same two stores in every chunk (a fixed count, so the
-    // compiler's wait for the prefetched chunk stays exact): lanes without a
-    // query head, and lanes whose tokens lie past the range's last block (the
-    // missing second block of a range with an odd block count, which at the
-    // end of a full row would be the next row's first positions), write to a
-    // dummy area; masked positions before that (beyond the valid length,
-    // never read by the selection) get -inf.
-    float* sp = (head_ok && tok0 < blk_end * kPage) ? score_row + tok0 : a.score_dummy + 8 * lane;
-    *reinterpret_cast<f32x4*>(sp) = f32x4{x[0], x[1], x[2], x[3]};
-    *reinterpret_cast<f32x4*>(sp + 4) = f32x4{x[4], x[5], x[6], x[7]};
-  }
   mx = wave_xor_max(mx, 16);
   mx = wave_xor_max(mx, 32);
+  if (SCORES) {
+    // Anchor layer: keep the scaled scores for the top-k selection.  Each
+    // score is rounded to the code grid (kScoreCodeScale steps per log2 unit)
+    // and kept as its 16-bit distance below the grid point of the chunk's
+    // maximum for this head, which is the reference of each of the chunk's two
+    // blocks; a kept score therefore reads back as its own grid point
+    // whatever chunk it was scored in (equal scores stay equal), unless its
+    // distance saturates.  Masked positions (beyond the valid length, never
+    // read by the selection) saturate.  Every lane issues the same stores in
+    // every chunk (a fixed count, so the compiler's wait for the prefetched
+    // chunk stays exact): lanes without a query head, and lanes whose tokens
+    // lie past the range's last block (the missing second block of a range
+    // with an odd block count, which at the end of a full row would be the
+    // next row's first positions), write to a dummy area.
+    const bool keep = head_ok && tok0 < blk_end * kPage;
+    // grid points are integer-valued floats; mx is one of the scores, so
+    // every distance is >= 0; -inf scores give +inf, clamped before the
+    // conversion
+    const float top = rintf(mx * kScoreCodeScale);
+    uint32_t w[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t lo = (uint32_t)fminf(top - rintf(x[2 * j] * kScoreCodeScale), 65535.f);
+      const uint32_t hi = (uint32_t)fminf(top - rintf(x[2 * j + 1] * kScoreCodeScale), 65535.f);
+      w[j] = lo | (hi << 16);
+    }
+    uint16_t* cp = keep ? code_row + tok0 : a.code_dummy + 8 * lane;
+    *reinterpret_cast<u32x4*>(cp) = u32x4{w[0], w[1], w[2], w[3]};
+    // lane groups 0 and 2 start the chunk's two blocks
+    if ((G & 1) == 0) *(keep ? ref_row + tok0 / kPage : a.ref_dummy + lane) = top * (1.f / kScoreCodeScale);
+  }
   const float m_new = fmaxf(m_run, mx);  // finite: every chunk holds a valid token
   const float alpha = fast_exp2(m_run - m_new);
   m_run = m_new;
@@ -249,7 +267,9 @@ __device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const Cac
     }
 
     fold_chunk<D, SCORES>(a, kcur, vcur, qreg, c, tok_end, blk_end, head_ok,
-                          SCORES ? a.scores + ((int64_t)b * a.Hq + hq) * a.score_len : nullptr, acc, m_run, l_run);
+                          SCORES ? a.score_codes + ((int64_t)b * a.Hq + hq) * a.score_len : nullptr,
+                          SCORES ? a.score_refs + ((int64_t)b * a.Hq + hq) * (a.score_len / kPage) : nullptr, acc,
+                          m_run, l_run);
   }
 
   // Partial results of this split: m (log2 units), l, acc[D] for each head.

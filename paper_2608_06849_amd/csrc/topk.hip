@@ -4,14 +4,16 @@
 // heads share one index set).
 //
 // Each (sequence, retrieval KV head) list is cut into kTopkParts segments, one
-// workgroup of 1024 threads each, over five launches that exchange partial
+// workgroup of 1024 threads each, over four launches that exchange partial
 // histograms and counts through the workspace (no atomics in memory).  The score
 // of position j is the sum over the group's query heads of their attention
 // probability exp2(s_hj - m_h) / l_h (the mean up to the constant 1/gs, so the
-// same ranking), from the scaled scores the split pass kept and the final
-// (m, l) of the merge.  Probabilities are non-negative, so their fp32 bit
-// patterns order like the values; the k-th largest bit pattern is found by a
-// three-digit (11 + 11 + 10 bits) radix select over per-segment histograms, and the
+// same ranking), from the scaled scores the split pass kept (16-bit offsets
+// below a per-block reference) and the final (m, l) of the merge.  Probabilities are non-negative, so their fp32 bit
+// patterns order like the values.  Keys keep the top 22 bits of the pattern
+// (8 exponent and 13 mantissa bits: 1.2e-4 relative), so the k-th largest key
+// is found by a two-digit (11 + 11 bits) radix select over per-segment
+// histograms, and the
 // positions are then compacted in ascending order: every key above the
 // threshold, and as many keys equal to it as still needed, lowest positions
 // first.  Sequences with at most k positions select all of them; unused
@@ -66,9 +68,9 @@ constexpr int kTile = 4 * kTopkThreads;  // positions per compaction tile
 struct ListView {
   int n;                 // positions of the list (lens clamped to the score row)
   int seg0, seg1;        // this workgroup's segment [seg0, seg1)
-  uint32_t* keys;        // key row (the group's first score row)
-  const uint32_t* part;  // partial histograms of the list [3][kTopkParts][2048]
-  uint32_t* my_part;     // this workgroup's [3][...] slot base
+  uint32_t* keys;        // key row of the list
+  const uint32_t* part;  // partial histograms of the list [kTopkPasses][kTopkParts][2048]
+  uint32_t* my_part;     // this workgroup's [kTopkPasses][...] slot base
   uint32_t* counts;      // [kTopkParts][2]
   int32_t* out;
 };
@@ -76,17 +78,16 @@ struct ListView {
 __device__ __forceinline__ ListView list_view(const TopkArgs& a) {
   ListView v;
   const int p = blockIdx.x, kvl = blockIdx.y, b = blockIdx.z;
-  const int g = a.kv_heads[kvl];
   v.n = max(0, min(a.lens[b], a.score_len));
   // segments are whole compaction tiles
   const int per = (v.n + kTopkParts - 1) / kTopkParts;
   const int seg = ((per + kTile - 1) / kTile) * kTile;
   v.seg0 = min(v.n, p * seg);
   v.seg1 = min(v.n, v.seg0 + seg);
-  v.keys = reinterpret_cast<uint32_t*>(a.scores + ((int64_t)b * a.Hq + (int64_t)g * a.gs) * a.score_len);
   const int64_t list = (int64_t)b * a.n_kv + kvl;
-  v.part = a.part + list * 3 * kTopkParts * 2048;
-  v.my_part = a.part + list * 3 * kTopkParts * 2048 + (int64_t)p * 2048;
+  v.keys = a.keys + list * a.score_len;
+  v.part = a.part + list * kTopkPasses * kTopkParts * 2048;
+  v.my_part = a.part + list * kTopkPasses * kTopkParts * 2048 + (int64_t)p * 2048;
   v.counts = a.counts + list * kTopkParts * 2;
   v.out = a.sel + list * a.n_sel;
   return v;
@@ -119,16 +120,17 @@ __device__ __forceinline__ void find_digit(const uint32_t* part, int pass, int n
   __syncthreads();
 }
 
-constexpr int kShift[3] = {21, 10, 0};
-constexpr int kBins[3] = {2048, 2048, 1024};
+constexpr int kShift[kTopkPasses] = {21, 10};
+constexpr int kBins[kTopkPasses] = {2048, 2048};
+constexpr uint32_t kKeyMask = 0xFFFFFC00u;  // the key bits the two digits cover
 
 // Threshold key (the k-th largest) and the number of keys equal to it to take,
-// from the three histograms.
+// from the histograms of both digits.
 __device__ __forceinline__ void threshold(const ListView& v, int k, uint32_t& thr, uint32_t& need_eq,
                                           uint32_t* wsum, uint32_t* s_bin) {
   uint32_t kk = (uint32_t)k, prefix = 0, bin;
 #pragma unroll
-  for (int pass = 0; pass < 3; ++pass) {
+  for (int pass = 0; pass < kTopkPasses; ++pass) {
     find_digit(v.part, pass, kBins[pass], kk, bin, wsum, s_bin);
     prefix |= bin << kShift[pass];
   }
@@ -167,13 +169,20 @@ __global__ __launch_bounds__(kTopkThreads) void topk_hist_kernel(TopkArgs a) {
   __syncthreads();
   uint32_t* my_hist = hist[t & (kHistCopies - 1)];
   const int64_t row = a.score_len;
+  const int64_t head0 = (int64_t)b * a.Hq + (int64_t)g * a.gs;
+  const uint16_t* c0 = a.score_codes + head0 * row;
+  const float* r0 = a.score_refs + head0 * (row / 16);
   for (int j = v.seg0 + t; j < v.seg1; j += kTopkThreads) {
     uint32_t key;
     if (PASS == 0) {
-      const float* s0 = reinterpret_cast<const float*>(v.keys);
+      // score = ref - code / kScoreCodeScale (log2 units): a grid point,
+      // computed exactly, so equal kept scores give equal keys
       float p = 0.f;
-      for (int h = 0; h < a.gs; ++h) p += fast_exp2(s0[h * row + j] - s_m[h]) * s_il[h];
-      key = __builtin_bit_cast(uint32_t, p);
+      for (int h = 0; h < a.gs; ++h) {
+        const float xq = r0[h * (row / 16) + j / 16] - (float)c0[h * row + j] * (1.f / kScoreCodeScale);
+        p += fast_exp2(xq - s_m[h]) * s_il[h];
+      }
+      key = __builtin_bit_cast(uint32_t, p) & kKeyMask;
       v.keys[j] = key;
     } else {
       key = v.keys[j];
@@ -299,7 +308,6 @@ hipError_t launch_topk(const TopkArgs& a, hipStream_t s) {
   const dim3 grid(kTopkParts, a.n_kv, a.B);
   hipLaunchKernelGGL(topk_hist_kernel<0>, grid, dim3(kTopkThreads), 0, s, a);
   hipLaunchKernelGGL(topk_hist_kernel<1>, grid, dim3(kTopkThreads), 0, s, a);
-  hipLaunchKernelGGL(topk_hist_kernel<2>, grid, dim3(kTopkThreads), 0, s, a);
   hipLaunchKernelGGL(topk_count_kernel, grid, dim3(kTopkThreads), 0, s, a);
   hipLaunchKernelGGL(topk_compact_kernel, grid, dim3(kTopkThreads), 0, s, a);
   return hipGetLastError();

@@ -183,6 +183,47 @@ def test_anchor_exact_ties_go_to_lower_positions():
     assert idx.cpu().numpy()[0, 0].tolist() == [40, 90, 140]
 
 
+@pytest.mark.parametrize("scale,top_k", [
+    (1.0, 200),    # planted keys ~16-24 log2 units above the rest: the k-th score lies inside the code span
+    (5.0, 48),     # ~80-120 units above: the selection reaches scores far below the span (saturated codes)
+])
+def test_anchor_wide_score_range(scale, top_k):
+    # 24 planted K rows (a common direction times distinct factors) dominate
+    # the seeded ones by tens of log2 units, spread over many 32-token chunks,
+    # so a chunk holding one keeps the other positions' scores as large
+    # offsets below it (saturated in the second case); the selection is
+    # checked against the float64 oracle's group probabilities
+    B, L, hq, hkv, d, mask = 1, 3000, 8, 2, 128, [0, 0]
+    planted = synth.rng(11, "h2-wide").choice(L, 24, replace=False)
+
+    kk0 = synth.gaussian((B, L, hkv, d), 11, "h2-k")[0, 5]   # the planted direction, before boosting
+
+    def boost(kk):
+        u = kk[0, 5, :].copy()
+        for i, p in enumerate(planted):
+            kk[0, p, :] = u * scale * (1.0 + 0.02 * i)
+    k, v, full, ring = _decode_setup(B, L, hq, hkv, d, mask, 4, 16, 11, k_boost=boost)
+    _fill(k, v, mask, [L], full, None, 4, 16)
+    # query heads of group g aligned with the planted direction of KV head g
+    qq = np.stack([kk0[h // (hq // hkv)] for h in range(hq)])[None]
+    qq = qq + 0.2 * synth.gaussian((B, hq, d), 11, "h2-wide-q")
+    q = _bf(qq)
+    lens_t = torch.tensor([L], dtype=torch.int32, device=DEV)
+    _, idx = aoh_decode_anchor(q.to(DEV), full, None, mask, lens_t, 4, 16, top_k)
+    torch.cuda.synchronize()
+    got = idx.cpu().numpy()
+    n_exact = _check_selection(got, q, k, [L], mask, top_k, f"wide scores x{scale}")
+    # every planted position holding more than the absolute tolerance of its
+    # group's probability is selected (saturated codes only reorder positions
+    # below ~2^-32 of their chunk's maximum, far under that tolerance)
+    q64, k64 = f64(q), f64(k)
+    for r in range(hkv):
+        sc = HS.group_scores(q64, k64, [L], 0, r, hkv)
+        big = [p for p in planted.tolist() if sc[p] > 10 * SEL_ATOL]
+        assert big and set(big) <= set(got[0, r].tolist()), f"group {r}: a planted position was not selected"
+    print(f"wide scores x{scale}, top {top_k}: selections exact for {n_exact} lists")
+
+
 def _lists(B, n_lists, lens, top_k, seed):
     """Seeded borrowed lists: per (b, list) min(lens, top_k) distinct sorted positions, then -1."""
     out = np.full((B, n_lists, top_k), -1, dtype=np.int32)
