@@ -460,9 +460,9 @@ size_t aoh_decode_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t d_he
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 // Anchor extras: score codes [B][Hq][16 * max_pages] (16-bit) and their
-// references [B][Hq][max_pages], final (m, l) [B][Hq][2], and the top-k keys,
-// partial histograms and counts per (sequence, KV head) list (sized with Hq
-// lists per sequence, a bound on the retrieval KV heads).
+// references [B][Hq][max_pages], final (m, l) [B][Hq][2], and the top-k keys
+// and partial histograms per (sequence, KV head) list (sized with Hq lists per
+// sequence, a bound on the retrieval KV heads).
 static size_t anchor_codes_bytes(int64_t B, int64_t Hq, int64_t max_pages) {
   return align256((size_t)(B * Hq * max_pages * kPageTokens) * sizeof(uint16_t));
 }
@@ -476,16 +476,13 @@ static size_t anchor_ml_bytes(int64_t B, int64_t Hq) { return align256((size_t)(
 static size_t anchor_part_bytes(int64_t B, int64_t Hq) {
   return align256((size_t)(B * Hq * kTopkPasses * kTopkParts * 2048) * sizeof(uint32_t));
 }
-static size_t anchor_counts_bytes(int64_t B, int64_t Hq) {
-  return align256((size_t)(B * Hq * kTopkParts * 2) * sizeof(uint32_t));
-}
 // dummy targets of the score stores: 64 x 8 codes, then 64 references
 static constexpr size_t kCodeDummyBytes = 64 * 8 * sizeof(uint16_t);
 static constexpr size_t kScoreDummyBytes = kCodeDummyBytes + 64 * sizeof(float);
 static size_t anchor_extra(int64_t B, int64_t Hq, int64_t max_pages) {
   return anchor_codes_bytes(B, Hq, max_pages) + anchor_refs_bytes(B, Hq, max_pages) +
          anchor_keys_bytes(B, Hq, max_pages) + anchor_ml_bytes(B, Hq) + anchor_part_bytes(B, Hq) +
-         anchor_counts_bytes(B, Hq) + kScoreDummyBytes;
+         kScoreDummyBytes;
 }
 
 // H2Share roles of a decode call (Sec. "AoH-Guided Sparse Attention"): plain,
@@ -671,7 +668,6 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
   uint32_t* keys = nullptr;
   float* ml = nullptr;
   uint32_t* part = nullptr;
-  uint32_t* counts = nullptr;
   if (x.mode == kAnchor) {
     char* w = reinterpret_cast<char*>(workspace) + align256(base_need);
     codes = reinterpret_cast<uint16_t*>(w);
@@ -684,8 +680,6 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
     w += anchor_ml_bytes(B, Hq);
     part = reinterpret_cast<uint32_t*>(w);
     w += anchor_part_bytes(B, Hq);
-    counts = reinterpret_cast<uint32_t*>(w);
-    w += anchor_counts_bytes(B, Hq);
     a.code_dummy = reinterpret_cast<uint16_t*>(w);
     a.ref_dummy = reinterpret_cast<float*>(w + kCodeDummyBytes);
     a.score_codes = codes;
@@ -724,7 +718,7 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
     t.B = (int)B; t.Hq = (int)Hq; t.gs = gs; t.n_kv = hs.n_ret;
     t.score_len = max_pages * kPageTokens;
     t.n_sel = x.top_k;
-    t.part = part; t.counts = counts;
+    t.part = part;
     std::memcpy(t.kv_heads, hs.ret, hs.n_ret);
     e = launch_topk(t, s);
     if (e != hipSuccess) return fail(AOH_ERR_HIP, "top-k launch: %s", hipGetErrorString(e));

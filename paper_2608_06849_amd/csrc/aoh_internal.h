@@ -208,7 +208,6 @@ struct TopkArgs {
   int32_t score_len;            // positions per row (16 * pages per sequence)
   int32_t n_sel;
   uint32_t* part;               // [B][n_kv][kTopkPasses][kTopkParts][2048] partial histograms
-  uint32_t* counts;             // [B][n_kv][kTopkParts][2]  (above, equal to the threshold)
   uint8_t kv_heads[kMaxKvHeads];
 };
 constexpr int kTopkParts = 8;   // workgroups per (sequence, KV head) list

@@ -4,8 +4,8 @@
 // heads share one index set).
 //
 // Each (sequence, retrieval KV head) list is cut into kTopkParts segments, one
-// workgroup of 1024 threads each, over four launches that exchange partial
-// histograms and counts through the workspace (no atomics in memory).  The score
+// workgroup of 1024 threads each, over three launches that exchange partial
+// histograms through the workspace (no atomics in memory).  The score
 // of position j is the sum over the group's query heads of their attention
 // probability exp2(s_hj - m_h) / l_h (the mean up to the constant 1/gs, so the
 // same ranking), from the scaled scores the split pass kept (16-bit offsets
@@ -71,7 +71,6 @@ struct ListView {
   uint32_t* keys;        // key row of the list
   const uint32_t* part;  // partial histograms of the list [kTopkPasses][kTopkParts][2048]
   uint32_t* my_part;     // this workgroup's [kTopkPasses][...] slot base
-  uint32_t* counts;      // [kTopkParts][2]
   int32_t* out;
 };
 
@@ -88,7 +87,6 @@ __device__ __forceinline__ ListView list_view(const TopkArgs& a) {
   v.keys = a.keys + list * a.score_len;
   v.part = a.part + list * kTopkPasses * kTopkParts * 2048;
   v.my_part = a.part + list * kTopkPasses * kTopkParts * 2048 + (int64_t)p * 2048;
-  v.counts = a.counts + list * kTopkParts * 2;
   v.out = a.sel + list * a.n_sel;
   return v;
 }
@@ -199,27 +197,26 @@ __global__ __launch_bounds__(kTopkThreads) void topk_hist_kernel(TopkArgs a) {
   }
 }
 
-// Counts of keys above and equal to the threshold in this workgroup's segment.
-__global__ __launch_bounds__(kTopkThreads) void topk_count_kernel(TopkArgs a) {
-  __shared__ uint32_t wsum[kTopkWaves];
-  __shared__ uint32_t s_bin[2];
-  const ListView v = list_view(a);
-  if (v.n <= a.n_sel) return;
-  uint32_t thr, need_eq;
-  threshold(v, a.n_sel, thr, need_eq, wsum, s_bin);
-  uint32_t gt = 0, eq = 0;
-  for (int j = v.seg0 + (int)threadIdx.x; j < v.seg1; j += kTopkThreads) {
-    const uint32_t key = v.keys[j];
-    gt += key > thr;
-    eq += key == thr;
+// Keys above and equal to the threshold in the segments before this
+// workgroup's, from their partial histograms: keys carry exactly the two
+// digits, so a key above the threshold has a larger first digit, or the same
+// first digit and a larger second one, and a key equal to it has both digits.
+__device__ __forceinline__ void counts_before(const ListView& v, uint32_t thr, uint32_t& gt, uint32_t& eq,
+                                              uint32_t* wsum) {
+  const int t = threadIdx.x;
+  const uint32_t d0 = thr >> kShift[0], d1 = (thr >> kShift[1]) & (kBins[1] - 1);
+  uint32_t my_gt = 0, my_eq = 0;
+  for (int q = 0; q < (int)blockIdx.x; ++q) {
+    const uint32_t* h0 = v.part + (int64_t)q * 2048;
+    const uint32_t* h1 = v.part + ((int64_t)kTopkParts + q) * 2048;
+    for (int b = t; b < 2048; b += kTopkThreads) {
+      if ((uint32_t)b > d0) my_gt += h0[b];
+      if ((uint32_t)b > d1) my_gt += h1[b];
+    }
+    if (t == 0) my_eq += h1[d1];
   }
-  uint32_t tot_gt, tot_eq;
-  block_excl_scan(gt, wsum, tot_gt);
-  block_excl_scan(eq, wsum, tot_eq);
-  if (threadIdx.x == 0) {
-    v.counts[blockIdx.x * 2 + 0] = tot_gt;
-    v.counts[blockIdx.x * 2 + 1] = tot_eq;
-  }
+  block_excl_scan(my_gt, wsum, gt);
+  block_excl_scan(my_eq, wsum, eq);
 }
 
 // Ascending compaction of this workgroup's segment into the list: tiles of
@@ -239,11 +236,8 @@ __global__ __launch_bounds__(kTopkThreads) void topk_compact_kernel(TopkArgs a) 
   }
   uint32_t thr, need_eq;
   threshold(v, k, thr, need_eq, wsum, s_bin);
-  uint32_t gt_before = 0, eq_before0 = 0;
-  for (int q = 0; q < (int)blockIdx.x; ++q) {
-    gt_before += v.counts[q * 2 + 0];
-    eq_before0 += v.counts[q * 2 + 1];
-  }
+  uint32_t gt_before, eq_before0;
+  counts_before(v, thr, gt_before, eq_before0, wsum);
   const int lane = t & (kWave - 1), wave = t / kWave;
   uint32_t carry_eq = eq_before0;
   uint32_t carry_sel = gt_before + min(eq_before0, need_eq);
@@ -308,7 +302,6 @@ hipError_t launch_topk(const TopkArgs& a, hipStream_t s) {
   const dim3 grid(kTopkParts, a.n_kv, a.B);
   hipLaunchKernelGGL(topk_hist_kernel<0>, grid, dim3(kTopkThreads), 0, s, a);
   hipLaunchKernelGGL(topk_hist_kernel<1>, grid, dim3(kTopkThreads), 0, s, a);
-  hipLaunchKernelGGL(topk_count_kernel, grid, dim3(kTopkThreads), 0, s, a);
   hipLaunchKernelGGL(topk_compact_kernel, grid, dim3(kTopkThreads), 0, s, a);
   return hipGetLastError();
 }
