@@ -125,10 +125,10 @@ DECODE_SOURCES = ("decode.hip", "aoh_device.h", "aoh_internal.h")
 TRAFFIC = {
     "fetch_factor": 524301.2 / 1048576.0,   # FETCH_SIZE of a 1 GiB copy / 1 GiB
     "write_factor": 1048576.0 / 1048576.0,  # WRITE_SIZE of a 1 GiB copy / 1 GiB
-    "prefill_mixed": {"fetch_kib": 458095.5, "write_kib": 263256.0,
-                      "sources": PREFILL_SOURCES, "source_hash": "5f81a5122298f37b"},
-    "decode_ws": {"fetch_kib": 1081572.9, "write_kib": 1169.7,
-                  "sources": DECODE_SOURCES, "source_hash": "12a50a525449c597"},
+    "prefill_mixed": {"fetch_kib": 458024.0, "write_kib": 263257.4,
+                      "sources": PREFILL_SOURCES, "source_hash": "34211f06277739e8"},
+    "decode_ws": {"fetch_kib": 1081631.2, "write_kib": 1169.9,
+                  "sources": DECODE_SOURCES, "source_hash": "cdbad26860bafbbc"},
 }
 
 
