@@ -481,7 +481,10 @@ def h2share_decode(torch, q, full, ring, mask, lens, n_sink, window, B, Hq, D, m
     """H2Share decode on the same caches: an anchor step (decode + top-k
     selection) and a reuse step (retrieval groups attend to the anchor's
     top_k positions in their own cache; identity group mapping), each timed
-    alone; a block of `block` layers costs one anchor and block-1 reuse steps."""
+    alone; a block of `block` layers costs one anchor and block-1 reuse steps.
+    The reuse step is timed on token-major V pages (the layout of a reuse
+    layer's cache; the same tokens, V transposed) and, for comparison, on the
+    dimension-major pages the anchor reads."""
     from paper_2608_06849_amd import (aoh_decode_anchor, aoh_decode_anchor_workspace_bytes, aoh_decode_reuse,
                                       aoh_decode_reuse_workspace_bytes)
     n_ret, n_str = mask.count(0), mask.count(1)
@@ -512,16 +515,24 @@ def h2share_decode(torch, q, full, ring, mask, lens, n_sink, window, B, Hq, D, m
 
     anchor_ms = timed(lambda: aoh_decode_anchor(q, full, ring, mask, lens, n_sink, window, top_k, indices=idx,
                                                 out=out, workspace=ws_a))
-    reuse_ms = timed(lambda: aoh_decode_reuse(q, full, ring, mask, lens, n_sink, window, idx, mapping, out=out,
+    reuse_dm_ms = timed(lambda: aoh_decode_reuse(q, full, ring, mask, lens, n_sink, window, idx, mapping, out=out,
+                                                 workspace=ws_r))
+    # a reuse layer's own cache keeps token-major V pages (the layout its
+    # scattered reads want): the same pages with V transposed
+    from paper_2608_06849_amd import PagedCache
+    full_tm = PagedCache(full.k, full.v.transpose(-1, -2).contiguous(), full.block_table, v_token_major=True)
+    reuse_ms = timed(lambda: aoh_decode_reuse(q, full_tm, ring, mask, lens, n_sink, window, idx, mapping, out=out,
                                               workspace=ws_r))
+    del full_tm
     gs = Hq // len(mask)
     reuse_bytes = B * (n_ret * top_k + n_str * min(length, n_sink + window)) * D * 2 * 2
     per_layer = (anchor_ms + (block - 1) * reuse_ms) / block
-    log(f"H2Share: anchor {anchor_ms:.4f} ms, reuse {reuse_ms:.4f} ms (top-{top_k}); block of {block}: "
-        f"{per_layer:.4f} ms/layer vs {plain_ms:.4f} plain")
+    log(f"H2Share: anchor {anchor_ms:.4f} ms, reuse {reuse_ms:.4f} ms (top-{top_k}; {reuse_dm_ms:.4f} ms with "
+        f"dimension-major V pages); block of {block}: {per_layer:.4f} ms/layer vs {plain_ms:.4f} plain")
     return {
         "top_k": top_k, "block": block,
-        "anchor_ms": round(anchor_ms, 4), "reuse_ms": round(reuse_ms, 4), "plain_ms": round(plain_ms, 4),
+        "anchor_ms": round(anchor_ms, 4), "reuse_ms": round(reuse_ms, 4),
+        "reuse_ms_v_dim_major": round(reuse_dm_ms, 4), "plain_ms": round(plain_ms, 4),
         "anchor_overhead": round(anchor_ms / plain_ms, 3),
         "ms_per_layer_in_block": round(per_layer, 4),
         "speedup_per_layer_vs_plain": round(plain_ms / per_layer, 3),

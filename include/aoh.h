@@ -87,11 +87,18 @@ typedef struct {
  * block_table[b * max_pages_per_seq + p / 16], row p % 16.  Layouts
  * (contiguous, dtype = the call's dtype):
  *   k: [num_pages][n_heads][16][D]   token-major inside a page
- *   v: [num_pages][n_heads][D][16]   dimension-major inside a page
+ *   v: [num_pages][n_heads][D][16]   dimension-major inside a page, or, with
+ *      v_token_major = 1, [num_pages][n_heads][16][D] like k
  * block_table is a DEVICE int32 array [n_seqs][max_pages_per_seq]; the caller
  * allocates pages and fills it for every page a call touches.  A call with B
  * sequences requires n_seqs >= B (AOH_ERR_INVALID_ARG otherwise), so no row
  * outside the table is ever read.
+ * Token-major V pages are for the caches of H2Share reuse layers, which are
+ * only read at scattered borrowed positions: aoh_kv_append writes them and
+ * aoh_decode_reuse reads them (a borrowed token's V is then one contiguous
+ * row instead of a column spread over its page); aoh_decode, aoh_decode_step,
+ * aoh_decode_anchor and the prefill calls that fill caches return
+ * AOH_ERR_UNSUPPORTED for them.
  */
 typedef struct {
   void* k;
@@ -100,7 +107,8 @@ typedef struct {
   int64_t num_pages;
   int32_t max_pages_per_seq;
   int32_t n_heads;
-  int32_t n_seqs; /* rows of block_table */
+  int32_t n_seqs;        /* rows of block_table */
+  int32_t v_token_major; /* 0: dimension-major V pages; 1: token-major */
 } aoh_paged_cache;
 
 /*

@@ -11,7 +11,9 @@ from that description and from the documented cache layout of the C interface:
       token p of sequence b  ->  physical page block_table[b][p // 16],
                                  row p % 16 of that page
       K page: [num_pages][n_ret][16][D]   (token-major inside a page)
-      V page: [num_pages][n_ret][D][16]   (dimension-major inside a page)
+      V page: [num_pages][n_ret][D][16]   (dimension-major inside a page), or
+              [num_pages][n_ret][16][D] for a cache with token-major V pages
+              (the option meant for H2Share reuse layers)
 
   ring cache (streaming KV heads, rank s among the streaming KV heads),
   capacity C = n_sink + window slots, padded to a multiple of 16:
@@ -64,11 +66,12 @@ def split_heads(head_is_streaming):
     return ret, st
 
 
-def paged_read_token(k_pages, v_pages, block_table, b, r, p):
+def paged_read_token(k_pages, v_pages, block_table, b, r, p, v_token_major=False):
     """(K row, V row) of token p of sequence b, retrieval rank r, per the layout."""
     page = int(block_table[b][p // PAGE])
     row = p % PAGE
-    return k_pages[page, r, row, :], v_pages[page, r, :, row]
+    v_row = v_pages[page, r, row, :] if v_token_major else v_pages[page, r, :, row]
+    return k_pages[page, r, row, :], v_row
 
 
 def ring_read_slot(k_ring, v_ring, b, s, slot):
@@ -77,7 +80,7 @@ def ring_read_slot(k_ring, v_ring, b, s, slot):
     return k_ring[b, s, blk, row, :], v_ring[b, s, blk, :, row]
 
 
-def check_paged(k_pages, v_pages, block_table, k_seq, v_seq, lens, head_is_streaming):
+def check_paged(k_pages, v_pages, block_table, k_seq, v_seq, lens, head_is_streaming, v_token_major=False):
     """Compare every stored token of every retrieval head with the logical
     sequence, bit for bit.  Returns the number of mismatching tokens."""
     ret, _ = split_heads(head_is_streaming)
@@ -85,7 +88,7 @@ def check_paged(k_pages, v_pages, block_table, k_seq, v_seq, lens, head_is_strea
     for b in range(len(lens)):
         for r, g in enumerate(ret):
             for p in range(int(lens[b])):
-                kr, vr = paged_read_token(k_pages, v_pages, block_table, b, r, p)
+                kr, vr = paged_read_token(k_pages, v_pages, block_table, b, r, p, v_token_major)
                 if not (np.array_equal(kr, k_seq[b, p, g]) and np.array_equal(vr, v_seq[b, p, g])):
                     bad += 1
     return bad
@@ -108,14 +111,15 @@ def check_ring(k_ring, v_ring, k_seq, v_seq, lens, head_is_streaming, n_sink, wi
     return bad
 
 
-def gather_paged(k_pages, v_pages, block_table, b, r, length):
+def gather_paged(k_pages, v_pages, block_table, b, r, length, v_token_major=False):
     """K [length, D] and V [length, D] of sequence b, retrieval rank r, read
     through the block table per the layout (vectorised form of
     paged_read_token over positions 0..length-1)."""
     p = np.arange(length)
     pages = np.asarray(block_table[b])[p // PAGE]
     rows = p % PAGE
-    return k_pages[pages, r, rows, :], v_pages[pages, r, :, rows]
+    v_rows = v_pages[pages, r, rows, :] if v_token_major else v_pages[pages, r, :, rows]
+    return k_pages[pages, r, rows, :], v_rows
 
 
 def gather_ring(k_ring, v_ring, b, s, length, n_sink, window):

@@ -38,7 +38,7 @@ class AohTensor(ctypes.Structure):
 class AohPagedCache(ctypes.Structure):
     _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("block_table", ctypes.c_void_p),
                 ("num_pages", ctypes.c_int64), ("max_pages_per_seq", ctypes.c_int32),
-                ("n_heads", ctypes.c_int32), ("n_seqs", ctypes.c_int32)]
+                ("n_heads", ctypes.c_int32), ("n_seqs", ctypes.c_int32), ("v_token_major", ctypes.c_int32)]
 
 
 class AohRingCache(ctypes.Structure):
@@ -181,16 +181,23 @@ def _ptr(t):
 
 class PagedCache:
     """Retrieval-head cache: 16-token pages, K token-major and V dimension-major
-    inside a page, and a per-sequence block table (device int32)."""
+    inside a page (or token-major with v_token_major, for reuse layers), and a
+    per-sequence block table (device int32)."""
 
-    def __init__(self, k, v, block_table):
+    def __init__(self, k, v, block_table, v_token_major=False):
         self.k, self.v, self.block_table = k, v, block_table
+        self.v_token_major = bool(v_token_major)
 
     @classmethod
-    def allocate(cls, num_pages, n_heads, d, dtype, block_table, device="cuda"):
+    def allocate(cls, num_pages, n_heads, d, dtype, block_table, device="cuda", v_token_major=False):
         k = torch.empty((num_pages, n_heads, PAGE_TOKENS, d), dtype=dtype, device=device)
-        v = torch.empty((num_pages, n_heads, d, PAGE_TOKENS), dtype=dtype, device=device)
-        return cls(k, v, block_table.to(device=device, dtype=torch.int32).contiguous())
+        vshape = (num_pages, n_heads, PAGE_TOKENS, d) if v_token_major else (num_pages, n_heads, d, PAGE_TOKENS)
+        v = torch.empty(vshape, dtype=dtype, device=device)
+        return cls(k, v, block_table.to(device=device, dtype=torch.int32).contiguous(), v_token_major)
+
+    def rows(self, b0, b1):
+        """The same pages with block-table rows b0 .. b1-1 (sequences b0 .. b1-1)."""
+        return PagedCache(self.k, self.v, self.block_table[b0:b1], self.v_token_major)
 
     def desc(self):
         c = AohPagedCache()
@@ -200,6 +207,7 @@ class PagedCache:
         c.max_pages_per_seq = self.block_table.shape[1]
         c.n_heads = self.k.shape[1]
         c.n_seqs = self.block_table.shape[0]
+        c.v_token_major = int(self.v_token_major)
         return c
 
 

@@ -179,6 +179,7 @@ int32_t aoh_version(void) { return 100; }
 const char* aoh_last_error(void) { return g_err; }
 
 static aoh_status check_paged(const aoh_paged_cache* c, int n_ret, int64_t B);
+static aoh_status check_v_dim_major(const aoh_paged_cache* c, int n_ret, const char* call);
 static aoh_status check_ring(const aoh_ring_cache* c, int n_str, int n_sink, int window, int64_t B);
 
 // Prefill; with append set, also writes the prompt's K/V (positions 0..T-1 of
@@ -239,6 +240,7 @@ static aoh_status prefill_impl(const aoh_tensor* q, const aoh_tensor* k, const a
   if (n_qblocks * Hq * B >= (1ll << 31)) return fail(AOH_ERR_UNSUPPORTED, "grid too large");
   if (append) {
     if ((st = check_paged(kv_full, hs.n_ret, B))) return st;
+    if ((st = check_v_dim_major(kv_full, hs.n_ret, "a prefill that fills the caches"))) return st;
     if ((st = check_ring(kv_ring, hs.n_str, n_sink, window, B))) return st;
     if (B > 65535) return fail(AOH_ERR_UNSUPPORTED, "batch too large");
     // fp32 prompts are appended by a separate launch, which has no packed form
@@ -385,6 +387,17 @@ static aoh_status check_paged(const aoh_paged_cache* c, int n_ret, int64_t B) {
                 c->n_seqs, (long long)B);
   if (reinterpret_cast<uintptr_t>(c->k) % 16 || reinterpret_cast<uintptr_t>(c->v) % 16)
     return fail(AOH_ERR_INVALID_ARG, "kv_full: cache pointers must be 16-byte aligned");
+  if (c->v_token_major != 0 && c->v_token_major != 1)
+    return fail(AOH_ERR_INVALID_ARG, "kv_full.v_token_major=%d; must be 0 or 1", c->v_token_major);
+  return AOH_OK;
+}
+
+// Token-major V pages are written by aoh_kv_append and read by the reuse layer
+// only; the other readers and writers take dimension-major pages.
+static aoh_status check_v_dim_major(const aoh_paged_cache* c, int n_ret, const char* call) {
+  if (n_ret && c->v_token_major)
+    return fail(AOH_ERR_UNSUPPORTED, "%s needs dimension-major V pages (kv_full.v_token_major=0); "
+                "token-major pages are for aoh_kv_append and aoh_decode_reuse", call);
   return AOH_OK;
 }
 
@@ -435,6 +448,7 @@ aoh_status aoh_kv_append(const aoh_tensor* k_new, const aoh_tensor* v_new,
   if (hs.n_ret) {
     a.pk = kv_full->k; a.pv = kv_full->v; a.block_table = kv_full->block_table;
     a.max_pages = kv_full->max_pages_per_seq; a.num_pages = (int)kv_full->num_pages; a.n_ret = hs.n_ret;
+    a.v_token_major = kv_full->v_token_major;
   }
   if (hs.n_str) {
     a.rk = kv_ring->k; a.rv = kv_ring->v; a.n_str = hs.n_str;
@@ -526,6 +540,10 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
   HeadSchedule hs;
   if ((st = schedule_heads(head_is_streaming, (int)Hkv, &hs))) return st;
   if ((st = check_paged(kv_full, hs.n_ret, B))) return st;
+  if (x.mode != kReuse) {
+    const char* call = x.k_new ? "aoh_decode_step" : x.mode == kAnchor ? "aoh_decode_anchor" : "aoh_decode";
+    if ((st = check_v_dim_major(kv_full, hs.n_ret, call))) return st;
+  }
   if ((st = check_ring(kv_ring, hs.n_str, n_sink, window, B))) return st;
   const int gs = (int)(Hq / Hkv);
   if (dt == AOH_BF16 && gs > 16) return fail(AOH_ERR_UNSUPPORTED, "Hq/Hkv=%d > 16", gs);
@@ -580,6 +598,7 @@ static aoh_status decode_impl(const aoh_tensor* q, const aoh_paged_cache* kv_ful
     CacheView& c = a.full;
     c.k = kv_full->k; c.v = kv_full->v; c.block_table = kv_full->block_table;
     c.max_pages = kv_full->max_pages_per_seq; c.num_pages = (int)kv_full->num_pages;
+    c.v_token_major = kv_full->v_token_major;
     c.n_kv = hs.n_ret;
     c.split_blocks = sp.split_blocks_full; c.n_splits = sp.n_splits_full;
     c.n_groups = (int)ceil_div(sp.n_splits_full, kSplitWaves);

@@ -62,6 +62,7 @@ struct CacheView {
   int32_t n_splits;             // splits per (batch, KV head)
   int32_t n_groups;             // workgroups per (batch, KV head): ceil(n_splits / kSplitWaves)
   int32_t n_items;              // workgroups of the launch: B * n_kv * n_groups
+  int32_t v_token_major;        // paged: V pages [16][D] (read by the reuse layer only)
   uint8_t kv_heads[kMaxKvHeads];  // KV head ids; rank in the cache = index here
 };
 
@@ -152,6 +153,7 @@ struct AppendArgs {
   int32_t max_pages;
   int32_t num_pages;
   int32_t n_ret;
+  int32_t v_token_major;        // V pages [16][D] instead of [D][16]
   // ring cache
   void* rk;
   void* rv;

@@ -284,9 +284,11 @@ __device__ __forceinline__ void decode_split_body(const DecodeArgs& a, const Cac
 // borrowed position list).  The same 16x16x32 MFMA structure as the dense
 // body, on gathered tokens: each lane loads the K rows of its two MFMA rows
 // from their own pages (16-byte loads), and the V^T operand element by
-// element from the dimension-major pages (the 8 tokens of a lane group are in
-// general on 8 different pages).  List entries < 0 or beyond the sequence
-// are masked out.
+// element (the 8 tokens of a lane group are in general on 8 different pages).
+// With dimension-major V pages every element sits in its own 32-byte sector;
+// with token-major ones the 16 lanes of a group read 32 contiguous bytes of
+// one token's row per load.  List entries < 0 or beyond the sequence are
+// masked out.
 template <int D>
 __device__ __forceinline__ void decode_sparse_body(const DecodeArgs& a, const CacheView& cv, int b, int kvl,
                                                    int split, f32x4 (&acc)[D / 16], float& m_out, float& l_out) {
@@ -346,18 +348,22 @@ __device__ __forceinline__ void decode_sparse_body(const DecodeArgs& a, const Ca
     int vpos[8];
     bool vok[8];
     int64_t vb[8];
+    // element (token row r, dimension d) of a V page: r + 16 d (dimension-major)
+    // or D r + d (token-major)
+    const int v_row = cv.v_token_major ? D : 1;
+    const int v_dim = cv.v_token_major ? 1 : kPage;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       vpos[j] = __shfl(my_pos, 8 * G + j, kWave);
       vok[j] = vpos[j] >= 0 && vpos[j] < n_valid;
-      vb[j] = unit_of(vpos[j]) * (kPage * D) + (vok[j] ? vpos[j] % kPage : 0);
+      vb[j] = unit_of(vpos[j]) * (kPage * D) + (vok[j] ? vpos[j] % kPage : 0) * v_row;
     }
     bf16x8 vcur[kDimBlocks];
 #pragma unroll
     for (int nb = 0; nb < kDimBlocks; ++nb)
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const uint16_t raw = vc[vb[j] + (int64_t)(16 * nb + (lane & 15)) * kPage];
+        const uint16_t raw = vc[vb[j] + (int64_t)(16 * nb + (lane & 15)) * v_dim];
         vcur[nb][j] = vok[j] ? __builtin_bit_cast(bf16, raw) : (bf16)0.f;
       }
 

@@ -7,7 +7,8 @@
 // start position is read on the device.
 //   retrieval head -> paged cache: K rows copied as 16-byte vectors; V staged
 //     in LDS and written dimension-major ([D][16] per page), only for the
-//     positions of this append (a page may already hold earlier tokens).
+//     positions of this append (a page may already hold earlier tokens), or,
+//     for token-major V pages, copied like K.
 //   streaming head -> ring: a position is written only if no later position of
 //     the same append maps to its slot (p < n_sink or p >= end - window), so
 //     the final state is independent of the order in which lanes write.
@@ -55,9 +56,12 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
       if (p >= p_lo && p < p_hi) {
         const int t = p - start;
         st16(pk + (int64_t)row * D + cv * kVec, ld16(kn + (int64_t)t * a.k_st + cv * kVec));
-        *reinterpret_cast<u32x4*>(&vtile[row][cv * kVec]) = ld16(vn + (int64_t)t * a.v_st + cv * kVec);
+        const u32x4 vv = ld16(vn + (int64_t)t * a.v_st + cv * kVec);
+        if (a.v_token_major) st16(pv + (int64_t)row * D + cv * kVec, vv);
+        else *reinterpret_cast<u32x4*>(&vtile[row][cv * kVec]) = vv;
       }
     }
+    if (a.v_token_major) return;  // uniform across the workgroup
     __syncthreads();
     // Dimension-major V page: element (d, r) at pv[d * 16 + r].
     for (int e = tid; e < D * kPage; e += blockDim.x) {

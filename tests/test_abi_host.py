@@ -357,3 +357,37 @@ def test_noalloc_step_rejects_a_workspace_beyond_the_static_area():
                                          ctypes.byref(ring), ctypes.cast(mask, ctypes.c_void_p), ctypes.c_void_p(FAKE),
                                          4, 32, ctypes.byref(out), None)
     assert st == A.AOH_ERR_UNSUPPORTED and "static scratch" in A.aoh_last_error()
+
+
+def test_token_major_v_pages_only_for_append_and_reuse():
+    # a cache with token-major V pages is rejected, before any launch, by the
+    # calls that read or write dimension-major pages; an invalid flag is an
+    # argument error everywhere
+    L = A.lib()
+    q, out = _t((2, 8, 128)), _t((2, 8, 128))
+    mask = ctypes.create_string_buffer(b"\x00\x01", 2)
+    full = A.AohPagedCache(k=FAKE, v=FAKE, block_table=FAKE, num_pages=8, max_pages_per_seq=4, n_heads=1, n_seqs=2,
+                           v_token_major=1)
+    ring = A.AohRingCache(k=FAKE, v=FAKE, n_heads=1, capacity=36, batch=2)
+    need = A.aoh_decode_workspace_bytes(2, 8, 128, 4, 36)
+    m = ctypes.cast(mask, ctypes.c_void_p)
+    st = L.aoh_decode(ctypes.byref(q), ctypes.byref(full), ctypes.byref(ring), m, ctypes.c_void_p(FAKE), 4, 32,
+                      ctypes.byref(out), ctypes.c_void_p(FAKE), need, None)
+    assert st == A.AOH_ERR_UNSUPPORTED and "aoh_decode needs dimension-major" in A.aoh_last_error()
+    kn = _t((2, 2, 128))
+    st = L.aoh_decode_step(ctypes.byref(q), ctypes.byref(kn), ctypes.byref(kn), ctypes.byref(full),
+                           ctypes.byref(ring), m, ctypes.c_void_p(FAKE), 4, 32, ctypes.byref(out),
+                           ctypes.c_void_p(FAKE), need, None)
+    assert st == A.AOH_ERR_UNSUPPORTED and "aoh_decode_step" in A.aoh_last_error()
+    st = L.aoh_decode_anchor(ctypes.byref(q), ctypes.byref(full), ctypes.byref(ring), m, ctypes.c_void_p(FAKE), 4,
+                             32, 16, ctypes.c_void_p(FAKE), ctypes.byref(out), ctypes.c_void_p(FAKE), 1 << 40, None)
+    assert st == A.AOH_ERR_UNSUPPORTED and "aoh_decode_anchor" in A.aoh_last_error()
+    q4, k4, v4, o4 = _t((2, 64, 4, 128)), _t((2, 64, 2, 128)), _t((2, 64, 2, 128)), _t((2, 64, 4, 128))
+    st = L.aoh_prefill_append(ctypes.byref(q4), ctypes.byref(k4), ctypes.byref(v4), m, 4, 32, 0, ctypes.byref(full),
+                              ctypes.byref(ring), ctypes.byref(o4), None)
+    assert st == A.AOH_ERR_UNSUPPORTED and "prefill" in A.aoh_last_error()
+    full.v_token_major = 2
+    k5, v5 = _t((2, 5, 2, 128)), _t((2, 5, 2, 128))
+    st = L.aoh_kv_append(ctypes.byref(k5), ctypes.byref(v5), m, ctypes.c_void_p(FAKE), ctypes.byref(full),
+                         ctypes.byref(ring), 4, 32, None)
+    assert st == A.AOH_ERR_INVALID_ARG and "v_token_major" in A.aoh_last_error()

@@ -48,7 +48,7 @@ class Run:
         self.ws = torch.empty(max(ws, 16) // 4 + 4, dtype=torch.float32, device=DEV)
 
     def _views(self, b):
-        f = PagedCache(self.full.k, self.full.v, self.full.block_table[b:b + 1]) if self.full else None
+        f = self.full.rows(b, b + 1) if self.full else None
         r = RingCache(self.ring.k[b:b + 1], self.ring.v[b:b + 1], self.ring.capacity) if self.ring else None
         return f, r
 

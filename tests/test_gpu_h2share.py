@@ -21,6 +21,7 @@ import torch
 import synth
 from oracle import h2share as HS
 from oracle import attention as OA
+from oracle import cache_model as CM
 from paper_2608_06849_amd import (PagedCache, RingCache, aoh_decode, aoh_decode_anchor, aoh_decode_reuse,
                                   aoh_decode_workspace_bytes, aoh_head_mapping, aoh_kv_append)
 from tests.helpers import assert_parity, bits, f64
@@ -89,9 +90,9 @@ def test_mapping_qwen_shaped_layers():
 
 # ------------------------------------------------------------------------- decode
 
-def _decode_setup(B, L, hq, hkv, d, mask, n_sink, window, seed, k_boost=None):
-    """Seeded K/V for L positions of B sequences in a paged cache (shuffled pages)
-    and a ring, appended from position 0."""
+def _decode_setup(B, L, hq, hkv, d, mask, n_sink, window, seed, k_boost=None, v_token_major=False):
+    """Seeded K/V for L positions of B sequences in a paged cache (shuffled pages;
+    V pages token-major on request) and a ring, appended from position 0."""
     kk = synth.gaussian((B, L, hkv, d), seed, "h2-k")
     vv = synth.gaussian((B, L, hkv, d), seed, "h2-v")
     if k_boost is not None:
@@ -101,7 +102,7 @@ def _decode_setup(B, L, hq, hkv, d, mask, n_sink, window, seed, k_boost=None):
     max_pages = (L + 15) // 16
     perm = synth.page_permutation(B * max_pages, seed, "h2-pages")
     bt = torch.from_numpy(perm.reshape(B, max_pages).astype(np.int32))
-    full = PagedCache.allocate(B * max_pages, n_ret, d, BF, bt) if n_ret else None
+    full = PagedCache.allocate(B * max_pages, n_ret, d, BF, bt, v_token_major=v_token_major) if n_ret else None
     ring = RingCache.allocate(B, n_str, n_sink, window, d, BF) if n_str else None
     return k, v, full, ring
 
@@ -109,7 +110,7 @@ def _decode_setup(B, L, hq, hkv, d, mask, n_sink, window, seed, k_boost=None):
 def _fill(k, v, mask, lens, full, ring, n_sink, window):
     # append each sequence's first lens[b] tokens (the ring must end at lens[b])
     for b, n in enumerate(lens):
-        f = PagedCache(full.k, full.v, full.block_table[b:b + 1]) if full else None
+        f = full.rows(b, b + 1) if full else None
         rg = RingCache(ring.k[b:b + 1], ring.v[b:b + 1], ring.capacity) if ring else None
         aoh_kv_append(k[b:b + 1, :n].to(DEV), v[b:b + 1, :n].to(DEV), mask, torch.zeros(1, dtype=torch.int32, device=DEV),
                       f, rg, n_sink, window)
@@ -242,9 +243,10 @@ def _lists(B, n_lists, lens, top_k, seed):
     (2, 300, [300, 20], 4, 2, 64, [0, 0], [0, 0], 1, 64, 8),             # lens < top_k
     (1, 3000, [3000], 28, 4, 128, [0, 1, 0, 1], [1, -1, 0, -1], 2, 1024, 9),
 ])
-def test_reuse_decode(B, L, lens, hq, hkv, d, mask, mapping, n_lists, top_k, seed):
+@pytest.mark.parametrize("vtm", [False, True], ids=["v_dim_major", "v_token_major"])
+def test_reuse_decode(B, L, lens, hq, hkv, d, mask, mapping, n_lists, top_k, seed, vtm):
     n_sink, window = 8, 96
-    k, v, full, ring = _decode_setup(B, L, hq, hkv, d, mask, n_sink, window, seed)
+    k, v, full, ring = _decode_setup(B, L, hq, hkv, d, mask, n_sink, window, seed, v_token_major=vtm)
     _fill(k, v, mask, lens, full, ring, n_sink, window)
     q = _bf(synth.gaussian((B, hq, d), seed, "h2-q"))
     sel = _lists(B, n_lists, lens, top_k, seed)
@@ -255,6 +257,40 @@ def test_reuse_decode(B, L, lens, hq, hkv, d, mask, mapping, n_lists, top_k, see
     want = HS.reuse_decode(f64(q), f64(k), f64(v), lens, mask, n_sink, window, sel, mapping)
     mx, mean = assert_parity(out, want, BF, f"reuse {B, L, hq, hkv, d, top_k}")
     print(f"reuse {B, L, hq, hkv, d, top_k}: max abs {mx:.2e} mean {mean:.2e}")
+
+
+def test_reuse_token_major_v_equals_dimension_major():
+    # the same tokens appended to a cache of each V layout (ragged prompt
+    # chunks starting mid-page, then single-token steps): both caches hold every
+    # token bit for bit in their own layout, and the reuse step reads them to
+    # bit-identical outputs (same products in the same order)
+    B, L, hq, hkv, d, mask = 2, 1000, 8, 2, 128, [0, 1]
+    n_sink, window, seed = 4, 64, 12
+    lens = [1000, 613]
+    caches = [_decode_setup(B, L, hq, hkv, d, mask, n_sink, window, seed, v_token_major=t) for t in (False, True)]
+    k, v = caches[0][0], caches[0][1]
+    outs = []
+    for _, _, full, ring in caches:
+        full.k.fill_(float("nan"))
+        full.v.fill_(float("nan"))
+        for b, n in enumerate(lens):
+            f = full.rows(b, b + 1)
+            rg = RingCache(ring.k[b:b + 1], ring.v[b:b + 1], ring.capacity)
+            cut = [0, 37, n - 3, n - 2, n - 1, n]            # 37 tokens, then up to the last 3, then 1 at a time
+            for lo, hi in zip(cut, cut[1:]):
+                start = torch.full((1,), lo, dtype=torch.int32, device=DEV)
+                aoh_kv_append(k[b:b + 1, lo:hi].to(DEV), v[b:b + 1, lo:hi].to(DEV), mask, start, f, rg, n_sink, window)
+        torch.cuda.synchronize()
+        bad = CM.check_paged(bits(full.k), bits(full.v), full.block_table.cpu().numpy(), bits(k), bits(v), lens, mask,
+                             v_token_major=full.v_token_major)
+        assert bad == 0, f"{bad} tokens wrong in the cache (v_token_major={full.v_token_major})"
+        q = _bf(synth.gaussian((B, hq, d), seed, "h2-q"))
+        sel = _lists(B, 1, lens, 300, seed)
+        out = aoh_decode_reuse(q.to(DEV), full, ring, mask, torch.tensor(lens, dtype=torch.int32, device=DEV), n_sink,
+                               window, torch.from_numpy(sel).to(DEV), [0, -1])
+        torch.cuda.synchronize()
+        outs.append(out)
+    assert np.array_equal(bits(outs[0]), bits(outs[1])), "reuse output depends on the V page layout"
 
 
 def test_reuse_every_position_matches_oracle_full_decode():

@@ -82,7 +82,7 @@ def test_varlen_fills_the_caches_like_per_sequence_appends():
     off = 0
     for b, n in enumerate(lens):
         if n:
-            fb = PagedCache(f2.k, f2.v, f2.block_table[b:b + 1])
+            fb = f2.rows(b, b + 1)
             rb = RingCache(r2.k[b:b + 1], r2.v[b:b + 1], r2.capacity)
             ref = aoh_prefill_append(q[off:off + n][None].contiguous(), k[off:off + n][None].contiguous(),
                                      v[off:off + n][None].contiguous(), mask, n_sink, window, fb, rb)

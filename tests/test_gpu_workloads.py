@@ -146,7 +146,7 @@ def test_varlen_sweep(sparsity, sweep_seqs):
             T = sq["q"].shape[1]
             qd, kd, vd = sq["q"].to(DEV), sq["k"].to(DEV), sq["v"].to(DEV)
             out = aoh_prefill(qd, kd, vd, mask, n_sink, window)
-            f = PagedCache(full.k, full.v, full.block_table[b:b + 1]) if full else None
+            f = full.rows(b, b + 1) if full else None
             r = RingCache(ring.k[b:b + 1], ring.v[b:b + 1], ring.capacity) if ring else None
             aoh_kv_append(kd, vd, mask, lens[b:b + 1], f, r, n_sink, window)
             lens[b:b + 1] += T

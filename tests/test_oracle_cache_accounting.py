@@ -55,6 +55,20 @@ def test_paged_and_ring_readers_follow_layout():
     assert M.ring_capacity_padded(64, 1024) == 1088 and M.ring_capacity_padded(4, 32) == 48
 
 
+def test_paged_reader_follows_the_token_major_v_layout():
+    # the same hand-placed token with V pages [num_pages][n_ret][16][D]
+    d, n_pages = 4, 5
+    kp = np.zeros((n_pages, 2, 16, d))
+    vp = np.zeros((n_pages, 2, 16, d))
+    bt = np.array([[3, 0, 4]])
+    kp[0, 1, 2, :] = 7.0      # token 18 = page index 1 -> physical 0, row 2, rank 1
+    vp[0, 1, 2, :] = np.arange(d) + 1.0
+    k, v = M.paged_read_token(kp, vp, bt, 0, 1, 18, v_token_major=True)
+    assert (k == 7).all() and v.tolist() == [1.0, 2.0, 3.0, 4.0]
+    K, V = M.gather_paged(kp, vp, bt, 0, 1, 19, v_token_major=True)
+    assert V[18].tolist() == [1.0, 2.0, 3.0, 4.0] and (V[:18] == 0).all()
+
+
 @pytest.mark.parametrize("t", [1, 2, 5, 31, 32, 33, 36, 37, 100, 256])
 @pytest.mark.parametrize("n_sink,window", [(4, 32), (0, 1), (3, 3), (40, 2)])
 def test_visible_pairs_closed_form_matches_mask_count(t, n_sink, window):
@@ -195,6 +209,22 @@ def test_checker_counts_a_v_column_of_the_wrong_token():
     page = c["bt"][0, 0]
     c["vp"][page, 0, :, 5] = c["vs"][0, 6, 0]       # token 5's V column holds token 6
     assert _bad_paged(c) == 1
+
+
+def _token_major(c):
+    """The same image with token-major V pages, by index arithmetic."""
+    c = dict(c)
+    c["vp"] = np.ascontiguousarray(np.swapaxes(c["vp"], 2, 3))
+    return c
+
+
+def test_checker_reads_token_major_v_pages():
+    c = _token_major(_cache_image())
+    args = (c["kp"], c["vp"], c["bt"], c["ks"], c["vs"], c["lens"], c["mask"])
+    assert M.check_paged(*args, v_token_major=True) == 0
+    page = c["bt"][1, 50 // 16]
+    c["vp"][page, 1, 50 % 16, 2] += 1.0             # one element of token 50's V row
+    assert M.check_paged(*args, v_token_major=True) == 1
 
 
 def test_checker_counts_a_stale_ring_slot_after_wrap():
