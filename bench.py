@@ -513,26 +513,67 @@ def h2share_decode(torch, q, full, ring, mask, lens, n_sink, window, B, Hq, D, m
         torch.cuda.synchronize()
         return ev[0].elapsed_time(ev[1]) / n
 
-    anchor_ms = timed(lambda: aoh_decode_anchor(q, full, ring, mask, lens, n_sink, window, top_k, indices=idx,
-                                                out=out, workspace=ws_a))
-    reuse_dm_ms = timed(lambda: aoh_decode_reuse(q, full, ring, mask, lens, n_sink, window, idx, mapping, out=out,
-                                                 workspace=ws_r))
+    def graph_timed(fn, n=20, reps=5):
+        """Per-call time of fn from one HIP graph of n calls replayed reps
+        times (GPU time, without a host dispatch per call, which a ~20 us
+        call cannot hide), and whether the last replay left the same outputs,
+        bit for bit, as an eager call."""
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fn()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(n):
+                fn()
+        g.replay()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record()
+        for _ in range(reps):
+            g.replay()
+        ev[1].record()
+        torch.cuda.synchronize()
+        got, got_idx = out.clone(), idx.clone()
+        fn()
+        torch.cuda.synchronize()
+        same = bool(torch.equal(got.view(torch.int16), out.view(torch.int16)) and torch.equal(got_idx, idx))
+        del g
+        return ev[0].elapsed_time(ev[1]) / (reps * n), same
+
+    def anchor():
+        aoh_decode_anchor(q, full, ring, mask, lens, n_sink, window, top_k, indices=idx, out=out, workspace=ws_a)
+
     # a reuse layer's own cache keeps token-major V pages (the layout its
     # scattered reads want): the same pages with V transposed
     from paper_2608_06849_amd import PagedCache
     full_tm = PagedCache(full.k, full.v.transpose(-1, -2).contiguous(), full.block_table, v_token_major=True)
-    reuse_ms = timed(lambda: aoh_decode_reuse(q, full_tm, ring, mask, lens, n_sink, window, idx, mapping, out=out,
-                                              workspace=ws_r))
+
+    def reuse(f):
+        return lambda: aoh_decode_reuse(q, f, ring, mask, lens, n_sink, window, idx, mapping, out=out, workspace=ws_r)
+
+    anchor_eager_ms = timed(anchor)
+    reuse_eager_ms = timed(reuse(full_tm))
+    anchor_ms, ok_a = graph_timed(anchor)
+    anchor()                                   # the reuse steps borrow this anchor's selection
+    reuse_dm_ms, ok_dm = graph_timed(reuse(full))
+    reuse_ms, ok_r = graph_timed(reuse(full_tm))
     del full_tm
     gs = Hq // len(mask)
     reuse_bytes = B * (n_ret * top_k + n_str * min(length, n_sink + window)) * D * 2 * 2
     per_layer = (anchor_ms + (block - 1) * reuse_ms) / block
-    log(f"H2Share: anchor {anchor_ms:.4f} ms, reuse {reuse_ms:.4f} ms (top-{top_k}; {reuse_dm_ms:.4f} ms with "
-        f"dimension-major V pages); block of {block}: {per_layer:.4f} ms/layer vs {plain_ms:.4f} plain")
+    log(f"H2Share (graph-timed): anchor {anchor_ms:.4f} ms, reuse {reuse_ms:.4f} ms (top-{top_k}; {reuse_dm_ms:.4f} ms "
+        f"with dimension-major V pages); block of {block}: {per_layer:.4f} ms/layer vs {plain_ms:.4f} plain; "
+        f"eager calls: anchor {anchor_eager_ms:.4f} ms, reuse {reuse_eager_ms:.4f} ms; "
+        f"graph replays equal eager: {ok_a and ok_dm and ok_r}")
     return {
-        "top_k": top_k, "block": block,
+        "top_k": top_k, "block": block, "timing": "per call from a HIP graph of 20 calls",
         "anchor_ms": round(anchor_ms, 4), "reuse_ms": round(reuse_ms, 4),
         "reuse_ms_v_dim_major": round(reuse_dm_ms, 4), "plain_ms": round(plain_ms, 4),
+        "anchor_eager_ms": round(anchor_eager_ms, 4), "reuse_eager_ms": round(reuse_eager_ms, 4),
+        "graph_replays_equal_eager": ok_a and ok_dm and ok_r,
         "anchor_overhead": round(anchor_ms / plain_ms, 3),
         "ms_per_layer_in_block": round(per_layer, 4),
         "speedup_per_layer_vs_plain": round(plain_ms / per_layer, 3),

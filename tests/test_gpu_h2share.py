@@ -24,6 +24,7 @@ from oracle import attention as OA
 from oracle import cache_model as CM
 from paper_2608_06849_amd import (PagedCache, RingCache, aoh_decode, aoh_decode_anchor, aoh_decode_reuse,
                                   aoh_decode_workspace_bytes, aoh_head_mapping, aoh_kv_append)
+from paper_2608_06849_amd import aoh as A
 from tests.helpers import assert_parity, bits, f64
 
 pytestmark = pytest.mark.gpu
@@ -430,3 +431,52 @@ def test_anchor_odd_page_count_full_last_page():
     for b in range(B):
         for r in range(2):
             assert set(range(16)) <= set(got[b, r].tolist())
+
+
+def test_anchor_and_reuse_replay_from_a_graph():
+    # the anchor step (split keeping score codes, merge, three top-k launches)
+    # and the reuse step on token-major V pages, captured as one HIP graph:
+    # every replay, with eager calls and synchronisations between replays,
+    # leaves the eager outputs bit for bit
+    B, L, hq, hkv, d, mask = 2, 2500, 8, 2, 128, [0, 1]
+    n_sink, window, seed, top_k = 4, 64, 13, 200
+    lens = [2500, 1777]
+    k, v, full, ring = _decode_setup(B, L, hq, hkv, d, mask, n_sink, window, seed)
+    _fill(k, v, mask, lens, full, ring, n_sink, window)
+    _, _, full_tm, ring_tm = _decode_setup(B, L, hq, hkv, d, mask, n_sink, window, seed, v_token_major=True)
+    _fill(k, v, mask, lens, full_tm, ring_tm, n_sink, window)
+    q = _bf(synth.gaussian((B, hq, d), seed, "h2-q")).to(DEV)
+    lens_t = torch.tensor(lens, dtype=torch.int32, device=DEV)
+    idx = torch.empty((B, 1, top_k), dtype=torch.int32, device=DEV)
+    out_a, out_r = torch.empty_like(q), torch.empty_like(q)
+    ws_a = torch.empty(A.aoh_decode_anchor_workspace_bytes(B, hq, d, full.block_table.shape[1], n_sink + window),
+                       dtype=torch.uint8, device=DEV)
+    ws_r = torch.empty(A.aoh_decode_reuse_workspace_bytes(B, hq, d, top_k, n_sink + window), dtype=torch.uint8,
+                       device=DEV)
+
+    def step():
+        aoh_decode_anchor(q, full, ring, mask, lens_t, n_sink, window, top_k, indices=idx, out=out_a, workspace=ws_a)
+        aoh_decode_reuse(q, full_tm, ring_tm, mask, lens_t, n_sink, window, idx, [0, -1], out=out_r, workspace=ws_r)
+
+    step()
+    torch.cuda.synchronize()
+    want = [bits(out_a), idx.cpu().numpy().copy(), bits(out_r)]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    for rep in range(3):
+        out_a.zero_(); out_r.zero_(); idx.fill_(-7)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = [bits(out_a), idx.cpu().numpy(), bits(out_r)]
+        for w, x, name in zip(want, got, ("anchor output", "indices", "reuse output")):
+            assert np.array_equal(w, x), f"replay {rep}: {name} differs from the eager call"
+        step()                                  # eager work between the replays
+        torch.cuda.synchronize()
