@@ -168,6 +168,27 @@ def test_anchor_decode(B, L, lens, hq, hkv, d, mask, top_k, seed):
     print(f"anchor {B, L, hq, hkv, d, top_k}: selections exact for {n_exact} separable lists")
 
 
+def test_anchor_many_sequences_fixed_splits():
+    # more sequences than the work-space split takes: the anchor runs on fixed
+    # splits per (sequence, KV head); outputs equal aoh_decode bit for bit and
+    # every list is a valid top-k of the oracle's scores
+    B, L, hq, hkv, d, mask, top_k, seed = 70, 400, 8, 2, 128, [0, 1], 64, 14
+    n_sink, window = 4, 64
+    lens = [int(x) for x in synth.rng(seed, "h2-many-lens").integers(30, L + 1, size=B)]
+    k, v, full, ring = _decode_setup(B, L, hq, hkv, d, mask, n_sink, window, seed)
+    _fill(k, v, mask, lens, full, ring, n_sink, window)
+    q = _bf(synth.gaussian((B, hq, d), seed, "h2-q"))
+    lens_t = torch.tensor(lens, dtype=torch.int32, device=DEV)
+    out_a, idx = aoh_decode_anchor(q.to(DEV), full, ring, mask, lens_t, n_sink, window, top_k)
+    ws = torch.empty(aoh_decode_workspace_bytes(B, hq, d, full.block_table.shape[1], n_sink + window) // 4 + 4,
+                     dtype=torch.float32, device=DEV)
+    out_d = aoh_decode(q.to(DEV), full, ring, mask, lens_t, n_sink, window, workspace=ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits(out_a), bits(out_d)), "anchor output differs from aoh_decode"
+    n_exact = _check_selection(idx.cpu().numpy(), q, k, lens, mask, top_k, f"anchor B={B}")
+    print(f"anchor B={B}: selections exact for {n_exact} separable lists")
+
+
 def test_anchor_exact_ties_go_to_lower_positions():
     # K rows at positions 40, 90, 140, 190, 240 are identical and dominant: five
     # exactly tied scores for a top-3 selection -> positions 40, 90, 140
