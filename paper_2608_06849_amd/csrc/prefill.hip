@@ -594,12 +594,15 @@ __global__ __launch_bounds__(kPrefillRowsF32) void prefill_f32_kernel(PrefillArg
 // query head, 32 rows per wave, S^T = K.Q^T and O^T += V^T.P^T on the 32x32x16
 // bf16 MFMA, online softmax in fp32); differences:
 //  * K/V tiles move global -> LDS with direct loads (global_load_lds_dwordx4),
-//    no register staging, into a ring of four 32 KB stages, issued two tiles
-//    ahead of their first use.
+//    no register staging, into a K ring and a V ring of four 16 KB tiles
+//    each, issued two tiles ahead of their first use.
 //  * Rows hold 16 chunks of 16 bytes with no padding; chunk c of row r sits
 //    at c ^ (r & 15) for K and c ^ 4 (r & 3) for V, which keeps the K row
-//    reads and the V transpose reads free of bank conflicts and makes every
-//    operand address one base register XOR a constant.
+//    reads and the V transpose reads free of bank conflicts.  Every operand
+//    address is one of 12 per-lane base registers plus a constant, and the
+//    tile loop runs four tiles per pass so that each ring slot is a
+//    compile-time constant too: the operand reads take it as an immediate
+//    offset, with no address arithmetic per tile.
 //  * Per tile t a wave runs an MFMA phase (P(t-1).V(t-1) then K(t).Q^T, at
 //    raised wave priority) and a vector phase (mask, exponentials of S(t)
 //    against a trailing reference max, no max pass unless the tile's
@@ -608,17 +611,23 @@ __global__ __launch_bounds__(kPrefillRowsF32) void prefill_f32_kernel(PrefillArg
 //    the vector phase for waves 0-3, after the MFMA phase for waves 4-7).
 //    The loop has a single path (a tile with no visible key for a wave
 //    yields P = 0), so the accumulators never move between registers.
+//  * The fused cache append writes the block's own (diagonal) tiles after
+//    the loop, from the ring, which still holds them.
 //  * Workgroups are ordered so that the query heads of one KV group and query
 //    block run on the same XCD (one L2).
-constexpr int kPPStages = 4;  // LDS stages of 32 KB
+constexpr int kPPStages = 4;  // slots of the K and V rings
 constexpr int kPPD = 128;
 constexpr int kPPRows = kPrefillRows;     // query rows per workgroup (8 waves x 32)
 static_assert(kPPRows == 256 && kPrefillRB == 1, "phase-shifted kernel: 8 waves x 32 rows");
 
-struct PPStage {
-  uint16_t k[kBN * kPPD];
-  uint16_t v[kBN * kPPD];
+// The LDS rings of the d_head-128 kernel: the K tiles of the kPPStages slots,
+// then their V tiles (a slot's offset within a ring fits the 16-bit immediate
+// offset of an LDS read).
+struct PPRing {
+  uint16_t k[kPPStages][kBN * kPPD];
+  uint16_t v[kPPStages][kBN * kPPD];
 };
+constexpr uint32_t kPPTileBytes = kBN * kPPD * 2;  // one K or V tile
 // Element offset of 16-byte chunk c of row r in a stage's K / V tile.
 __device__ __forceinline__ int pp_koff(int r, int c) { return r * kPPD + 8 * (c ^ (r & 15)); }
 __device__ __forceinline__ int pp_voff(int r, int c) { return r * kPPD + 8 * (c ^ (4 * (r & 3))); }
@@ -703,8 +712,8 @@ __device__ __forceinline__ bool pp_work_item(const PrefillArgs& a, int rows, int
 // if no later prompt position maps to its slot).  Threads tid, tid + nthr, ..
 // take the 16-byte chunks of the tile; crank = the KV head's rank in the cache.
 template <bool STREAM>
-__device__ __forceinline__ void pp_write_tile(const PrefillArgs& a, const PPStage& st, int kb, int b, int crank,
-                                              int T, int tid, int nthr) {
+__device__ __forceinline__ void pp_write_tile(const PrefillArgs& a, const uint16_t* tk, const uint16_t* tv, int kb,
+                                              int b, int crank, int T, int tid, int nthr) {
   constexpr int D = kPPD;
   constexpr int kCh = D / 8;
   uint16_t* ck = static_cast<uint16_t*>(a.ck);
@@ -718,7 +727,7 @@ __device__ __forceinline__ void pp_write_tile(const PrefillArgs& a, const PPStag
       const int page = a.block_table[(int64_t)b * a.max_pages + lp];
       if (page < 0 || page >= a.num_pages) continue;
       uint16_t* dst = ck + (((int64_t)page * a.n_cache + crank) * kPageTokens + p % kPageTokens) * D + 8 * ch;
-      st16(dst, *reinterpret_cast<const u32x4*>(&st.k[pp_koff(row, ch)]));
+      st16(dst, *reinterpret_cast<const u32x4*>(&tk[pp_koff(row, ch)]));
     }
     for (int e = tid; e < (kBN / kPageTokens) * D * 2; e += nthr) {
       const int pg = e / (2 * D), d = (e / 2) % D, hf = e % 2;
@@ -734,11 +743,11 @@ __device__ __forceinline__ void pp_write_tile(const PrefillArgs& a, const PPStag
         u32x4 w;
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          w[j] = (uint32_t)st.v[pp_voff(row0 + 2 * j, dc) + de] |
-                 ((uint32_t)st.v[pp_voff(row0 + 2 * j + 1, dc) + de] << 16);
+          w[j] = (uint32_t)tv[pp_voff(row0 + 2 * j, dc) + de] |
+                 ((uint32_t)tv[pp_voff(row0 + 2 * j + 1, dc) + de] << 16);
         st16(dst, w);
       } else {
-        for (int j = 0; p0 + j < T; ++j) dst[j] = st.v[pp_voff(row0 + j, dc) + de];
+        for (int j = 0; p0 + j < T; ++j) dst[j] = tv[pp_voff(row0 + j, dc) + de];
       }
     }
   } else {
@@ -749,19 +758,19 @@ __device__ __forceinline__ void pp_write_tile(const PrefillArgs& a, const PPStag
       const int slot = p < a.n_sink ? p : a.n_sink + (p - a.n_sink) % a.window;
       const int64_t unit = ((int64_t)b * a.n_cache + crank) * a.ring_blocks + slot / kPageTokens;
       const int r = slot % kPageTokens;
-      st16(ck + unit * (kPageTokens * D) + r * D + 8 * ch, *reinterpret_cast<const u32x4*>(&st.k[pp_koff(row, ch)]));
+      st16(ck + unit * (kPageTokens * D) + r * D + 8 * ch, *reinterpret_cast<const u32x4*>(&tk[pp_koff(row, ch)]));
       uint16_t* rv = cv + unit * (kPageTokens * D);
       const int vo = pp_voff(row, ch);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) rv[(8 * ch + j) * kPageTokens + r] = st.v[vo + j];
+      for (int j = 0; j < 8; ++j) rv[(8 * ch + j) * kPageTokens + r] = tv[vo + j];
     }
   }
 }
 
 // One work item (workgroup index wg of its launch's item space) of the
-// d_head-128 kernel; lds = the kPPStages-stage ring of the workgroup.
+// d_head-128 kernel; ring = the workgroup's LDS rings.
 template <bool STREAM, bool OUT_F32, bool APPEND>
-__device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PPStage* lds) {
+__device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PPRing& ring) {
   constexpr int D = kPPD;
   constexpr int kKSteps = D / 16;
   constexpr int kMBlocks = D / 32;
@@ -826,15 +835,16 @@ __device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PP
   }
   auto issue_tile = [&](int it) {
     const int kb = plan.tile(it) * kBN;
-    PPStage& st = lds[it % kPPStages];
+    uint16_t* sk = ring.k[it % kPPStages];
+    uint16_t* sv = ring.v[it % kPPStages];
     if (kb + kBN <= T) {
       const uint16_t* kt = kp + (int64_t)kb * a.k_st;
       const uint16_t* vt = vp + (int64_t)kb * a.v_st;
 #pragma unroll
       for (int jj = 0; jj < 2; ++jj) {
         const int j = 2 * wave + jj;
-        lds_dma16(kt + dma_k[jj], &st.k[4 * j * kPPD]);
-        lds_dma16(vt + dma_v[jj], &st.v[4 * j * kPPD]);
+        lds_dma16(kt + dma_k[jj], &sk[4 * j * kPPD]);
+        lds_dma16(vt + dma_v[jj], &sv[4 * j * kPPD]);
       }
     } else {
 #pragma unroll
@@ -843,8 +853,8 @@ __device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PP
         const int r = dma_r[jj];
         const int pc = lane & 15;
         const int64_t row = min(kb + r, T - 1);
-        lds_dma16(kp + row * a.k_st + 8 * (pc ^ (r & 15)), &st.k[4 * j * kPPD]);
-        lds_dma16(vp + row * a.v_st + 8 * (pc ^ (4 * (r & 3))), &st.v[4 * j * kPPD]);
+        lds_dma16(kp + row * a.k_st + 8 * (pc ^ (r & 15)), &sk[4 * j * kPPD]);
+        lds_dma16(vp + row * a.v_st + 8 * (pc ^ (4 * (r & 3))), &sv[4 * j * kPPD]);
       }
     }
   };
@@ -869,24 +879,28 @@ __device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PP
   // block mb (transpose reads): row 16 ks + 4 h2 + i16 / 4 (+ 8 rows for the
   // second half), logical chunk 4 mb + 2 (q16 & 1) + (i16 & 3) / 2, 4 more
   // elements for odd i16; that is vaddr0 ^ 64 mb (+ 4 KB per key step).
-  // Stage bases are multiples of 32 KB, so the XORs stay inside a row.
   const int q16 = lane >> 4;
   const int i16 = lane & 15;
-  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&lds[0]));
+  const uint32_t kring0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&ring.k[0][0]));
+  const uint32_t vring0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&ring.v[0][0]));
   const uint32_t kaddr0 = 2u * (uint32_t)pp_koff(l32, h2);
   const int vrow0 = 4 * h2 + (i16 >> 2);
   const uint32_t vaddr0 = 2u * (uint32_t)(pp_voff(vrow0, 2 * (q16 & 1) + ((i16 & 3) >> 1)) + 4 * (i16 & 1));
-  auto stage_k = [&](int st) { return lds0 + (uint32_t)st * (uint32_t)sizeof(PPStage) + kaddr0; };
-  auto stage_v = [&](int st) {
-    return lds0 + (uint32_t)st * (uint32_t)sizeof(PPStage) + (uint32_t)(kBN * kPPD * 2) + vaddr0;
-  };
-  auto k_operand = [&](uint32_t kb_addr, int s, int blk) {
+  // The swizzle XORs touch bits below 256 and the rings are 1 KB aligned, so
+  // a slot offset adds after them: operand addresses are these per-lane bases
+  // plus constants (immediate offsets once the slot is known at compile time).
+  uint32_t kx[kKSteps], vx[kMBlocks];
+#pragma unroll
+  for (int s = 0; s < kKSteps; ++s) kx[s] = (kring0 + kaddr0) ^ (32u * s);
+#pragma unroll
+  for (int mb = 0; mb < kMBlocks; ++mb) vx[mb] = (vring0 + vaddr0) ^ (64u * mb);
+  auto k_operand = [&](int st, int s, int blk) {
     typedef __attribute__((address_space(3))) const bf16x8 lds_bf16x8;
-    return *reinterpret_cast<lds_bf16x8*>((kb_addr ^ (32u * s)) + 8192u * blk);
+    return *reinterpret_cast<lds_bf16x8*>(kx[s] + (uint32_t)st * kPPTileBytes + 8192u * blk);
   };
-  auto v_operand = [&](uint32_t vb_addr, int ks, int mb) {
+  auto v_operand = [&](int st, int ks, int mb) {
     typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-    const uint32_t a = (vb_addr ^ (64u * mb)) + 4096u * ks;
+    const uint32_t a = vx[mb] + (uint32_t)st * kPPTileBytes + 4096u * ks;
     const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(reinterpret_cast<lds_i16x4*>(a));
     const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(reinterpret_cast<lds_i16x4*>(a + 2048u));
     return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
@@ -900,25 +914,25 @@ __device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PP
            (STREAM && !(kb + kBN - 1 < a.n_sink || kb >= lo_of(r0 + 31, a.chunk, a.window)));
   };
 
-  // Fused append (as in prefill_bf16_kernel): the first query head of each
-  // group copies its block's own K/V rows from LDS into the cache; each wave
-  // writes its share (a fixed per-thread partition) in its MFMA phase of the
-  // tile.
+  // Fused append: the first query head of each group copies its block's own
+  // K/V rows from LDS into the cache.  They are the block's diagonal tiles,
+  // the last (up to four) tiles of the loop, which the ring still holds when
+  // the loop ends; the workgroup writes them then.
   const bool writer = APPEND && (qh_local % a.gs) == 0;
   const int crank = qh_local / a.gs;
-  auto write_tile = [&](const PPStage& st, int kb) { pp_write_tile<STREAM>(a, st, kb, b, crank, T, tid, 512); };
+  auto write_tile = [&](int st, int kb) {
+    pp_write_tile<STREAM>(a, ring.k[st], ring.v[st], kb, b, crank, T, tid, 512);
+  };
 
-  // MFMA phase of tile t: O^T += V(t-1)^T P(t-1)^T, then S^T(t) = K(t) Q^T.
-  int v_tile = 0;  // tile whose P^T is in pop
-  auto pv_part = [&]() {
-    const uint32_t va = stage_v(v_tile % kPPStages);
+  // MFMA phase of tile t (stage st = t % kPPStages): O^T += V(t-1)^T
+  // P(t-1)^T (stage vst), then S^T(t) = K(t) Q^T.
+  auto pv_part = [&](int vst) {
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
-      for (int mb = 0; mb < kMBlocks; ++mb) acc_o[mb] = mfma32(v_operand(va, ks, mb), pop[ks], acc_o[mb]);
+      for (int mb = 0; mb < kMBlocks; ++mb) acc_o[mb] = mfma32(v_operand(vst, ks, mb), pop[ks], acc_o[mb]);
   };
-  auto qk_part = [&](int t) {
-    const uint32_t ka = stage_k(t % kPPStages);
+  auto qk_part = [&](int st) {
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
@@ -926,12 +940,12 @@ __device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PP
 #pragma unroll
     for (int s = 0; s < kKSteps; ++s)
 #pragma unroll
-      for (int blk = 0; blk < 2; ++blk) sacc[blk] = mfma32(k_operand(ka, s, blk), qreg[s], sacc[blk]);
+      for (int blk = 0; blk < 2; ++blk) sacc[blk] = mfma32(k_operand(st, s, blk), qreg[s], sacc[blk]);
   };
-  auto append_tile = [&](int t) {
+  auto append_tile = [&](int t, int st) {
     if (APPEND && writer) {
       const int kb = plan.tile(t) * kBN;
-      if (kb >= i0 && kb < i0 + kPPRows) write_tile(lds[t % kPPStages], kb);
+      if (kb >= i0 && kb < i0 + kPPRows) write_tile(st, kb);
     }
   };
   // Steady-state MFMA phase.  Both products run unconditionally (a wave with
@@ -940,11 +954,10 @@ __device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PP
   // The MFMA phase runs at raised wave priority (s_setprio, this wave only):
   // its SIMD also holds a wave of the other group in its vector phase, and
   // the matrix core is kept fed first (2-3% faster than equal priority).
-  auto mfma_phase = [&](int t) {
-    append_tile(t);
+  auto mfma_phase = [&](int t, int st) {
     __builtin_amdgcn_s_setprio(1);
-    pv_part();
-    qk_part(t);
+    pv_part((st + kPPStages - 1) % kPPStages);
+    qk_part(st);
     // Operands are read four MFMAs ahead of their products, the first K
     // operands while the last P.V products run.
     __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
@@ -1027,7 +1040,6 @@ __device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PP
     l_run += tsum;
   };
   auto valu_phase = [&](int t) {
-    v_tile = t;
     const int kb = plan.tile(t) * kBN;
     if (wave_dead(kb)) {
 #pragma unroll
@@ -1073,18 +1085,33 @@ __device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PP
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
   barrier();
 
-  append_tile(0);
   qk_part(0);
   if (grp == 1) sync_tile(0);
   valu_phase(0);
   if (grp == 0) sync_tile(0);
-  for (int t = 1; t < n; ++t) {
-    mfma_phase(t);
+  // Tiles 1, 2, 3, 4, 5, .. use stages 1, 2, 3, 0, 1, ..: the loop runs four
+  // tiles per pass with each stage a compile-time constant (its operand
+  // addresses are then immediate offsets), the last n - 1 mod 4 tiles with
+  // the stage computed.
+  auto tile_step = [&](int t, int st) {
+    mfma_phase(t, st);
     if (grp == 1) sync_tile(t);
     valu_phase(t);
     if (grp == 0) sync_tile(t);
+  };
+  int t = 1;
+  for (; t + 3 < n; t += 4) {
+    tile_step(t, 1);
+    tile_step(t + 1, 2);
+    tile_step(t + 2, 3);
+    tile_step(t + 3, 0);
   }
-  pv_part();
+  for (; t < n; ++t) tile_step(t, t % kPPStages);
+  pv_part((n - 1) % kPPStages);
+  // every wave passed the barrier of tile n-1 after its loads of the last
+  // tiles completed, so the ring holds them
+  if (APPEND && writer)
+    for (int u = max(n - kPPStages, 0); u < n; ++u) append_tile(u, u % kPPStages);
 
   // Epilogue: normalise by the row sum, store.
   const float l_tot = xor32_sum(l_run);
@@ -1120,8 +1147,8 @@ __device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PP
 
 template <bool STREAM, bool OUT_F32, bool APPEND>
 __global__ __launch_bounds__(512, 1) void prefill_pp_kernel(PrefillArgs a) {
-  __shared__ __align__(1024) PPStage lds[kPPStages];
-  prefill_pp_body<STREAM, OUT_F32, APPEND>(a, blockIdx.x, lds);
+  __shared__ __align__(1024) PPRing ring;
+  prefill_pp_body<STREAM, OUT_F32, APPEND>(a, blockIdx.x, ring);
 }
 
 // Both head types of a layer in one launch: workgroups [0, n_ret) take the
@@ -1132,10 +1159,10 @@ __global__ __launch_bounds__(512, 1) void prefill_pp_kernel(PrefillArgs a) {
 template <bool OUT_F32, bool APPEND>
 __global__ __launch_bounds__(512, 1) void prefill_pp_mixed_kernel(PrefillArgs ar, PrefillArgs as, int n_ret,
                                                                   int ret_pad) {
-  __shared__ __align__(1024) PPStage lds[kPPStages];
+  __shared__ __align__(1024) PPRing ring;
   const int wg = blockIdx.x;
-  if (wg < n_ret) prefill_pp_body<false, OUT_F32, APPEND>(ar, wg, lds);
-  else if (wg >= ret_pad) prefill_pp_body<true, OUT_F32, APPEND>(as, wg - ret_pad, lds);
+  if (wg < n_ret) prefill_pp_body<false, OUT_F32, APPEND>(ar, wg, ring);
+  else if (wg >= ret_pad) prefill_pp_body<true, OUT_F32, APPEND>(as, wg - ret_pad, ring);
 }
 
 template <int D, bool STREAM, bool OUT_F32>
