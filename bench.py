@@ -125,9 +125,9 @@ DECODE_SOURCES = ("decode.hip", "aoh_device.h", "aoh_internal.h")
 TRAFFIC = {
     "fetch_factor": 524301.2 / 1048576.0,   # FETCH_SIZE of a 1 GiB copy / 1 GiB
     "write_factor": 1048576.0 / 1048576.0,  # WRITE_SIZE of a 1 GiB copy / 1 GiB
-    "prefill_mixed": {"fetch_kib": 457020.7, "write_kib": 263255.1,
-                      "sources": PREFILL_SOURCES, "source_hash": "d111e7aa82149578"},
-    "decode_ws": {"fetch_kib": 1081745.4, "write_kib": 1169.7,
+    "prefill_mixed": {"fetch_kib": 458275.0, "write_kib": 263242.4,
+                      "sources": PREFILL_SOURCES, "source_hash": "cdc3e753b85ee5e0"},
+    "decode_ws": {"fetch_kib": 1081754.2, "write_kib": 1169.9,
                   "sources": DECODE_SOURCES, "source_hash": "21a01592fbd3549f"},
 }
 
