@@ -666,15 +666,19 @@ __device__ __forceinline__ bool pp_work_item(const PrefillArgs& a, int rows, int
     // XCD-aware order.  Workgroups go to the 8 XCDs (each with its own L2)
     // in turn; work item group j = (query block, sequence, KV head), heaviest
     // block first, holds the gs query heads that read the same K/V tiles.
-    // Group j runs on XCD j % 8 as gs consecutive workgroups of that XCD, so
-    // its tiles are fetched into that L2 once; the trailing groups that do
-    // not fill a round of 8 are dealt out in plain order.
+    // Round m of 8 groups runs as gs consecutive workgroups on each XCD, so a
+    // group's tiles are fetched into one L2 once.  Even rounds deal the groups
+    // to XCDs 0..7, odd rounds to XCDs 7..0: the groups get lighter along the
+    // order, and alternating keeps each XCD's total work level (dealt in one
+    // direction, XCD 0 would take the heaviest group of every round).  The
+    // trailing groups that do not fill a round of 8 are dealt in plain order.
     const int n_groups = a.n_qblocks * a.n_kv * a.B;
     const int full = 8 * a.gs * (n_groups / 8);
     int j, hl;
     if (wg < full) {
       const int slot = wg >> 3;
-      j = 8 * (slot / a.gs) + (wg & 7);
+      const int m = slot / a.gs;
+      j = 8 * m + ((m & 1) ? 7 - (wg & 7) : (wg & 7));
       hl = slot % a.gs;
     } else {
       j = (full / a.gs) + (wg - full) / a.gs;
