@@ -42,6 +42,15 @@
  *     interface.
  *   - Calls are thread-safe; calls that write the same cache or workspace
  *     concurrently race, as any two kernels writing one buffer would.
+ *   - The prefill calls (aoh_prefill, aoh_prefill_chunked, aoh_prefill_append,
+ *     aoh_prefill_varlen) hand the streaming items of their one-launch form
+ *     (both head types in one kernel, at d_head 128) out through work-queue
+ *     counters in the library's own device memory (a static array per GPU,
+ *     not an allocation): each such launch takes the next of 64 counter slots
+ *     and leaves it cleared when it ends.  Prefill launches may run at the
+ *     same time on different streams unless 64 others were enqueued between
+ *     them; a prefill launch captured in a HIP graph must not run at the same
+ *     time as another replay of that graph.
  */
 #ifndef AOH_H_
 #define AOH_H_

@@ -31,6 +31,7 @@
 //
 // fp32 kernel: a plain per-row kernel (one thread per query row) kept exact
 // for fp32 inputs; it has no performance role.
+#include <atomic>
 #include <type_traits>
 
 #include "aoh_device.h"
@@ -1155,19 +1156,83 @@ __global__ __launch_bounds__(512, 1) void prefill_pp_kernel(PrefillArgs a) {
   prefill_pp_body<STREAM, OUT_F32, APPEND>(a, blockIdx.x, ring);
 }
 
+// Schedule of the streaming items of the one-launch form.  The XCDs run at
+// different speeds under this load (several percent apart), and the slowest
+// sets the end of a launch whose items are dealt to them in equal shares.
+// The retrieval items keep their static XCD-aware order; the light streaming
+// items at the end are taken dynamically: queue x holds the items the
+// XCD-aware order puts on XCD x (index w with w % 8 == x), a workgroup takes
+// the next item of the queue of the XCD it runs on (read from the XCC_ID
+// register) or, once that is empty, of another queue, and the launch has
+// kStreamSlack more streaming workgroups than items so that a fast XCD can
+// take over a slow one's share.  Workgroups that find every queue empty exit.
+// The queue counters live in one of kSchedSlots slots of a device array,
+// chosen per launch by the host; the last workgroup to take (or fail to take)
+// an item clears the slot.  Launches that run at the same time therefore
+// need different slots: consecutive launches take consecutive slots.
+constexpr int kSchedSlots = 64;
+constexpr float kStreamSlack = 0.25f;
+__device__ uint32_t g_pp_sched[kSchedSlots][16];  // [0, 8): queue heads; [8]: workgroups served
+
+// XCD (0..7) the calling wave runs on: bits 3:0 of hardware register XCC_ID.
+__device__ __forceinline__ int pp_xcc() { return __builtin_amdgcn_s_getreg((3 << 11) | 20) & 7; }
+
+// Next item for a workgroup on XCD x, or -1 when every queue is empty.
+// Queue y holds ceil((n - y) / 8) items.
+__device__ __forceinline__ int pp_grab(uint32_t* q, int n, int x) {
+  {
+    const int n_x = (n - x + 7) >> 3;
+    if (n_x > 0) {
+      const uint32_t k = atomicAdd(&q[x], 1u);
+      if (k < (uint32_t)n_x) return 8 * (int)k + x;
+    }
+  }
+  for (;;) {
+    uint32_t head[8];
+#pragma unroll
+    for (int y = 0; y < 8; ++y) head[y] = __hip_atomic_load(&q[y], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    int pick = -1;
+    for (int d = 1; d < 8 && pick < 0; ++d) {
+      const int y = (x + d) & 7;
+      if (head[y] < (uint32_t)((n - y + 7) >> 3)) pick = y;
+    }
+    if (pick < 0) return -1;
+    const uint32_t k = atomicAdd(&q[pick], 1u);
+    if (k < (uint32_t)((n - pick + 7) >> 3)) return 8 * (int)k + pick;
+  }
+}
+
 // Both head types of a layer in one launch: workgroups [0, n_ret) take the
-// retrieval items, [ret_pad, ret_pad + streaming items) the streaming ones
-// (ret_pad = n_ret rounded up to the 8 XCDs, so both item spaces keep their
-// XCD-aware order).  The light streaming items are dispatched last and fill
-// the CUs that the causal retrieval items leave idle at the end.
+// retrieval items, [ret_pad, ret_pad + n_dyn) the n_str streaming ones
+// through the queues above (ret_pad = n_ret rounded up to the 8 XCDs, so both
+// item spaces keep their XCD-aware order).  The light streaming items are
+// dispatched last and fill the CUs that the causal retrieval items leave
+// idle at the end.
 template <bool OUT_F32, bool APPEND>
 __global__ __launch_bounds__(512, 1) void prefill_pp_mixed_kernel(PrefillArgs ar, PrefillArgs as, int n_ret,
-                                                                  int ret_pad) {
+                                                                  int ret_pad, int n_str, int n_dyn, int slot) {
   __shared__ __align__(1024) PPRing ring;
+  __shared__ int s_item;
   const int wg = blockIdx.x;
-  if (wg < n_ret) prefill_pp_body<false, OUT_F32, APPEND>(ar, wg, ring);
-  else if (wg >= ret_pad) prefill_pp_body<true, OUT_F32, APPEND>(as, wg - ret_pad, ring);
+  if (wg < n_ret) {
+    prefill_pp_body<false, OUT_F32, APPEND>(ar, wg, ring);
+    return;
+  }
+  if (wg < ret_pad) return;
+  uint32_t* q = g_pp_sched[slot];
+  if (threadIdx.x == 0) {
+    s_item = pp_grab(q, n_str, pp_xcc());
+    if (atomicAdd(&q[8], 1u) == (uint32_t)n_dyn - 1) {
+#pragma unroll
+      for (int y = 0; y < 9; ++y) atomicExch(&q[y], 0u);
+    }
+  }
+  __syncthreads();
+  const int w = __builtin_amdgcn_readfirstlane(s_item);
+  if (w >= 0) prefill_pp_body<true, OUT_F32, APPEND>(as, w, ring);
 }
+
+static std::atomic<uint32_t> g_sched_next{0};
 
 template <int D, bool STREAM, bool OUT_F32>
 static hipError_t launch_bf16(const PrefillArgs& a, hipStream_t s) {
@@ -1210,14 +1275,19 @@ hipError_t launch_prefill_mixed(const PrefillArgs& ar, const PrefillArgs& as, in
   const int n_ret = ar.n_qblocks * ar.n_kv * ar.gs * ar.B;
   const int n_str = as.n_qblocks * as.n_kv * as.gs * as.B;
   const int ret_pad = (n_ret + 7) / 8 * 8;
-  const dim3 grid(ret_pad + n_str), blk(512);
+  const int n_dyn = (int)((1.f + kStreamSlack) * n_str / 8 + 1) * 8;
+  const int slot = (int)(g_sched_next.fetch_add(1, std::memory_order_relaxed) % kSchedSlots);
+  const dim3 grid(ret_pad + n_dyn), blk(512);
   const bool app = ar.append;
+  auto go = [&](auto kern) {
+    hipLaunchKernelGGL(kern, grid, blk, 0, s, ar, as, n_ret, ret_pad, n_str, n_dyn, slot);
+  };
   if (out_f32) {
-    if (app) hipLaunchKernelGGL((prefill_pp_mixed_kernel<true, true>), grid, blk, 0, s, ar, as, n_ret, ret_pad);
-    else hipLaunchKernelGGL((prefill_pp_mixed_kernel<true, false>), grid, blk, 0, s, ar, as, n_ret, ret_pad);
+    if (app) go(prefill_pp_mixed_kernel<true, true>);
+    else go(prefill_pp_mixed_kernel<true, false>);
   } else {
-    if (app) hipLaunchKernelGGL((prefill_pp_mixed_kernel<false, true>), grid, blk, 0, s, ar, as, n_ret, ret_pad);
-    else hipLaunchKernelGGL((prefill_pp_mixed_kernel<false, false>), grid, blk, 0, s, ar, as, n_ret, ret_pad);
+    if (app) go(prefill_pp_mixed_kernel<false, true>);
+    else go(prefill_pp_mixed_kernel<false, false>);
   }
   return hipGetLastError();
 }

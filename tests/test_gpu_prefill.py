@@ -198,6 +198,49 @@ def test_one_launch_equals_per_type_launches(B, T, Hq, Hkv, mask):
         assert np.array_equal(bits(one), bits(out.index_select(2, qi))), f"head type {typ}"
 
 
+def test_one_launch_queue_slots_across_calls_streams_and_graph_replays():
+    # The one-launch form hands its streaming items out through work-queue
+    # counters in one of 64 slots per launch, cleared by the launch's last
+    # workgroup.  Every later launch must see its slot cleared: more calls
+    # than slots on one stream, calls overlapping on two streams, and replays
+    # of a captured call all give the output of a first call, bit for bit.
+    B, T, Hq, Hkv, D, mask, n_sink, window = 1, 2000, 28, 4, 128, [0, 1, 0, 1], 64, 256
+    q, k, v = _inputs(B, T, Hq, Hkv, D, torch.bfloat16, seed=77)
+    ref = bits(aoh_prefill(q, k, v, mask, n_sink, window))
+    out = torch.empty_like(q)
+    for i in range(70):
+        aoh_prefill(q, k, v, mask, n_sink, window, out=out)
+        torch.cuda.synchronize()
+        assert np.array_equal(bits(out), ref), f"call {i} on one stream"
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    outs = [torch.empty_like(q) for _ in range(2)]
+    torch.cuda.synchronize()
+    for i in range(8):
+        for st, o in zip((s1, s2), outs):
+            with torch.cuda.stream(st):
+                aoh_prefill(q, k, v, mask, n_sink, window, out=o)
+    torch.cuda.synchronize()
+    for j, o in enumerate(outs):
+        assert np.array_equal(bits(o), ref), f"stream {j}"
+    g_out = torch.empty_like(q)
+    g = torch.cuda.CUDAGraph()
+    cap = torch.cuda.Stream()
+    cap.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(cap):
+        aoh_prefill(q, k, v, mask, n_sink, window, out=g_out)  # warm-up outside the graph
+        with torch.cuda.graph(g, stream=cap):
+            aoh_prefill(q, k, v, mask, n_sink, window, out=g_out)
+    torch.cuda.synchronize()
+    for r in range(5):
+        g_out.zero_()
+        aoh_prefill(q, k, v, mask, n_sink, window, out=out)  # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(bits(g_out), ref), f"graph replay {r}"
+        assert np.array_equal(bits(out), ref), f"eager call after replay {r}"
+
+
 @pytest.mark.parametrize("T,n_sink,window,step", [(1500, 4, 600, 20.0), (1100, 64, 300, 3.0), (700, 0, 1000, 40.0)])
 def test_rising_scores_raise_the_max_every_tile(T, n_sink, window, step):
     # Scores that grow along the sequence: key p carries (p / 64) * step
