@@ -668,18 +668,24 @@ __device__ __forceinline__ bool pp_work_item(const PrefillArgs& a, int rows, int
     // in turn; work item group j = (query block, sequence, KV head), heaviest
     // block first, holds the gs query heads that read the same K/V tiles.
     // Round m of 8 groups runs as gs consecutive workgroups on each XCD, so a
-    // group's tiles are fetched into one L2 once.  Even rounds deal the groups
-    // to XCDs 0..7, odd rounds to XCDs 7..0: the groups get lighter along the
-    // order, and alternating keeps each XCD's total work level (dealt in one
-    // direction, XCD 0 would take the heaviest group of every round).  The
-    // trailing groups that do not fill a round of 8 are dealt in plain order.
+    // group's tiles are fetched into one L2 once.  Groups get lighter along
+    // the order, so odd rounds deal them in reverse, which keeps each XCD's
+    // total work level (dealt one way, XCD 0 would take the heaviest group of
+    // every round).  When a round holds whole query blocks (the per-block
+    // group count divides 8) only the blocks' order is reversed: each XCD
+    // keeps serving one (sequence, KV head), whose causal prefix stays in its
+    // L2.  The trailing groups that do not fill a round of 8 are dealt in
+    // plain order.
     const int n_groups = a.n_qblocks * a.n_kv * a.B;
     const int full = 8 * a.gs * (n_groups / 8);
+    const int pq = a.n_kv * a.B;
     int j, hl;
     if (wg < full) {
       const int slot = wg >> 3;
       const int m = slot / a.gs;
-      j = 8 * m + ((m & 1) ? 7 - (wg & 7) : (wg & 7));
+      int x = wg & 7;
+      if (m & 1) x = (8 % pq == 0) ? (8 - pq) - (x - x % pq) + x % pq : 7 - x;
+      j = 8 * m + x;
       hl = slot % a.gs;
     } else {
       j = (full / a.gs) + (wg - full) / a.gs;
