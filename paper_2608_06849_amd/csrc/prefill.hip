@@ -1156,22 +1156,17 @@ __device__ __forceinline__ void prefill_pp_body(const PrefillArgs& a, int wg, PP
   }
 }
 
-template <bool STREAM, bool OUT_F32, bool APPEND>
-__global__ __launch_bounds__(512, 1) void prefill_pp_kernel(PrefillArgs a) {
-  __shared__ __align__(1024) PPRing ring;
-  prefill_pp_body<STREAM, OUT_F32, APPEND>(a, blockIdx.x, ring);
-}
-
-// Schedule of the streaming items of the one-launch form.  The XCDs run at
-// different speeds under this load (several percent apart), and the slowest
-// sets the end of a launch whose items are dealt to them in equal shares.
-// The retrieval items keep their static XCD-aware order; the light streaming
-// items at the end are taken dynamically: queue x holds the items the
-// XCD-aware order puts on XCD x (index w with w % 8 == x), a workgroup takes
-// the next item of the queue of the XCD it runs on (read from the XCC_ID
-// register) or, once that is empty, of another queue, and the launch has
-// kStreamSlack more streaming workgroups than items so that a fast XCD can
-// take over a slow one's share.  Workgroups that find every queue empty exit.
+// Dynamic tail of the d_head-128 launches.  The XCDs run at different speeds
+// under this load (several percent apart), and the slowest sets the end of a
+// launch whose items are dealt to them in equal shares.  The first items keep
+// their static XCD-aware order; the light items at the end (the streaming
+// items of the one-launch form, the second half of the items of a one-type
+// launch) are taken dynamically: queue x holds the items the XCD-aware order
+// puts on XCD x (index w with w % 8 == x), a workgroup takes the next item of
+// the queue of the XCD it runs on (read from the XCC_ID register) or, once
+// that is empty, of another queue, and the launch has kStreamSlack more
+// workgroups than tail items so that a fast XCD can take over a slow one's
+// share.  Workgroups that find every queue empty exit.
 // The queue counters live in one of kSchedSlots slots of a device array,
 // chosen per launch by the host; the last workgroup to take (or fail to take)
 // an item clears the slot.  Launches that run at the same time therefore
@@ -1214,40 +1209,76 @@ __device__ __forceinline__ int pp_grab(uint32_t* q, int n, int x) {
 // item spaces keep their XCD-aware order).  The light streaming items are
 // dispatched last and fill the CUs that the causal retrieval items leave
 // idle at the end.
-template <bool OUT_F32, bool APPEND>
-__global__ __launch_bounds__(512, 1) void prefill_pp_mixed_kernel(PrefillArgs ar, PrefillArgs as, int n_ret,
-                                                                  int ret_pad, int n_str, int n_dyn, int slot) {
-  __shared__ __align__(1024) PPRing ring;
+// One tail item for this workgroup (every thread gets it), or -1: n tail
+// items, n_dyn workgroups of the launch take part.  The last of them to take
+// (or fail to take) an item clears the slot.
+__device__ __forceinline__ int pp_take(int slot, int n, int n_dyn) {
   __shared__ int s_item;
-  const int wg = blockIdx.x;
-  if (wg < n_ret) {
-    prefill_pp_body<false, OUT_F32, APPEND>(ar, wg, ring);
-    return;
-  }
-  if (wg < ret_pad) return;
   uint32_t* q = g_pp_sched[slot];
   if (threadIdx.x == 0) {
-    s_item = pp_grab(q, n_str, pp_xcc());
+    s_item = pp_grab(q, n, pp_xcc());
     if (atomicAdd(&q[8], 1u) == (uint32_t)n_dyn - 1) {
 #pragma unroll
       for (int y = 0; y < 9; ++y) atomicExch(&q[y], 0u);
     }
   }
   __syncthreads();
-  const int w = __builtin_amdgcn_readfirstlane(s_item);
+  return __builtin_amdgcn_readfirstlane(s_item);
+}
+
+// One head type: workgroups [0, n_static) take items [0, n_static) in the
+// XCD-aware order, the n_dyn others the tail items [n_static, n_static + n_tail).
+template <bool STREAM, bool OUT_F32, bool APPEND>
+__global__ __launch_bounds__(512, 1) void prefill_pp_kernel(PrefillArgs a, int n_static, int n_tail, int n_dyn,
+                                                            int slot) {
+  __shared__ __align__(1024) PPRing ring;
+  int w = blockIdx.x;
+  if (w >= n_static) {
+    w = pp_take(slot, n_tail, n_dyn);
+    if (w < 0) return;
+    w += n_static;
+  }
+  prefill_pp_body<STREAM, OUT_F32, APPEND>(a, w, ring);
+}
+
+// Both head types of a layer in one launch: workgroups [0, n_ret) take the
+// retrieval items, [ret_pad, ret_pad + n_dyn) the n_str streaming ones
+// through the queues (ret_pad = n_ret rounded up to the 8 XCDs, so both item
+// spaces keep their XCD-aware order).  The light streaming items are
+// dispatched last and fill the CUs that the causal retrieval items leave
+// idle at the end.
+template <bool OUT_F32, bool APPEND>
+__global__ __launch_bounds__(512, 1) void prefill_pp_mixed_kernel(PrefillArgs ar, PrefillArgs as, int n_ret,
+                                                                  int ret_pad, int n_str, int n_dyn, int slot) {
+  __shared__ __align__(1024) PPRing ring;
+  const int wg = blockIdx.x;
+  if (wg < n_ret) {
+    prefill_pp_body<false, OUT_F32, APPEND>(ar, wg, ring);
+    return;
+  }
+  if (wg < ret_pad) return;
+  const int w = pp_take(slot, n_str, n_dyn);
   if (w >= 0) prefill_pp_body<true, OUT_F32, APPEND>(as, w, ring);
 }
 
 static std::atomic<uint32_t> g_sched_next{0};
+static int pp_slot() { return (int)(g_sched_next.fetch_add(1, std::memory_order_relaxed) % kSchedSlots); }
+// Workgroups that take part in a dynamic tail of n items.
+static int pp_n_dyn(int n) { return (int)((1.f + kStreamSlack) * n / 8 + 1) * 8; }
 
 template <int D, bool STREAM, bool OUT_F32>
 static hipError_t launch_bf16(const PrefillArgs& a, hipStream_t s) {
   const int grid = a.n_qblocks * a.n_kv * a.gs * a.B;
   if constexpr (D == kPPD) {
+    // the first half of the items (a multiple of 8) static, the rest dynamic
+    const int n_static = grid / 16 * 8, n_tail = grid - n_static, n_dyn = pp_n_dyn(n_tail);
+    const int slot = pp_slot();
     if (a.append)
-      hipLaunchKernelGGL((prefill_pp_kernel<STREAM, OUT_F32, true>), dim3(grid), dim3(512), 0, s, a);
+      hipLaunchKernelGGL((prefill_pp_kernel<STREAM, OUT_F32, true>), dim3(n_static + n_dyn), dim3(512), 0, s, a,
+                         n_static, n_tail, n_dyn, slot);
     else
-      hipLaunchKernelGGL((prefill_pp_kernel<STREAM, OUT_F32, false>), dim3(grid), dim3(512), 0, s, a);
+      hipLaunchKernelGGL((prefill_pp_kernel<STREAM, OUT_F32, false>), dim3(n_static + n_dyn), dim3(512), 0, s, a,
+                         n_static, n_tail, n_dyn, slot);
   } else {
     if (a.append)
       hipLaunchKernelGGL((prefill_bf16_kernel<D, STREAM, OUT_F32, true>), dim3(grid), dim3(kWaves * kWave), 0, s, a);
@@ -1281,8 +1312,8 @@ hipError_t launch_prefill_mixed(const PrefillArgs& ar, const PrefillArgs& as, in
   const int n_ret = ar.n_qblocks * ar.n_kv * ar.gs * ar.B;
   const int n_str = as.n_qblocks * as.n_kv * as.gs * as.B;
   const int ret_pad = (n_ret + 7) / 8 * 8;
-  const int n_dyn = (int)((1.f + kStreamSlack) * n_str / 8 + 1) * 8;
-  const int slot = (int)(g_sched_next.fetch_add(1, std::memory_order_relaxed) % kSchedSlots);
+  const int n_dyn = pp_n_dyn(n_str);
+  const int slot = pp_slot();
   const dim3 grid(ret_pad + n_dyn), blk(512);
   const bool app = ar.append;
   auto go = [&](auto kern) {
