@@ -125,9 +125,9 @@ DECODE_SOURCES = ("decode.hip", "aoh_device.h", "aoh_internal.h")
 TRAFFIC = {
     "fetch_factor": 524301.2 / 1048576.0,   # FETCH_SIZE of a 1 GiB copy / 1 GiB
     "write_factor": 1048576.0 / 1048576.0,  # WRITE_SIZE of a 1 GiB copy / 1 GiB
-    "prefill_mixed": {"fetch_kib": 458275.0, "write_kib": 263242.4,
-                      "sources": PREFILL_SOURCES, "source_hash": "cdc3e753b85ee5e0"},
-    "decode_ws": {"fetch_kib": 1081754.2, "write_kib": 1169.9,
+    "prefill_mixed": {"fetch_kib": 461597.2, "write_kib": 263393.8,
+                      "sources": PREFILL_SOURCES, "source_hash": "154d329fa4c197b3"},
+    "decode_ws": {"fetch_kib": 1081565.0, "write_kib": 1169.9,
                   "sources": DECODE_SOURCES, "source_hash": "21a01592fbd3549f"},
 }
 
