@@ -615,7 +615,9 @@ __global__ __launch_bounds__(kPrefillRowsF32) void prefill_f32_kernel(PrefillArg
 //  * The fused cache append writes the block's own (diagonal) tiles after
 //    the loop, from the ring, which still holds them.
 //  * Workgroups are ordered so that the query heads of one KV group and query
-//    block run on the same XCD (one L2).
+//    block run on the same XCD (one L2); the light items at the end of a
+//    launch are taken from per-XCD work queues, so that faster XCDs take over
+//    part of the slower ones' share.
 constexpr int kPPStages = 4;  // slots of the K and V rings
 constexpr int kPPD = 128;
 constexpr int kPPRows = kPrefillRows;     // query rows per workgroup (8 waves x 32)
